@@ -1,0 +1,102 @@
+// api.hip -- extern "C" entry points of libsnls.so (declared in
+// include/snls.h).  Each call validates its arguments on the host, then
+// launches the kernels on the caller's stream.  Nothing is allocated and no
+// state is kept between calls.
+#include <cmath>
+
+#include "snls_internal.h"
+
+using namespace snls;
+
+namespace {
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// Device present and usable (the first HIP call of a process may fail here
+// on a machine without a GPU).
+snls_status device_ready() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
+    (void)hipGetLastError();
+    return SNLS_ERR_HIP;
+  }
+  return SNLS_OK;
+}
+
+size_t backward_ws_bytes(const Geo& g) { return (size_t)g.rows * (size_t)g.k * sizeof(float); }
+
+}  // namespace
+
+extern "C" {
+
+int snls_abi_version(void) { return SNLS_ABI_VERSION; }
+
+const char* snls_status_string(snls_status s) {
+  switch (s) {
+    case SNLS_OK: return "ok";
+    case SNLS_ERR_INVALID_ARG: return "invalid argument";
+    case SNLS_ERR_UNSUPPORTED: return "unsupported parameters";
+    case SNLS_ERR_HIP: return "HIP runtime error";
+    case SNLS_ERR_WORKSPACE: return "workspace missing or too small";
+  }
+  return "unknown status";
+}
+
+size_t snls_workspace_size(int op, const snls_params* p) {
+  Geo g;
+  if (op == SNLS_OP_SEARCH) return check_params(p, false, &g) == SNLS_OK ? 0 : (size_t)-1;
+  if (op == SNLS_OP_AGGREGATE) return check_params(p, true, &g) == SNLS_OK ? 0 : (size_t)-1;
+  if (op == SNLS_OP_BACKWARD) return check_params(p, true, &g) == SNLS_OK ? backward_ws_bytes(g) : (size_t)-1;
+  return (size_t)-1;
+}
+
+snls_status snls_search(const float* q, const float* k, const float* flows, const snls_params* p, float* dists,
+                        float* inds, void* stream) {
+  Geo g;
+  snls_status st = check_params(p, false, &g);
+  if (st != SNLS_OK) return st;
+  if (!q || !k || !dists || !inds || (g.wt > 0 && !flows)) return SNLS_ERR_INVALID_ARG;
+  if ((st = device_ready()) != SNLS_OK) return st;
+  if (g.k == 0) return launch_search_full(q, k, flows, g, dists, inds, as_stream(stream));
+  return launch_search_topk(q, k, flows, g, dists, inds, as_stream(stream));
+}
+
+snls_status snls_topk(const float* dists_all, const float* inds_all, int64_t rows, int32_t n_cand, int32_t k,
+                      int32_t dist_type, float* dists, float* inds, void* stream) {
+  snls_status st = check_topk_args(rows, n_cand, k, dist_type);
+  if (st != SNLS_OK) return st;
+  if (!dists_all || !inds_all || !dists || !inds) return SNLS_ERR_INVALID_ARG;
+  if ((st = device_ready()) != SNLS_OK) return st;
+  return launch_topk(dists_all, inds_all, rows, n_cand, k, dist_type, dists, inds, as_stream(stream));
+}
+
+snls_status snls_aggregate(const float* v, const float* dists, const float* inds, const snls_params* p,
+                           float scale, float* out, void* stream) {
+  Geo g;
+  snls_status st = check_params(p, true, &g);
+  if (st != SNLS_OK) return st;
+  if (!v || !dists || !inds || !out || !std::isfinite(scale)) return SNLS_ERR_INVALID_ARG;
+  if ((st = device_ready()) != SNLS_OK) return st;
+  return launch_aggregate(v, dists, inds, g, scale, out, as_stream(stream));
+}
+
+snls_status snls_backward(const float* q, const float* k, const float* v, const float* flows, const float* dists,
+                          const float* inds, const float* grad_out, const float* grad_dists, const snls_params* p,
+                          float scale, float* grad_q, float* grad_k, float* grad_v, float* grad_flows,
+                          void* workspace, size_t workspace_bytes, void* stream) {
+  Geo g;
+  snls_status st = check_params(p, true, &g);
+  if (st != SNLS_OK) return st;
+  (void)flows;  // positions come from inds; d disp / d flow = 1
+  if (!q || !k || !v || !dists || !inds || !grad_out || !grad_q || !grad_k || !grad_v) return SNLS_ERR_INVALID_ARG;
+  if (g.wt > 0 && !grad_flows) return SNLS_ERR_INVALID_ARG;
+  if (!std::isfinite(scale)) return SNLS_ERR_INVALID_ARG;
+  size_t need = backward_ws_bytes(g);
+  if (need > 0 && (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)))
+    return SNLS_ERR_WORKSPACE;
+  if ((st = device_ready()) != SNLS_OK) return st;
+  return launch_backward(q, k, v, dists, inds, grad_out, grad_dists, g, scale, grad_q, grad_k, grad_v, grad_flows,
+                         static_cast<float*>(workspace), as_stream(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,188 @@
+// search_direct.hip -- direct shifted non-local search kernels (Sec. 3.2):
+// each thread scores candidates straight from the video tensors with
+// bilinear reads (the in-place computation of Sec. 3.4), for any parameter
+// combination.  k == 0 writes every candidate; k >= 1 keeps the top-k per
+// query row in registers.  These kernels are the general path; the tiled
+// kernel in search_tile.hip covers the common S_Q = S_K = 1 case faster.
+#include "snls_internal.h"
+
+namespace snls {
+
+// Decoded query row (b, hd, t, h, w) of a flattened row index over
+// (B, HD, T, nH, nW).
+struct QueryPos {
+  int b, hd, t, h, w;
+};
+
+SNLS_DEV QueryPos decode_row(long long row, const Geo& g) {
+  QueryPos qp;
+  int mw = (int)(row % g.nW);
+  row /= g.nW;
+  int mh = (int)(row % g.nH);
+  row /= g.nH;
+  qp.t = (int)(row % g.T);
+  row /= g.T;
+  qp.hd = (int)(row % g.HD);
+  qp.b = (int)(row / g.HD);
+  qp.h = mh * g.s0;
+  qp.w = mw * g.s0;
+  return qp;
+}
+
+// Window offset F of frame step dt at the query pixel (zero for dt == 0).
+SNLS_DEV void read_shift(const float* __restrict__ flows, const Geo& g, const QueryPos& qp, int dt, float* fh,
+                         float* fw) {
+  if (dt == 0) {
+    *fh = 0.f;
+    *fw = 0.f;
+    return;
+  }
+  long long base = (((long long)qp.b * g.T + qp.t) * g.nslot + flow_slot(dt, g.wt)) * 2;
+  long long pix = (long long)qp.h * g.W + qp.w;
+  *fh = flows[base * g.HW + pix];
+  *fw = flows[(base + 1) * g.HW + pix];
+}
+
+// Patch similarity of a valid candidate with displacement (disp_h, disp_w)
+// in frame t2 (inner product or squared L2 over in-frame query pixels and
+// the head's channels).
+SNLS_DEV float score_candidate(const float* __restrict__ q, const float* __restrict__ k, const Geo& g,
+                               const QueryPos& qp, int t2, float disp_h, float disp_w) {
+  int nh, nw;
+  float ah, aw;
+  split_disp(disp_h, &nh, &ah);
+  split_disp(disp_w, &nw, &aw);
+  const float* qbase = q + (((long long)qp.b * g.T + qp.t) * g.C + (long long)qp.hd * g.Ch) * g.HW;
+  const float* kbase = k + (((long long)qp.b * g.T + t2) * g.C + (long long)qp.hd * g.Ch) * g.HW;
+  float acc = 0.f;
+  for (int ph = g.lo; ph < g.lo + g.ps; ++ph) {
+    int y = qp.h + ph;
+    if (y < 0 || y >= g.H) continue;
+    for (int pw = g.lo; pw < g.lo + g.ps; ++pw) {
+      int x = qp.w + pw;
+      if (x < 0 || x >= g.W) continue;
+      for (int c = 0; c < g.Ch; ++c) {
+        float qv = qbase[c * g.HW + (long long)y * g.W + x];
+        float kv = bilinear_plane(kbase + c * g.HW, g.H, g.W, y + nh, x + nw, ah, aw);
+        if (g.dist == SNLS_DIST_PROD) {
+          acc = fmaf(qv, kv, acc);
+        } else {
+          float e = qv - kv;
+          acc = fmaf(e, e, acc);
+        }
+      }
+    }
+  }
+  return acc;
+}
+
+// One thread per (query row, candidate): every candidate in id order.
+__global__ void __launch_bounds__(256) search_full_kernel(const float* __restrict__ q, const float* __restrict__ k,
+                                                          const float* __restrict__ flows, Geo g,
+                                                          float* __restrict__ dists, float* __restrict__ inds) {
+  long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= g.rows * g.ncand) return;
+  int cid = (int)(gid % g.ncand);
+  QueryPos qp = decode_row(gid / g.ncand, g);
+  int dw = cid % g.ws;
+  int dh = (cid / g.ws) % g.ws;
+  int dt = cid / (g.ws * g.ws) - g.wt;
+  float fh, fw;
+  read_shift(flows, g, qp, dt, &fh, &fw);
+  float disp_h = cand_disp(fh, g.s1, dh, g.r);
+  float disp_w = cand_disp(fw, g.s1, dw, g.r);
+  int t2 = qp.t + dt;
+  bool ok = t2 >= 0 && t2 < g.T && centre_ok(qp.h, disp_h, g.H) && centre_ok(qp.w, disp_w, g.W);
+  float d = ok ? score_candidate(q, k, g, qp, t2, disp_h, disp_w) : from_score(-INFINITY, g.dist);
+  dists[gid] = d;
+  inds[3 * gid + 0] = (float)t2;
+  inds[3 * gid + 1] = disp_h;
+  inds[3 * gid + 2] = disp_w;
+}
+
+// One thread per query row: all candidates, top-k kept in registers.
+template <int KMAX>
+__global__ void __launch_bounds__(128) search_topk_direct_kernel(const float* __restrict__ q,
+                                                                 const float* __restrict__ k,
+                                                                 const float* __restrict__ flows, Geo g,
+                                                                 float* __restrict__ dists,
+                                                                 float* __restrict__ inds) {
+  long long row = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= g.rows) return;
+  QueryPos qp = decode_row(row, g);
+  TopList<KMAX> lst;
+  lst.init();
+  for (int dt = -g.wt; dt <= g.wt; ++dt) {
+    int t2 = qp.t + dt;
+    if (t2 < 0 || t2 >= g.T) continue;  // frame outside the clip: never selected ahead of a valid one
+    float fh, fw;
+    read_shift(flows, g, qp, dt, &fh, &fw);
+    for (int dh = 0; dh < g.ws; ++dh) {
+      float disp_h = cand_disp(fh, g.s1, dh, g.r);
+      bool okh = centre_ok(qp.h, disp_h, g.H);
+      for (int dw = 0; dw < g.ws; ++dw) {
+        float disp_w = cand_disp(fw, g.s1, dw, g.r);
+        int cid = ((dt + g.wt) * g.ws + dh) * g.ws + dw;
+        float sc = -INFINITY;
+        if (okh && centre_ok(qp.w, disp_w, g.W)) sc = to_score(score_candidate(q, k, g, qp, t2, disp_h, disp_w), g.dist);
+        lst.push(sc, cid, g.k);
+      }
+    }
+  }
+  // Rows with fewer than k valid candidates are completed with the invalid
+  // candidates of smallest id (frames outside the clip included), matching
+  // a full sort of all candidates.
+  for (int dt = -g.wt; dt <= g.wt; ++dt) {
+    int t2 = qp.t + dt;
+    if (t2 >= 0 && t2 < g.T) continue;
+    for (int c = 0; c < g.ws * g.ws; ++c) lst.push(-INFINITY, (dt + g.wt) * g.ws * g.ws + c, g.k);
+  }
+  float* drow = dists + row * g.k;
+  float* irow = inds + row * g.k * 3;
+#pragma unroll
+  for (int i = 0; i < KMAX; ++i) {
+    if (i < g.k) {
+      int cid = lst.id[i];
+      int dw = cid % g.ws;
+      int dh = (cid / g.ws) % g.ws;
+      int dt = cid / (g.ws * g.ws) - g.wt;
+      float fh, fw;
+      read_shift(flows, g, qp, dt, &fh, &fw);
+      drow[i] = from_score(lst.s[i], g.dist);
+      irow[3 * i + 0] = (float)(qp.t + dt);
+      irow[3 * i + 1] = cand_disp(fh, g.s1, dh, g.r);
+      irow[3 * i + 2] = cand_disp(fw, g.s1, dw, g.r);
+    }
+  }
+}
+
+snls_status launch_search_full(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
+                               float* inds, hipStream_t s) {
+  long long total = g.rows * g.ncand;
+  if (total == 0) return SNLS_OK;
+  long long blocks = (total + 255) / 256;
+  hipLaunchKernelGGL(search_full_kernel, dim3((unsigned)blocks), dim3(256), 0, s, q, k, flows, g, dists, inds);
+  return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+}
+
+snls_status launch_search_topk_direct(const float* q, const float* k, const float* flows, const Geo& g,
+                                      float* dists, float* inds, hipStream_t s) {
+  if (g.rows == 0) return SNLS_OK;
+  unsigned blocks = (unsigned)((g.rows + 127) / 128);
+  if (g.k <= 16)
+    hipLaunchKernelGGL(search_topk_direct_kernel<16>, dim3(blocks), dim3(128), 0, s, q, k, flows, g, dists, inds);
+  else if (g.k <= 32)
+    hipLaunchKernelGGL(search_topk_direct_kernel<32>, dim3(blocks), dim3(128), 0, s, q, k, flows, g, dists, inds);
+  else if (g.k <= 64)
+    hipLaunchKernelGGL(search_topk_direct_kernel<64>, dim3(blocks), dim3(128), 0, s, q, k, flows, g, dists, inds);
+  else
+    hipLaunchKernelGGL(search_topk_direct_kernel<128>, dim3(blocks), dim3(128), 0, s, q, k, flows, g, dists, inds);
+  return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+}
+
+snls_status launch_search_topk(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
+                               float* inds, hipStream_t s) {
+  return launch_search_topk_direct(q, k, flows, g, dists, inds, s);
+}
+
+}  // namespace snls

@@ -1,0 +1,151 @@
+// snls_internal.h -- shared definitions of the HIP implementation (not part
+// of the public ABI).
+//
+// Geometry and conventions follow the paper's Sec. 3.1-3.2 as restated in
+// include/snls.h: query grid with stride S_Q, Ws x Ws window cells at
+// displacement F + S_K*(d - Ws/2) in each of the W_t = 2wt+1 frames,
+// P x P patches at offsets -(P/2) .. P-1-(P/2), bilinear reads with zero
+// outside the frame.
+#pragma once
+
+#include <stdint.h>
+#include "../../include/snls.h"
+
+#ifdef __HIPCC__
+#include <hip/hip_runtime.h>
+#endif
+
+namespace snls {
+
+// Derived geometry of one call, passed to kernels by value.
+struct Geo {
+  int B, T, C, H, W, HD;
+  int ws, wt, ps, s0;
+  float s1;
+  int k, dist;
+  int nH, nW, Ch, r, lo, ncand, nslot;
+  long long HW;    // H*W
+  long long rows;  // B*HD*T*nH*nW query rows
+};
+
+// Host-side checks (validate.cpp).  Return SNLS_OK or an error code; they
+// never touch the GPU.
+snls_status check_params(const snls_params* p, bool need_k, Geo* g);
+snls_status check_topk_args(int64_t rows, int32_t n_cand, int32_t k, int32_t dist_type);
+
+#ifdef __HIPCC__
+
+// Launchers (one per kernel family); all return SNLS_OK or SNLS_ERR_HIP.
+snls_status launch_search_full(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
+                               float* inds, hipStream_t s);
+snls_status launch_search_topk(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
+                               float* inds, hipStream_t s);
+snls_status launch_topk(const float* dall, const float* iall, int64_t rows, int ncand, int k, int dist,
+                        float* dists, float* inds, hipStream_t s);
+snls_status launch_aggregate(const float* v, const float* dists, const float* inds, const Geo& g, float scale,
+                             float* out, hipStream_t s);
+snls_status launch_backward(const float* q, const float* k, const float* v, const float* dists, const float* inds,
+                            const float* grad_out, const float* grad_dists, const Geo& g, float scale,
+                            float* grad_q, float* grad_k, float* grad_v, float* grad_flows, float* Gws,
+                            hipStream_t s);
+
+// ---------------------------------------------------------------- device --
+
+#define SNLS_DEV __device__ __forceinline__
+
+// Candidate displacement disp = fl32(F + fl32(S_K * (d - r))), rounded once
+// per operation (no contraction), the fp32 convention of the outputs.
+SNLS_DEV float cand_disp(float F, float s1, int d, int r) { return __fadd_rn(F, __fmul_rn(s1, (float)(d - r))); }
+
+// Centre (h + disp) inside [0, H-1]; exact: -h and H-1-h are exact in fp32.
+SNLS_DEV bool centre_ok(int h, float disp, int H) { return disp >= (float)(-h) && disp <= (float)(H - 1 - h); }
+
+// Neighbour slot of a frame step dt != 0 (dt = -wt..-1 -> 0..wt-1, 1..wt -> wt..2wt-1).
+SNLS_DEV int flow_slot(int dt, int wt) { return dt < 0 ? dt + wt : dt + wt - 1; }
+
+// Score with "larger is better" for both distances: s = d (inner product),
+// s = -d (L2).  Invalid candidates map to -inf either way.
+SNLS_DEV float to_score(float d, int dist) { return dist == SNLS_DIST_PROD ? d : -d; }
+SNLS_DEV float from_score(float s, int dist) { return dist == SNLS_DIST_PROD ? s : -s; }
+
+// (s1, id1) ranks before (s2, id2): larger score, ties to the smaller id.
+SNLS_DEV bool ranks_before(float s1, int id1, float s2, int id2) { return s1 > s2 || (s1 == s2 && id1 < id2); }
+
+// Bilinear read of one channel plane at integer corner (y0, x0) with
+// fractional weights (ay, ax); taps outside the frame read 0.
+SNLS_DEV float bilinear_plane(const float* __restrict__ plane, int H, int W, int y0, int x0, float ay, float ax) {
+  const bool y0in = y0 >= 0 && y0 < H, y1in = y0 + 1 >= 0 && y0 + 1 < H;
+  const bool x0in = x0 >= 0 && x0 < W, x1in = x0 + 1 >= 0 && x0 + 1 < W;
+  const long long o = (long long)y0 * W + x0;
+  float v00 = (y0in && x0in) ? plane[o] : 0.f;
+  float v01 = (y0in && x1in) ? plane[o + 1] : 0.f;
+  float v10 = (y1in && x0in) ? plane[o + W] : 0.f;
+  float v11 = (y1in && x1in) ? plane[o + W + 1] : 0.f;
+  float top = (1.f - ax) * v00 + ax * v01;
+  float bot = (1.f - ax) * v10 + ax * v11;
+  return (1.f - ay) * top + ay * bot;
+}
+
+// Split a displacement into integer part and fraction (disp = n + a, a in [0,1)).
+SNLS_DEV void split_disp(float disp, int* n, float* a) {
+  float f = floorf(disp);
+  *n = (int)f;
+  *a = disp - f;
+}
+
+// Number of query patches covering pixel coordinate y along one axis: grid
+// positions m*S (0 <= m < n) with y - m*S in [lo, lo+P-1].
+SNLS_DEV int cover_count_1d(int y, int S, int n, int lo, int P) {
+  int a = y - lo - P + 1;  // m*S >= a
+  int b = y - lo;          // m*S <= b
+  if (b < 0) return 0;
+  int mmin = a <= 0 ? 0 : (a + S - 1) / S;
+  int mmax = b / S;
+  if (mmax > n - 1) mmax = n - 1;
+  return mmax >= mmin ? mmax - mmin + 1 : 0;
+}
+
+// Sorted top-K list in registers, best first.  KMAX is the capacity; only
+// the first k entries are kept meaningful, the threshold test uses entry k-1.
+template <int KMAX>
+struct TopList {
+  float s[KMAX];
+  int id[KMAX];
+  float thr_s;  // score of entry k-1
+  int thr_id;
+
+  SNLS_DEV void init() {
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) {
+      s[i] = -INFINITY;
+      id[i] = 0x7fffffff;
+    }
+    thr_s = -INFINITY;
+    thr_id = 0x7fffffff;
+  }
+  // Insert (sc, cid) if it ranks before the current k-th entry.
+  SNLS_DEV void push(float sc, int cid, int k) {
+    if (!ranks_before(sc, cid, thr_s, thr_id)) return;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) {
+      bool sw = ranks_before(sc, cid, s[i], id[i]);
+      float ts = s[i];
+      int ti = id[i];
+      s[i] = sw ? sc : ts;
+      id[i] = sw ? cid : ti;
+      sc = sw ? ts : sc;
+      cid = sw ? ti : cid;
+    }
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) {
+      if (i == k - 1) {
+        thr_s = s[i];
+        thr_id = id[i];
+      }
+    }
+  }
+};
+
+#endif  // __HIPCC__
+
+}  // namespace snls

@@ -1,0 +1,121 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/snls.h declares, and rejects invalid arguments with the documented
+status codes before touching any buffer or the device."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+from paper_2309_16849_amd import snls as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "snls.h")
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(snls_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return B.load_library()
+
+
+def _params(**kw):
+    p = dict(B=1, T=3, C=8, H=16, W=17, HD=2, ws=3, wt=1, ps=3, stride0=1, stride1=1.0, k=4, dist_type=0)
+    p.update(kw)
+    return B.params_from_dict(p)
+
+
+def test_exports_every_declared_function(lib):
+    names = _declared_functions()
+    assert set(names) == set(B.SYMBOLS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_abi_version_and_status_strings(lib):
+    assert B.snls_abi_version() == 1
+    assert B.snls_status_string(0) == "ok"
+    for s in range(1, 5):
+        assert B.snls_status_string(s) not in ("ok", "unknown status")
+    assert B.snls_status_string(99) == "unknown status"
+    assert ctypes.sizeof(B.SnlsParams) == 4 * 14  # 14 four-byte fields, no padding
+
+
+BAD_PARAMS = [
+    dict(ws=0), dict(ps=0), dict(wt=-1), dict(stride0=0), dict(stride1=0.0), dict(stride1=-1.0),
+    dict(stride1=float("nan")), dict(C=9, HD=2), dict(HD=0), dict(B=0), dict(T=0), dict(H=0), dict(W=0),
+    dict(dist_type=2), dict(k=-1), dict(k=28),  # k > (2wt+1)*ws^2 = 27
+]
+
+
+@pytest.mark.parametrize("kw", BAD_PARAMS, ids=[str(k) for k in BAD_PARAMS])
+def test_search_rejects_bad_params(lib, kw):
+    prm = _params(**kw)
+    st = lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, None)
+    assert st == B.SNLS_ERR_INVALID_ARG
+
+
+def test_search_rejects_bad_struct_size_and_nulls(lib):
+    prm = _params()
+    prm.struct_size = 12
+    assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    prm = _params()
+    assert lib.snls_search(FAKE, FAKE, FAKE, None, FAKE, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    for i in range(5):
+        args = [FAKE] * 5
+        args[i] = None
+        q, k, fl, d, ind = args
+        assert lib.snls_search(q, k, fl, ctypes.byref(prm), d, ind, None) == B.SNLS_ERR_INVALID_ARG
+    # flows may be NULL when wt == 0: the call then passes validation (checked below without a device)
+
+
+def test_k_limits(lib):
+    prm = _params(ws=15, wt=1, k=B.SNLS_MAX_K + 1)
+    assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, None) == B.SNLS_ERR_UNSUPPORTED
+    assert lib.snls_topk(FAKE, FAKE, 10, 500, B.SNLS_MAX_K + 1, 0, FAKE, FAKE, None) == B.SNLS_ERR_UNSUPPORTED
+    for rows, nc, k, dt in ((-1, 10, 2, 0), (5, 0, 1, 0), (5, 10, 0, 0), (5, 10, 11, 0), (5, 10, 2, 3)):
+        assert lib.snls_topk(FAKE, FAKE, rows, nc, k, dt, FAKE, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_topk(None, FAKE, 5, 10, 2, 0, FAKE, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+
+
+def test_aggregate_and_backward_validation(lib):
+    prm = _params(k=0)  # aggregation needs k >= 1
+    assert lib.snls_aggregate(FAKE, FAKE, FAKE, ctypes.byref(prm), 1.0, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    prm = _params()
+    assert lib.snls_aggregate(FAKE, FAKE, FAKE, ctypes.byref(prm), float("inf"), FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_aggregate(FAKE, None, FAKE, ctypes.byref(prm), 1.0, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    need = lib.snls_workspace_size(B.SNLS_OP_BACKWARD, ctypes.byref(prm))
+    nq = 1 * 2 * 3 * 16 * 17
+    assert need == nq * 4 * 4
+    args = [FAKE] * 8
+    st = lib.snls_backward(*args, ctypes.byref(prm), 1.0, FAKE, FAKE, FAKE, FAKE, None, 0, None)
+    assert st == B.SNLS_ERR_WORKSPACE
+    st = lib.snls_backward(*args, ctypes.byref(prm), 1.0, FAKE, FAKE, FAKE, FAKE, ctypes.c_void_p(0x1104), need,
+                           None)
+    assert st == B.SNLS_ERR_WORKSPACE  # not 256-byte aligned
+    st = lib.snls_backward(*args, ctypes.byref(prm), 1.0, FAKE, FAKE, FAKE, None, FAKE, need, None)
+    assert st == B.SNLS_ERR_INVALID_ARG  # grad_flows required when wt > 0
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(prm)) == 0
+    assert lib.snls_workspace_size(7, ctypes.byref(prm)) == ctypes.c_size_t(-1).value
+    bad = _params(ws=0)
+    assert lib.snls_workspace_size(B.SNLS_OP_BACKWARD, ctypes.byref(bad)) == ctypes.c_size_t(-1).value
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device error path")
+def test_valid_call_without_device_reports_hip_error(lib):
+    prm = _params(wt=0)
+    assert lib.snls_search(FAKE, FAKE, None, ctypes.byref(prm), FAKE, FAKE, None) == B.SNLS_ERR_HIP
+
+
+def test_binding_refuses_cpu_tensors():
+    p = dict(B=1, T=1, C=2, H=4, W=4, HD=1, ws=3, wt=0, ps=1, stride0=1, stride1=1.0, k=2, dist_type=0)
+    x = torch.zeros(1, 1, 2, 4, 4)
+    with pytest.raises(ValueError):
+        B.snls_search(x, x, None, p)

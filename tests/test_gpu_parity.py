@@ -1,0 +1,284 @@
+"""Parity of the HIP library against the oracle on the same seeded inputs.
+
+Small cases are compared element by element over whole outputs; the five
+workloads at their full sizes are compared on sampled query rows and output
+pixels that the oracle evaluates one by one.  Tolerances: see tests/parity.py.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2309_16849_amd import snls as B
+from tests.parity import REL, assert_close, compare_topk, rms_finite
+from workloads import config_params, make_config, small_params
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load_library()
+    return torch.device("cuda:0")
+
+
+def _d(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+
+
+def _h(t):
+    return t.detach().cpu().numpy()
+
+
+def _inputs(p, seed, flow_kind="frac", shared_qk=False):
+    r = np.random.default_rng(seed)
+    shp = (p["B"], p["T"], p["C"], p["H"], p["W"])
+    q = r.standard_normal(shp, dtype=np.float32)
+    k = q.copy() if shared_qk else r.standard_normal(shp, dtype=np.float32)
+    v = r.standard_normal(shp, dtype=np.float32)
+    fshp = (p["B"], p["T"], 2 * p["wt"], 2, p["H"], p["W"])
+    if flow_kind == "frac":
+        flows = r.uniform(-3, 3, fshp).astype(np.float32)
+    elif flow_kind == "int":
+        flows = r.integers(-2, 3, fshp).astype(np.float32)
+    elif flow_kind == "far":
+        flows = (r.choice([-1.0, 1.0], fshp) * 60.0).astype(np.float32)
+    else:
+        raise ValueError(flow_kind)
+    return q, k, v, flows
+
+
+def _sweep_cases(n=22, seed=7):
+    r = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        ws = int(r.choice([1, 3, 5, 9]))
+        wt = int(r.choice([0, 1, 2]))
+        HD = int(r.choice([1, 2, 4]))
+        p = small_params(
+            B=int(r.choice([1, 2])), T=int(r.choice([1, 2, 3])), C=HD * int(r.choice([1, 3, 4])),
+            H=int(r.choice([1, 7, 33])), W=int(r.choice([1, 7, 33])), HD=HD, ws=ws, wt=wt,
+            ps=int(r.choice([1, 2, 3, 5])), stride0=int(r.choice([1, 2, 3])),
+            stride1=float(r.choice([1.0, 0.5])), dist_type=int(r.choice([0, 1])))
+        nc = (2 * wt + 1) * ws * ws
+        p["k"] = int(min(nc, r.choice([1, 4, 10, 33])))
+        kind = ["frac", "int", "far"][i % 3] if wt > 0 else "frac"
+        cases.append((p, kind, bool(i % 4 == 0)))
+    # fixed edge cases: frames shorter than the window, single pixel, big k
+    cases.append((small_params(T=1, wt=2, ws=3, k=9, H=5, W=6), "frac", False))
+    cases.append((small_params(T=2, H=1, W=1, ws=3, wt=1, ps=3, k=5), "frac", False))
+    cases.append((small_params(T=3, H=20, W=19, ws=7, wt=1, ps=1, k=100, C=4), "frac", False))
+    return cases
+
+
+CASES = _sweep_cases()
+IDS = ["c%d-ws%d-wt%d-ps%d-s%d-hd%d-%s" % (i, p["ws"], p["wt"], p["ps"], p["stride0"], p["HD"], kd)
+       for i, (p, kd, _) in enumerate(CASES)]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)), ids=IDS)
+def test_search_all_candidates(dev, case):
+    p, kind, shared = CASES[case]
+    p = dict(p, k=0)
+    q, k, v, flows = _inputs(p, 1000 + case, kind, shared)
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    torch.cuda.synchronize()
+    od, oi = oracle.search_all(q, k, flows, p)
+    gd, gi = _h(gd).reshape(od.shape), _h(gi).reshape(oi.shape)
+    assert np.array_equal(gi, oi.astype(np.float32)), "candidate positions differ"
+    assert_close(gd, od, "all-candidate scores")
+
+
+@pytest.mark.parametrize("case", range(len(CASES)), ids=IDS)
+def test_fused_search_topk(dev, case):
+    p, kind, shared = CASES[case]
+    q, k, v, flows = _inputs(p, 2000 + case, kind, shared)
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    torch.cuda.synchronize()
+    res = oracle.search(q, k, flows, p)
+    compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
+
+
+@pytest.mark.parametrize("case", range(0, len(CASES), 2), ids=IDS[::2])
+def test_standalone_topk(dev, case):
+    p, kind, shared = CASES[case]
+    q, k, v, flows = _inputs(p, 3000 + case, kind, shared)
+    ad, ai = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), dict(p, k=0))
+    gd, gi = B.snls_topk(ad, ai, p["k"], p["dist_type"])
+    torch.cuda.synchronize()
+    res = oracle.search(q, k, flows, p)
+    compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
+
+
+@pytest.mark.parametrize("case", range(len(CASES)), ids=IDS)
+def test_aggregate(dev, case):
+    p, kind, shared = CASES[case]
+    q, k, v, flows = _inputs(p, 4000 + case, kind, shared)
+    scale = 0.25
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    out = B.snls_aggregate(_d(v, dev), gd, gi, p, scale)
+    torch.cuda.synchronize()
+    gd_h, gi_h, out_h = _h(gd), _h(gi), _h(out)
+    # decoupled: the oracle aggregates the GPU's own neighbours
+    ref = oracle.aggregate(v, gd_h, gi_h, p, scale)
+    assert_close(out_h, ref, "aggregate (GPU neighbours)")
+    # end to end: the oracle's own neighbours, pixels of rows with near-tie swaps masked
+    res = oracle.search(q, k, flows, p)
+    _, swaps = compare_topk(gd_h.reshape(-1, p["k"]), gi_h.reshape(-1, p["k"], 3), res, p["k"])
+    nH, nW = oracle.grid(p)
+    shp = (p["B"], p["HD"], p["T"], nH, nW, p["k"])
+    ref2 = oracle.aggregate(v, res["dists"][:, :p["k"]].reshape(shp), res["inds"][:, :p["k"]].reshape(shp + (3,)),
+                            p, scale)
+    mask = _swap_mask(p, swaps.reshape(shp[:-1]))
+    assert_close(out_h[~mask], ref2[~mask], "aggregate (end to end)", scale=rms_finite(ref2))
+
+
+def _swap_mask(p, swaps):
+    """Output pixels covered by a query patch whose top-k had a near-tie swap."""
+    mask = np.zeros((p["B"], p["T"], p["C"], p["H"], p["W"]), bool)
+    lo = -(p["ps"] // 2)
+    for b, hd, t, mh, mw in zip(*np.nonzero(swaps)):
+        h, w = mh * p["stride0"], mw * p["stride0"]
+        mask[b, t, :, max(h + lo, 0):max(h + lo + p["ps"], 0), max(w + lo, 0):max(w + lo + p["ps"], 0)] = True
+    return mask
+
+
+def test_deterministic(dev):
+    p = small_params(T=3, C=8, H=33, W=33, HD=2, ws=5, wt=1, ps=3, k=7)
+    q, k, v, flows = _inputs(p, 5000)
+    a = [B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p) for _ in range(2)]
+    o = [B.snls_aggregate(_d(v, dev), a[0][0], a[0][1], p, 0.5) for _ in range(2)]
+    torch.cuda.synchronize()
+    assert torch.equal(a[0][0], a[1][0]) and torch.equal(a[0][1], a[1][1])
+    assert torch.equal(o[0], o[1])
+
+
+# ------------------------------------------------------------ workloads --
+
+_CFG_CACHE = {}
+
+
+def _cfg(idx):
+    if idx not in _CFG_CACHE:
+        _CFG_CACHE.clear()
+        _CFG_CACHE[idx] = make_config(idx)
+    return _CFG_CACHE[idx]
+
+
+def _sample_rows(p, n, rng):
+    nH, nW = oracle.grid(p)
+    rows = []
+    for b in range(p["B"]):
+        for hd in range(p["HD"]):
+            for t in range(p["T"]):
+                for mh, mw in ((0, 0), (0, nW - 1), (nH - 1, 0), (nH - 1, nW - 1), (nH // 2, 0), (0, nW // 2)):
+                    rows.append((((b * p["HD"] + hd) * p["T"] + t) * nH + mh) * nW + mw)
+    total = oracle.n_queries(p)
+    rows += list(rng.choice(total, size=min(n, total), replace=False))
+    return np.unique(np.array(rows, np.int64))
+
+
+def _covering_rows(p, pix):
+    nH, nW = oracle.grid(p)
+    lo, S = -(p["ps"] // 2), p["stride0"]
+    rows = set()
+    for pi in pix:
+        x = pi % p["W"]
+        y = (pi // p["W"]) % p["H"]
+        t = (pi // (p["W"] * p["H"])) % p["T"]
+        b = pi // (p["W"] * p["H"] * p["T"])
+        for ph in range(lo, lo + p["ps"]):
+            for pw in range(lo, lo + p["ps"]):
+                h, w = y - ph, x - pw
+                if h < 0 or w < 0 or h % S or w % S or h // S >= nH or w // S >= nW:
+                    continue
+                for hd in range(p["HD"]):
+                    rows.add((((b * p["HD"] + hd) * p["T"] + t) * nH + h // S) * nW + w // S)
+    return np.array(sorted(rows), np.int64)
+
+
+@pytest.mark.parametrize("idx", [0, 1, 2, 3, 4])
+def test_workload_parity(dev, idx):
+    """Search + top-k + aggregation of each workload at its full size (the
+    launch configuration bench.py times), on sampled rows and pixels."""
+    c = _cfg(idx)
+    p, scale = c["params"], c["scale"]
+    print("workload %d (%s) %s" % (idx, c["name"], p), flush=True)
+    rng = np.random.default_rng(77 + idx)
+    qd, fd = _d(c["q"], dev), _d(c["flows"], dev)
+    gd, gi = B.snls_search(qd, qd, fd, p)
+    out = B.snls_aggregate(qd, gd, gi, p, scale)
+    torch.cuda.synchronize()
+    kk = p["k"]
+    gd_h, gi_h, out_h = _h(gd).reshape(-1, kk), _h(gi).reshape(-1, kk, 3), _h(out)
+    assert np.isfinite(out_h).all()
+    # search + top-k on sampled rows
+    rows = _sample_rows(p, 400 if idx else 4000, rng)
+    res = oracle.search(c["q"], c["k"], c["flows"], p, qids=rows)
+    n_sw, _ = compare_topk(gd_h[rows], gi_h[rows], res, kk, scale=rms_finite(gd_h))
+    print("  rows %d, near-tie swaps %d" % (len(rows), n_sw), flush=True)
+    # aggregation on sampled pixels, decoupled and end to end
+    total_pix = p["B"] * p["T"] * p["H"] * p["W"]
+    pix = np.unique(np.concatenate([rng.choice(total_pix, 60, replace=False), [0, total_pix - 1, p["W"] - 1]]))
+    nH, nW = oracle.grid(p)
+    shp = (p["B"], p["HD"], p["T"], nH, nW, kk)
+    ref = oracle.aggregate_at(c["v"], gd_h.reshape(shp), gi_h.reshape(shp + (3,)), p, pix, scale)
+    got = out_h.transpose(0, 1, 3, 4, 2).reshape(-1, p["C"])[pix]
+    assert_close(got, ref, "aggregate at sampled pixels (GPU neighbours)", scale=rms_finite(out_h))
+    cov = _covering_rows(p, pix[:24])
+    res2 = oracle.search(c["q"], c["k"], c["flows"], p, qids=cov)
+    _, sw2 = compare_topk(gd_h[cov], gi_h[cov], res2, kk, scale=rms_finite(gd_h))
+    d_all = gd_h.astype(np.float64).copy()
+    i_all = gi_h.astype(np.float64).copy()
+    d_all[cov] = res2["dists"][:, :kk]
+    i_all[cov] = res2["inds"][:, :kk]
+    ref2 = oracle.aggregate_at(c["v"], d_all.reshape(shp), i_all.reshape(shp + (3,)), p, pix[:24], scale)
+    swapped_pix = set()
+    for r in cov[sw2]:
+        swapped_pix.add(int(r))
+    keep = [i for i, pi in enumerate(pix[:24]) if not (set(_covering_rows(p, [pi]).tolist()) & swapped_pix)]
+    assert_close(got[:24][keep], ref2[keep], "aggregate at sampled pixels (end to end)", scale=rms_finite(out_h))
+
+
+# ------------------------------------------------------------- backward --
+
+def test_backward_matches_oracle(dev):
+    """Gradients w.r.t. q, k, v and flows (train256 settings on a 40 x 44 crop
+    size), with an upstream gradient on the scores as well."""
+    p = config_params(4, H=40, W=44)
+    r = np.random.default_rng(11)
+    q, k, v, flows = _inputs(p, 6000)
+    q *= 0.3
+    k *= 0.3
+    go = r.standard_normal(q.shape, dtype=np.float32)
+    scale = 0.5
+    qd, kd, vd, fd = (_d(a, dev) for a in (q, k, v, flows))
+    gd, gi = B.snls_search(qd, kd, fd, p)
+    nH, nW = oracle.grid(p)
+    gdist = r.standard_normal((p["B"], p["HD"], p["T"], nH, nW, p["k"]), dtype=np.float32)
+    grads = B.snls_backward(qd, kd, vd, fd, gd, gi, _d(go, dev), p, scale, grad_dists=_d(gdist, dev))
+    torch.cuda.synchronize()
+    ref = oracle.backward(q, k, v, flows, _h(gd), _h(gi), go, p, scale, grad_dists=gdist)
+    for name, g_gpu, g_ref in zip(("dq", "dk", "dv", "dflows"), grads, ref):
+        assert_close(_h(g_gpu), g_ref, name)
+    assert np.any(_h(grads[3]) != 0)
+
+
+def test_backward_adjoint_full_size(dev):
+    """train256 at full size: v -> out is linear for fixed neighbours, so
+    <out(x), y> = <x, grad_v(y)> with both sides from the GPU."""
+    c = _cfg(4)
+    p = c["params"]
+    qd, fd = _d(c["q"], dev), _d(c["flows"], dev)
+    gd, gi = B.snls_search(qd, qd, fd, p)
+    r = np.random.default_rng(12)
+    x = _d(r.standard_normal(c["q"].shape, dtype=np.float32), dev)
+    y = _d(c["grad_out"], dev)
+    out = B.snls_aggregate(x, gd, gi, p, c["scale"])
+    _, _, gv, _ = B.snls_backward(qd, qd, x, fd, gd, gi, y, p, c["scale"])
+    torch.cuda.synchronize()
+    lhs = float((out.double() * y.double()).sum())
+    rhs = float((x.double() * gv.double()).sum())
+    assert abs(lhs - rhs) <= REL * max(abs(lhs), 1.0)
