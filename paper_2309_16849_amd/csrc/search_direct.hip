@@ -43,39 +43,6 @@ SNLS_DEV void read_shift(const float* __restrict__ flows, const Geo& g, const Qu
   *fw = flows[(base + 1) * g.HW + pix];
 }
 
-// Patch similarity of a valid candidate with displacement (disp_h, disp_w)
-// in frame t2 (inner product or squared L2 over in-frame query pixels and
-// the head's channels).
-SNLS_DEV float score_candidate(const float* __restrict__ q, const float* __restrict__ k, const Geo& g,
-                               const QueryPos& qp, int t2, float disp_h, float disp_w) {
-  int nh, nw;
-  float ah, aw;
-  split_disp(disp_h, &nh, &ah);
-  split_disp(disp_w, &nw, &aw);
-  const float* qbase = q + (((long long)qp.b * g.T + qp.t) * g.C + (long long)qp.hd * g.Ch) * g.HW;
-  const float* kbase = k + (((long long)qp.b * g.T + t2) * g.C + (long long)qp.hd * g.Ch) * g.HW;
-  float acc = 0.f;
-  for (int ph = g.lo; ph < g.lo + g.ps; ++ph) {
-    int y = qp.h + ph;
-    if (y < 0 || y >= g.H) continue;
-    for (int pw = g.lo; pw < g.lo + g.ps; ++pw) {
-      int x = qp.w + pw;
-      if (x < 0 || x >= g.W) continue;
-      for (int c = 0; c < g.Ch; ++c) {
-        float qv = qbase[c * g.HW + (long long)y * g.W + x];
-        float kv = bilinear_plane(kbase + c * g.HW, g.H, g.W, y + nh, x + nw, ah, aw);
-        if (g.dist == SNLS_DIST_PROD) {
-          acc = fmaf(qv, kv, acc);
-        } else {
-          float e = qv - kv;
-          acc = fmaf(e, e, acc);
-        }
-      }
-    }
-  }
-  return acc;
-}
-
 // One thread per (query row, candidate): every candidate in id order.
 __global__ void __launch_bounds__(256) search_full_kernel(const float* __restrict__ q, const float* __restrict__ k,
                                                           const float* __restrict__ flows, Geo g,
@@ -93,7 +60,7 @@ __global__ void __launch_bounds__(256) search_full_kernel(const float* __restric
   float disp_w = cand_disp(fw, g.s1, dw, g.r);
   int t2 = qp.t + dt;
   bool ok = t2 >= 0 && t2 < g.T && centre_ok(qp.h, disp_h, g.H) && centre_ok(qp.w, disp_w, g.W);
-  float d = ok ? score_candidate(q, k, g, qp, t2, disp_h, disp_w) : from_score(-INFINITY, g.dist);
+  float d = ok ? score_candidate(q, k, g, qp.b, qp.hd, qp.t, qp.h, qp.w, t2, disp_h, disp_w) : from_score(-INFINITY, g.dist);
   dists[gid] = d;
   inds[3 * gid + 0] = (float)t2;
   inds[3 * gid + 1] = disp_h;
@@ -124,7 +91,7 @@ __global__ void __launch_bounds__(128) search_topk_direct_kernel(const float* __
         float disp_w = cand_disp(fw, g.s1, dw, g.r);
         int cid = ((dt + g.wt) * g.ws + dh) * g.ws + dw;
         float sc = -INFINITY;
-        if (okh && centre_ok(qp.w, disp_w, g.W)) sc = to_score(score_candidate(q, k, g, qp, t2, disp_h, disp_w), g.dist);
+        if (okh && centre_ok(qp.w, disp_w, g.W)) sc = to_score(score_candidate(q, k, g, qp.b, qp.hd, qp.t, qp.h, qp.w, t2, disp_h, disp_w), g.dist);
         lst.push(sc, cid, g.k);
       }
     }
@@ -182,6 +149,7 @@ snls_status launch_search_topk_direct(const float* q, const float* k, const floa
 
 snls_status launch_search_topk(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, hipStream_t s) {
+  if (tile_supported(g)) return launch_search_tile(q, k, flows, g, dists, inds, s);
   return launch_search_topk_direct(q, k, flows, g, dists, inds, s);
 }
 

@@ -8,6 +8,7 @@
 // outside the frame.
 #pragma once
 
+#include <limits.h>
 #include <stdint.h>
 #include "../../include/snls.h"
 
@@ -40,6 +41,11 @@ snls_status launch_search_full(const float* q, const float* k, const float* flow
                                float* inds, hipStream_t s);
 snls_status launch_search_topk(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, hipStream_t s);
+snls_status launch_search_topk_direct(const float* q, const float* k, const float* flows, const Geo& g,
+                                      float* dists, float* inds, hipStream_t s);
+snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
+                               float* inds, hipStream_t s);
+bool tile_supported(const Geo& g);
 snls_status launch_topk(const float* dall, const float* iall, int64_t rows, int ncand, int k, int dist,
                         float* dists, float* inds, hipStream_t s);
 snls_status launch_aggregate(const float* v, const float* dists, const float* inds, const Geo& g, float scale,
@@ -103,6 +109,40 @@ SNLS_DEV int cover_count_1d(int y, int S, int n, int lo, int P) {
   int mmax = b / S;
   if (mmax > n - 1) mmax = n - 1;
   return mmax >= mmin ? mmax - mmin + 1 : 0;
+}
+
+// Patch similarity of a valid candidate with displacement (disp_h, disp_w)
+// in frame t2 for the query (b, hd, t, h, w): inner product or squared L2
+// over the query pixels inside the frame and the head's channels, with
+// bilinear reads of the key frame (the direct in-place computation).
+SNLS_DEV float score_candidate(const float* __restrict__ q, const float* __restrict__ k, const Geo& g, int b,
+                               int hd, int t, int h, int w, int t2, float disp_h, float disp_w) {
+  int nh, nw;
+  float ah, aw;
+  split_disp(disp_h, &nh, &ah);
+  split_disp(disp_w, &nw, &aw);
+  const float* qbase = q + (((long long)b * g.T + t) * g.C + (long long)hd * g.Ch) * g.HW;
+  const float* kbase = k + (((long long)b * g.T + t2) * g.C + (long long)hd * g.Ch) * g.HW;
+  float acc = 0.f;
+  for (int ph = g.lo; ph < g.lo + g.ps; ++ph) {
+    int y = h + ph;
+    if (y < 0 || y >= g.H) continue;
+    for (int pw = g.lo; pw < g.lo + g.ps; ++pw) {
+      int x = w + pw;
+      if (x < 0 || x >= g.W) continue;
+      for (int c = 0; c < g.Ch; ++c) {
+        float qv = qbase[c * g.HW + (long long)y * g.W + x];
+        float kv = bilinear_plane(kbase + c * g.HW, g.H, g.W, y + nh, x + nw, ah, aw);
+        if (g.dist == SNLS_DIST_PROD) {
+          acc = fmaf(qv, kv, acc);
+        } else {
+          float e = qv - kv;
+          acc = fmaf(e, e, acc);
+        }
+      }
+    }
+  }
+  return acc;
 }
 
 // Sorted top-K list in registers, best first.  KMAX is the capacity; only
