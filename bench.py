@@ -141,6 +141,7 @@ def main():
     dists = torch.empty(shp, device=dev)
     inds = torch.empty(shp + (3,), device=dev)
     out = torch.empty(B.video_shape(p), device=dev)
+    ws = B.workspace_for(B.SNLS_OP_AGGREGATE, p, dev)
 
     def step(ev=None):
         if ev is not None:
@@ -148,7 +149,7 @@ def main():
         B.snls_search(x, x, fl, p, dists, inds)
         if ev is not None:
             ev[1].record()
-        B.snls_aggregate(x, dists, inds, p, scale, out)
+        B.snls_aggregate(x, dists, inds, p, scale, out, ws)
         if ev is not None:
             ev[2].record()
 

@@ -129,16 +129,21 @@ snls_status snls_topk(const float* dists_all, const float* inds_all, int64_t row
  * sum_l w_l * v~(frame_l, c, h+p_h+disp_h,l, w+p_w+disp_w,l) for the head's
  * channels; each output pixel is divided by the number of query patches
  * covering it, and pixels no patch covers are 0.  Neighbours whose frame
- * entry is not an integer in [0,T) contribute nothing.
- *   v      device, (B, T, C, H, W) value video
- *   dists  device, (B, HD, T, nH, nW, k) with k = p->k >= 1
- *   inds   device, (B, HD, T, nH, nW, k, 3)
- *   scale  softmax temperature factor (finite)
- *   out    device out, (B, T, C, H, W), fully overwritten
+ * entry is not an integer in [0,T) or whose displacement is not finite
+ * contribute nothing.
+ *   v          device, (B, T, C, H, W) value video
+ *   dists      device, (B, HD, T, nH, nW, k) with k = p->k >= 1
+ *   inds       device, (B, HD, T, nH, nW, k, 3)
+ *   scale      softmax temperature factor (finite)
+ *   out        device out, (B, T, C, H, W), fully overwritten
+ *   workspace  device scratch of at least snls_workspace_size(SNLS_OP_AGGREGATE,
+ *              p) bytes, 256-byte aligned (softmax weights and a channels-last
+ *              copy of v); its contents are not needed between calls
+ * The result does not depend on scheduling: it is bit-identical between runs.
  * Errors: SNLS_ERR_INVALID_ARG, SNLS_ERR_UNSUPPORTED (k > SNLS_MAX_K),
- * SNLS_ERR_HIP. */
+ * SNLS_ERR_WORKSPACE, SNLS_ERR_HIP. */
 snls_status snls_aggregate(const float* v, const float* dists, const float* inds, const snls_params* p,
-                           float scale, float* out, void* stream);
+                           float scale, float* out, void* workspace, size_t workspace_bytes, void* stream);
 
 /* snls_backward -- gradients of search + aggregation (Sec. 1: the grid
  * search is differentiable; the top-k set is held fixed, Sec. 3.2).
@@ -162,7 +167,7 @@ snls_status snls_backward(const float* q, const float* k, const float* v, const 
 #define SNLS_OP_BACKWARD 2
 
 /* Device workspace in bytes that operation op needs for parameters p
- * (0 for search and aggregate; (size_t)-1 for invalid arguments). */
+ * (0 for search; (size_t)-1 for invalid arguments). */
 size_t snls_workspace_size(int op, const snls_params* p);
 
 /* Static, NUL-terminated description of a status code. */

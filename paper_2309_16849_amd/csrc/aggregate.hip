@@ -1,36 +1,289 @@
 // aggregate.hip -- weighted patch aggregation (Sec. 3.2 "Aggregation").
 //
-// Gather form (no atomics, deterministic): each thread owns one output pixel
-// and a chunk of channels of one head, visits every query patch covering the
-// pixel, recomputes that query's softmax weights from its k scores and adds
-// the weighted bilinear reads of its neighbours, then divides by the number
-// of covering patches (a product of two 1-D counts).
+// out(y) = 1/cnt(y) * sum over query patches covering y, over the query's k
+// neighbours l, of w_l * v~(frame_l, y + disp_l), with w = softmax over the
+// row and v~ the bilinear read.  Written output-stationary (a gather, no
+// float atomics on the output): for one output pixel, every (covering
+// query, neighbour, bilinear tap) contribution lands on an integer source
+// position of one frame.  Neighbouring queries select overlapping regions,
+// so the ~4*k*P^2 contributions fall on far fewer distinct positions.  They
+// are merged first -- weights summed per (frame, position) in a small LDS
+// box, in 2^-24 fixed point with integer atomics so the sum does not depend
+// on the order -- and only then is each distinct position's channel vector
+// read once (channels-last copy of V, one coalesced 256-byte row per
+// position for 64 channels) and accumulated.
+//
+// Kernels: softmax weights per (row, neighbour); transpose of V to
+// (B,T,H,W,C); the merged gather; plus the plain per-tap gather used when a
+// configuration exceeds the merged kernel's limits.
 #include "snls_internal.h"
 
 namespace snls {
 
-constexpr int kAggChunk = 16;  // channels per thread
+namespace agg {
+constexpr int TY = 8, TX = 8;          // output tile of one workgroup
+constexpr int WAVES = 4;               // each wave processes 16 of the 64 pixels
+constexpr int NSLOT = 7;               // frames per window: 2*wt + 1 <= 7
+constexpr int BB = 16;                 // bin box side (positions base-7 .. base+8)
+constexpr int BINS = NSLOT * BB * BB;  // per wave
+constexpr int LMAX = BB * BB;          // non-zero list capacity per wave (one frame)
+constexpr float QSCALE = 16777216.f;   // fixed point 2^24
+}  // namespace agg
 
-// Softmax statistics of one query row: max of sign*scale*d over finite
-// entries and the normaliser.
-SNLS_DEV void row_softmax_stats(const float* __restrict__ d, int k, float sscale, float* m, float* z) {
-  float mx = -INFINITY;
-  for (int l = 0; l < k; ++l) {
-    float v = d[l];
-    if (isfinite(v)) mx = fmaxf(mx, sscale * v);
+// Softmax weights of each row (0 for non-finite scores, for neighbours whose
+// frame is not an integer in [0,T) or whose position is not finite).
+__global__ void __launch_bounds__(256) softmax_weights_kernel(const float* __restrict__ dists,
+                                                              const float* __restrict__ inds, Geo g, float scale,
+                                                              float* __restrict__ wts) {
+  long long row = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= g.rows) return;
+  const float sscale = (g.dist == SNLS_DIST_PROD ? 1.f : -1.f) * scale;
+  const float* d = dists + row * g.k;
+  const float* ind = inds + row * g.k * 3;
+  float m = -INFINITY;
+  for (int l = 0; l < g.k; ++l)
+    if (isfinite(d[l])) m = fmaxf(m, sscale * d[l]);
+  float z = 0.f;
+  for (int l = 0; l < g.k; ++l)
+    if (isfinite(d[l])) z += expf(sscale * d[l] - m);
+  const float inv = z > 0.f ? 1.f / z : 0.f;
+  for (int l = 0; l < g.k; ++l) {
+    const float tf = ind[3 * l], dh = ind[3 * l + 1], dw = ind[3 * l + 2];
+    const bool ok = isfinite(d[l]) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < 1.0e6f &&
+                    fabsf(dw) < 1.0e6f;
+    wts[row * g.k + l] = ok ? expf(sscale * d[l] - m) * inv : 0.f;
   }
-  float s = 0.f;
-  for (int l = 0; l < k; ++l) {
-    float v = d[l];
-    if (isfinite(v)) s += expf(sscale * v - mx);
-  }
-  *m = mx;
-  *z = s;
 }
 
+// (B,T,C,H,W) -> (B,T,H,W,C) through 64 x 64 LDS tiles.
+__global__ void __launch_bounds__(256) to_channels_last_kernel(const float* __restrict__ v, Geo g,
+                                                               float* __restrict__ vcl) {
+  __shared__ float tileb[64][65];
+  const long long bt = blockIdx.z;
+  const int c0 = blockIdx.y * 64;
+  const long long p0 = (long long)blockIdx.x * 64;
+  const float* src = v + bt * g.C * g.HW;
+  float* dst = vcl + bt * g.C * g.HW;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i;
+    const long long p = p0 + tx;
+    tileb[i][tx] = (c < g.C && p < g.HW) ? src[(long long)c * g.HW + p] : 0.f;
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const long long p = p0 + i;
+    const int c = c0 + tx;
+    if (c < g.C && p < g.HW) dst[p * g.C + c] = tileb[tx][i];
+  }
+}
+
+// Order this wave's earlier LDS accesses before its later ones (lanes of the
+// wave read what other lanes of the same wave wrote).
+SNLS_DEV void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Merged gather.  One workgroup = 8 x 8 output pixels of one (b, t, head);
+// one wave per pixel at a time, lane = channel (CPL channels per lane).
+template <int CPL>
+__global__ void __launch_bounds__(256) aggregate_merged_kernel(const float* __restrict__ vcl,
+                                                               const float* __restrict__ wts,
+                                                               const float* __restrict__ inds, Geo g, int tiles_x,
+                                                               int tiles_y, float* __restrict__ out) {
+  using namespace agg;
+  __shared__ int bins[WAVES][BINS];
+  __shared__ int lst_off[WAVES][LMAX];
+  __shared__ float lst_w[WAVES][LMAX];
+  __shared__ float otile[64 * CPL][TY * TX + 1];
+
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const long long tiles_img = (long long)tiles_x * tiles_y;
+  const long long wg = blockIdx.x;
+  const int img = (int)(wg / tiles_img);
+  const int trem = (int)(wg % tiles_img);
+  const int ty = trem / tiles_x, tx = trem % tiles_x;
+  const int t = img % g.T, hd = (img / g.T) % g.HD, b = img / (g.T * g.HD);
+  const int y0 = ty * TY, x0 = tx * TX;
+  const int nslot = 2 * g.wt + 1;
+  const int npairs = g.ps * g.ps * g.k;
+
+  for (int i = lane; i < BINS; i += 64) bins[wv][i] = 0;
+
+  for (int pi = wv; pi < TY * TX; pi += WAVES) {
+    const int y = y0 + pi / TX, x = x0 + pi % TX;
+    float acc[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) acc[c] = 0.f;
+    if (y < g.H && x < g.W) {
+      unsigned have = 0;  // slots with a base position (wave-uniform)
+      int base_h[NSLOT], base_w[NSLOT];  // bin box origin per slot (wave-uniform)
+#pragma unroll
+      for (int s = 0; s < NSLOT; ++s) base_h[s] = base_w[s] = 0;
+      for (int e0 = 0; e0 < npairs; e0 += 64) {
+        const int e = e0 + lane;
+        // this lane's contribution: (query patch offset p, neighbour l)
+        bool has = false;
+        int slot = -1, t2 = 0, nh = 0, nw = 0;
+        float wl = 0.f, ah = 0.f, aw = 0.f;
+        if (e < npairs) {
+          const int pidx = e / g.k, l = e % g.k;
+          const int ph = g.lo + pidx / g.ps, pw = g.lo + pidx % g.ps;
+          const int h = y - ph, w = x - pw;
+          if (h >= 0 && w >= 0 && h % g.s0 == 0 && w % g.s0 == 0 && h / g.s0 < g.nH && w / g.s0 < g.nW) {
+            const long long row = ((((long long)b * g.HD + hd) * g.T + t) * g.nH + h / g.s0) * g.nW + w / g.s0;
+            wl = wts[row * g.k + l];
+            if (wl != 0.f) {
+              const float* ind = inds + (row * g.k + l) * 3;
+              t2 = (int)ind[0];  // an integer in [0,T): checked by the weight pass
+              slot = t2 - t + g.wt;
+              if (slot < 0 || slot >= nslot) slot = -1;  // outside the window: direct path
+              const float fh = floorf(ind[1]), fw = floorf(ind[2]);
+              nh = (int)fh;
+              nw = (int)fw;
+              ah = ind[1] - fh;
+              aw = ind[2] - fw;
+              has = true;
+            }
+          }
+        }
+        // bases of slots seen for the first time: the first such lane's position
+#pragma unroll
+        for (int s = 0; s < NSLOT; ++s) {
+          if (s >= nslot || (have & (1u << s))) continue;
+          const unsigned long long m = __ballot(has && slot == s);
+          if (m) {
+            const int src = __ffsll((long long)m) - 1;
+            base_h[s] = __shfl(nh, src) - (BB / 2 - 1);
+            base_w[s] = __shfl(nw, src) - (BB / 2 - 1);
+            have |= 1u << s;
+          }
+        }
+        bool over = has && slot < 0;
+        if (has && slot >= 0) {
+          int bh = 0, bw = 0;
+#pragma unroll
+          for (int s = 0; s < NSLOT; ++s)
+            if (slot == s) {
+              bh = base_h[s];
+              bw = base_w[s];
+            }
+          const int rh = nh - bh, rw = nw - bw;
+          if (rh >= 0 && rh + 1 < BB && rw >= 0 && rw + 1 < BB) {
+            int* bb = &bins[wv][slot * BB * BB + rh * BB + rw];
+            const float t00 = wl * (1.f - ah) * (1.f - aw), t01 = wl * (1.f - ah) * aw;
+            const float t10 = wl * ah * (1.f - aw), t11 = wl * ah * aw;
+            atomicAdd(bb, __float2int_rn(t00 * QSCALE));
+            atomicAdd(bb + 1, __float2int_rn(t01 * QSCALE));
+            atomicAdd(bb + BB, __float2int_rn(t10 * QSCALE));
+            atomicAdd(bb + BB + 1, __float2int_rn(t11 * QSCALE));
+          } else {
+            over = true;
+          }
+        }
+        // contributions outside the box: the whole wave reads their taps directly
+        unsigned long long om = __ballot(over);
+        while (om) {
+          const int src = __ffsll((long long)om) - 1;
+          om &= om - 1;
+          const int t2_ = __shfl(t2, src), nh_ = __shfl(nh, src), nw_ = __shfl(nw, src);
+          const float wl_ = __shfl(wl, src), ah_ = __shfl(ah, src), aw_ = __shfl(aw, src);
+          const float* vb = vcl + ((long long)b * g.T + t2_) * g.HW * g.C + (long long)hd * g.Ch;
+#pragma unroll
+          for (int eh = 0; eh < 2; ++eh)
+#pragma unroll
+            for (int ew = 0; ew < 2; ++ew) {
+              const int Y = y + nh_ + eh, X = x + nw_ + ew;
+              const float tw = wl_ * (eh ? ah_ : 1.f - ah_) * (ew ? aw_ : 1.f - aw_);
+              if (Y >= 0 && Y < g.H && X >= 0 && X < g.W && tw != 0.f) {
+                const float* vp = vb + ((long long)Y * g.W + X) * g.C;
+#pragma unroll
+                for (int c = 0; c < CPL; ++c)
+                  if (lane + 64 * c < g.Ch) acc[c] = fmaf(tw, vp[lane + 64 * c], acc[c]);
+              }
+            }
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      // per frame: non-zero bins -> list (bin order: deterministic), bins
+      // cleared on the way, then one channel-vector read per listed position
+      wave_lds_sync();
+      const float* vb = vcl + (long long)b * g.T * g.HW * g.C + (long long)hd * g.Ch;
+#pragma unroll
+      for (int s = 0; s < NSLOT; ++s) {
+        if (s >= nslot || !(have & (1u << s))) continue;
+        const int bh = base_h[s], bw = base_w[s];
+        const int fbase = (t + s - g.wt) * (int)g.HW;
+        int nlist = 0;
+        for (int i0 = 0; i0 < BB * BB; i0 += 64) {
+          const int i = i0 + lane;
+          const int qv = bins[wv][s * BB * BB + i];
+          const int Y = y + bh + i / BB, X = x + bw + i % BB;
+          const bool nz = qv != 0 && Y >= 0 && Y < g.H && X >= 0 && X < g.W;
+          if (qv != 0) bins[wv][s * BB * BB + i] = 0;
+          const unsigned long long m = __ballot(nz);
+          const int pos = nlist + __popcll(m & ((1ull << lane) - 1ull));
+          if (nz) {
+            lst_off[wv][pos] = (fbase + Y * g.W + X) * g.C;
+            lst_w[wv][pos] = (float)qv * (1.f / QSCALE);
+          }
+          nlist += __popcll(m);
+        }
+        wave_lds_sync();
+        int i = 0;
+        for (; i + 4 <= nlist; i += 4) {
+          const int o0 = lst_off[wv][i], o1 = lst_off[wv][i + 1], o2 = lst_off[wv][i + 2], o3 = lst_off[wv][i + 3];
+          const float w0 = lst_w[wv][i], w1 = lst_w[wv][i + 1], w2 = lst_w[wv][i + 2], w3 = lst_w[wv][i + 3];
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) {
+            const int cc = lane + 64 * c;
+            if (cc < g.Ch) {
+              const float a0 = vb[o0 + cc], a1 = vb[o1 + cc], a2 = vb[o2 + cc], a3 = vb[o3 + cc];
+              acc[c] = fmaf(w0, a0, acc[c]);
+              acc[c] = fmaf(w1, a1, acc[c]);
+              acc[c] = fmaf(w2, a2, acc[c]);
+              acc[c] = fmaf(w3, a3, acc[c]);
+            }
+          }
+        }
+        for (; i < nlist; ++i) {
+          const int o0 = lst_off[wv][i];
+          const float w0 = lst_w[wv][i];
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) {
+            const int cc = lane + 64 * c;
+            if (cc < g.Ch) acc[c] = fmaf(w0, vb[o0 + cc], acc[c]);
+          }
+        }
+        wave_lds_sync();
+      }
+      const int cnt = cover_count_1d(y, g.s0, g.nH, g.lo, g.ps) * cover_count_1d(x, g.s0, g.nW, g.lo, g.ps);
+      const float inv = cnt > 0 ? 1.f / (float)cnt : 0.f;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) acc[c] = cnt > 0 ? acc[c] * inv : 0.f;
+    }
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) otile[lane + 64 * c][pi] = acc[c];
+  }
+  __syncthreads();
+  // write the tile: rows of TX pixels per (channel, tile row)
+  for (int e = threadIdx.x; e < g.Ch * TY * TX; e += 256) {
+    const int c = e / (TY * TX), pi = e % (TY * TX);
+    const int y = y0 + pi / TX, x = x0 + pi % TX;
+    if (y < g.H && x < g.W)
+      out[(((long long)b * g.T + t) * g.C + (long long)hd * g.Ch + c) * g.HW + (long long)y * g.W + x] = otile[c][pi];
+  }
+}
+
+// Plain per-tap gather for configurations beyond the merged kernel's limits
+// (more than 7 frames per window or more than 256 channels per head).
+constexpr int kAggChunk = 16;
+
 __global__ void __launch_bounds__(256) aggregate_gather_kernel(const float* __restrict__ v,
-                                                               const float* __restrict__ dists,
-                                                               const float* __restrict__ inds, Geo g, float scale,
+                                                               const float* __restrict__ wts,
+                                                               const float* __restrict__ inds, Geo g,
                                                                float* __restrict__ out) {
   const int nchunk = (g.Ch + kAggChunk - 1) / kAggChunk;
   long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -48,12 +301,9 @@ __global__ void __launch_bounds__(256) aggregate_gather_kernel(const float* __re
   int b = (int)(r / g.T);
   const int c0 = hd * g.Ch + chunk * kAggChunk;
   const int nc = min(kAggChunk, g.Ch - chunk * kAggChunk);
-  const float sscale = (g.dist == SNLS_DIST_PROD ? 1.f : -1.f) * scale;
-
   float acc[kAggChunk];
 #pragma unroll
   for (int c = 0; c < kAggChunk; ++c) acc[c] = 0.f;
-
   for (int ph = g.lo; ph < g.lo + g.ps; ++ph) {
     int h = y - ph;
     if (h < 0 || h % g.s0) continue;
@@ -65,31 +315,20 @@ __global__ void __launch_bounds__(256) aggregate_gather_kernel(const float* __re
       int mw = w / g.s0;
       if (mw >= g.nW) continue;
       long long row = ((((long long)b * g.HD + hd) * g.T + t) * g.nH + mh) * g.nW + mw;
-      const float* drow = dists + row * g.k;
-      const float* irow = inds + row * g.k * 3;
-      float m, z;
-      row_softmax_stats(drow, g.k, sscale, &m, &z);
-      if (!(z > 0.f)) continue;
-      float inv = 1.f / z;
       for (int l = 0; l < g.k; ++l) {
-        float dl = drow[l];
-        if (!isfinite(dl)) continue;
-        float tf = irow[3 * l + 0];
-        if (!(tf >= 0.f && tf < (float)g.T) || tf != floorf(tf)) continue;
-        float py = (float)y + irow[3 * l + 1];
-        float px = (float)x + irow[3 * l + 2];
+        const float wl = wts[row * g.k + l];
+        if (wl == 0.f) continue;
+        const float* ind = inds + (row * g.k + l) * 3;
+        float py = (float)y + ind[1], px = (float)x + ind[2];
         if (!(py > -1.f && py < (float)g.H && px > -1.f && px < (float)g.W)) continue;
-        float wl = expf(sscale * dl - m) * inv;
-        int t2 = (int)tf;
         int ny, nx;
         float ay, ax;
-        split_disp(irow[3 * l + 1], &ny, &ay);
-        split_disp(irow[3 * l + 2], &nx, &ax);
-        const float* vb = v + (((long long)b * g.T + t2) * g.C + c0) * g.HW;
+        split_disp(ind[1], &ny, &ay);
+        split_disp(ind[2], &nx, &ax);
+        const float* vb = v + (((long long)b * g.T + (int)ind[0]) * g.C + c0) * g.HW;
 #pragma unroll
-        for (int c = 0; c < kAggChunk; ++c) {
+        for (int c = 0; c < kAggChunk; ++c)
           if (c < nc) acc[c] = fmaf(wl, bilinear_plane(vb + c * g.HW, g.H, g.W, y + ny, x + nx, ay, ax), acc[c]);
-        }
       }
     }
   }
@@ -97,18 +336,50 @@ __global__ void __launch_bounds__(256) aggregate_gather_kernel(const float* __re
   float inv = cnt > 0 ? 1.f / (float)cnt : 0.f;
   float* ob = out + (((long long)b * g.T + t) * g.C + c0) * g.HW + (long long)y * g.W + x;
 #pragma unroll
-  for (int c = 0; c < kAggChunk; ++c) {
+  for (int c = 0; c < kAggChunk; ++c)
     if (c < nc) ob[c * g.HW] = cnt > 0 ? acc[c] * inv : 0.f;
-  }
+}
+
+size_t aggregate_ws_bytes(const Geo& g) {
+  size_t w = (size_t)g.rows * (size_t)g.k * sizeof(float);
+  w = (w + 255) & ~(size_t)255;
+  return w + (size_t)g.B * g.T * g.C * g.HW * sizeof(float);
 }
 
 snls_status launch_aggregate(const float* v, const float* dists, const float* inds, const Geo& g, float scale,
-                             float* out, hipStream_t s) {
-  const int nchunk = (g.Ch + kAggChunk - 1) / kAggChunk;
-  long long total = (long long)g.B * g.T * g.HD * nchunk * g.HW;
-  if (total == 0) return SNLS_OK;
-  unsigned blocks = (unsigned)((total + 255) / 256);
-  hipLaunchKernelGGL(aggregate_gather_kernel, dim3(blocks), dim3(256), 0, s, v, dists, inds, g, scale, out);
+                             float* out, void* ws, hipStream_t s) {
+  if (g.rows == 0) return SNLS_OK;
+  float* wts = static_cast<float*>(ws);
+  size_t woff = ((size_t)g.rows * g.k * sizeof(float) + 255) & ~(size_t)255;
+  float* vcl = reinterpret_cast<float*>(static_cast<char*>(ws) + woff);
+  hipLaunchKernelGGL(softmax_weights_kernel, dim3((unsigned)((g.rows + 255) / 256)), dim3(256), 0, s, dists, inds, g,
+                     scale, wts);
+  const int nslot = 2 * g.wt + 1;
+  // merged kernel limits: frames per window, channels per head, 32-bit
+  // offsets inside one batch entry, per-bin weight sums below 2^31 in 2^-24
+  // fixed point (at most P^2 <= 121 covering patches)
+  if (nslot <= agg::NSLOT && g.Ch <= 256 && (long long)g.T * g.HW * g.C < (1LL << 31) && g.ps <= 11) {
+    dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
+    hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
+    const int tiles_x = (g.W + agg::TX - 1) / agg::TX, tiles_y = (g.H + agg::TY - 1) / agg::TY;
+    const long long nwg = (long long)tiles_x * tiles_y * g.B * g.T * g.HD;
+    if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
+    const int cpl = (g.Ch + 63) / 64;
+    if (cpl == 1)
+      hipLaunchKernelGGL(aggregate_merged_kernel<1>, dim3((unsigned)nwg), dim3(256), 0, s, vcl, wts, inds, g,
+                         tiles_x, tiles_y, out);
+    else if (cpl == 2)
+      hipLaunchKernelGGL(aggregate_merged_kernel<2>, dim3((unsigned)nwg), dim3(256), 0, s, vcl, wts, inds, g,
+                         tiles_x, tiles_y, out);
+    else
+      hipLaunchKernelGGL(aggregate_merged_kernel<4>, dim3((unsigned)nwg), dim3(256), 0, s, vcl, wts, inds, g,
+                         tiles_x, tiles_y, out);
+  } else {
+    const int nchunk = (g.Ch + kAggChunk - 1) / kAggChunk;
+    long long total = (long long)g.B * g.T * g.HD * nchunk * g.HW;
+    hipLaunchKernelGGL(aggregate_gather_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, v, wts, inds,
+                       g, out);
+  }
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
 }
 

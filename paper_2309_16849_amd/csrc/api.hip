@@ -45,7 +45,7 @@ const char* snls_status_string(snls_status s) {
 size_t snls_workspace_size(int op, const snls_params* p) {
   Geo g;
   if (op == SNLS_OP_SEARCH) return check_params(p, false, &g) == SNLS_OK ? 0 : (size_t)-1;
-  if (op == SNLS_OP_AGGREGATE) return check_params(p, true, &g) == SNLS_OK ? 0 : (size_t)-1;
+  if (op == SNLS_OP_AGGREGATE) return check_params(p, true, &g) == SNLS_OK ? aggregate_ws_bytes(g) : (size_t)-1;
   if (op == SNLS_OP_BACKWARD) return check_params(p, true, &g) == SNLS_OK ? backward_ws_bytes(g) : (size_t)-1;
   return (size_t)-1;
 }
@@ -71,13 +71,15 @@ snls_status snls_topk(const float* dists_all, const float* inds_all, int64_t row
 }
 
 snls_status snls_aggregate(const float* v, const float* dists, const float* inds, const snls_params* p,
-                           float scale, float* out, void* stream) {
+                           float scale, float* out, void* workspace, size_t workspace_bytes, void* stream) {
   Geo g;
   snls_status st = check_params(p, true, &g);
   if (st != SNLS_OK) return st;
   if (!v || !dists || !inds || !out || !std::isfinite(scale)) return SNLS_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < aggregate_ws_bytes(g) || (reinterpret_cast<uintptr_t>(workspace) & 255))
+    return SNLS_ERR_WORKSPACE;
   if ((st = device_ready()) != SNLS_OK) return st;
-  return launch_aggregate(v, dists, inds, g, scale, out, as_stream(stream));
+  return launch_aggregate(v, dists, inds, g, scale, out, workspace, as_stream(stream));
 }
 
 snls_status snls_backward(const float* q, const float* k, const float* v, const float* flows, const float* dists,

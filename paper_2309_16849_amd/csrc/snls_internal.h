@@ -34,6 +34,10 @@ struct Geo {
 snls_status check_params(const snls_params* p, bool need_k, Geo* g);
 snls_status check_topk_args(int64_t rows, int32_t n_cand, int32_t k, int32_t dist_type);
 
+// Device workspace of snls_aggregate: softmax weights (rows x k) then a
+// channels-last copy of V, 256-byte aligned.
+size_t aggregate_ws_bytes(const Geo& g);
+
 #ifdef __HIPCC__
 
 // Launchers (one per kernel family); all return SNLS_OK or SNLS_ERR_HIP.
@@ -49,7 +53,7 @@ bool tile_supported(const Geo& g);
 snls_status launch_topk(const float* dall, const float* iall, int64_t rows, int ncand, int k, int dist,
                         float* dists, float* inds, hipStream_t s);
 snls_status launch_aggregate(const float* v, const float* dists, const float* inds, const Geo& g, float scale,
-                             float* out, hipStream_t s);
+                             float* out, void* ws, hipStream_t s);
 snls_status launch_backward(const float* q, const float* k, const float* v, const float* dists, const float* inds,
                             const float* grad_out, const float* grad_dists, const Geo& g, float scale,
                             float* grad_q, float* grad_k, float* grad_v, float* grad_flows, float* Gws,

@@ -55,7 +55,7 @@ def load_library():
         PP = ctypes.POINTER(SnlsParams)
         lib.snls_search.argtypes = [P, P, P, PP, P, P, P]
         lib.snls_topk.argtypes = [P, P, I64, I32, I32, I32, P, P, P]
-        lib.snls_aggregate.argtypes = [P, P, P, PP, F32, P, P]
+        lib.snls_aggregate.argtypes = [P, P, P, PP, F32, P, P, SZ, P]
         lib.snls_backward.argtypes = [P] * 8 + [PP, F32, P, P, P, P, P, SZ, P]
         lib.snls_workspace_size.argtypes = [ctypes.c_int, PP]
         lib.snls_workspace_size.restype = SZ
@@ -173,7 +173,15 @@ def snls_topk(dists_all, inds_all, k: int, dist_type: int, dists=None, inds=None
     return dists, inds
 
 
-def snls_aggregate(v, dists, inds, p: dict, scale: float = 1.0, out=None, stream=None):
+def workspace_for(op: int, p: dict, device):
+    """A device buffer of snls_workspace_size(op, p) bytes (torch allocations are 256-byte aligned)."""
+    need = snls_workspace_size(op, p)
+    if need == ctypes.c_size_t(-1).value:
+        raise SnlsError(SNLS_ERR_INVALID_ARG, "snls_workspace_size")
+    return torch.empty(max((need + 3) // 4, 1), device=device, dtype=torch.float32)
+
+
+def snls_aggregate(v, dists, inds, p: dict, scale: float = 1.0, out=None, workspace=None, stream=None):
     """Softmax-weighted patch aggregation; returns out (B,T,C,H,W)."""
     lib = load_library()
     _dev(v, "v", video_shape(p))
@@ -183,9 +191,11 @@ def snls_aggregate(v, dists, inds, p: dict, scale: float = 1.0, out=None, stream
     if out is None:
         out = torch.empty(video_shape(p), device=v.device, dtype=torch.float32)
     _dev(out, "out", video_shape(p))
+    if workspace is None:
+        workspace = workspace_for(SNLS_OP_AGGREGATE, p, v.device)
     prm = params_from_dict(p)
     _check(lib.snls_aggregate(_ptr(v), _ptr(dists), _ptr(inds), ctypes.byref(prm), float(scale), _ptr(out),
-                              _stream(stream)), "snls_aggregate")
+                              _ptr(workspace), workspace.numel() * 4, _stream(stream)), "snls_aggregate")
     return out
 
 
@@ -204,9 +214,8 @@ def snls_backward(q, k, v, flows, dists, inds, grad_out, p: dict, scale: float =
         _dev(flows, "flows", flow_shape(p))
     gq, gk, gv = (torch.empty(vs, device=q.device, dtype=torch.float32) for _ in range(3))
     gf = torch.empty(flow_shape(p), device=q.device, dtype=torch.float32)
-    need = snls_workspace_size(SNLS_OP_BACKWARD, p)
     if workspace is None:
-        workspace = torch.empty(max(need // 4, 1), device=q.device, dtype=torch.float32)
+        workspace = workspace_for(SNLS_OP_BACKWARD, p, q.device)
     prm = params_from_dict(p)
     _check(lib.snls_backward(_ptr(q), _ptr(k), _ptr(v), _ptr(flows), _ptr(dists), _ptr(inds), _ptr(grad_out),
                              _ptr(grad_dists), ctypes.byref(prm), float(scale), _ptr(gq), _ptr(gk), _ptr(gv),

@@ -87,12 +87,19 @@ def test_k_limits(lib):
 
 def test_aggregate_and_backward_validation(lib):
     prm = _params(k=0)  # aggregation needs k >= 1
-    assert lib.snls_aggregate(FAKE, FAKE, FAKE, ctypes.byref(prm), 1.0, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    big = 1 << 40
+    assert lib.snls_aggregate(FAKE, FAKE, FAKE, ctypes.byref(prm), 1.0, FAKE, FAKE, big, None) == B.SNLS_ERR_INVALID_ARG
     prm = _params()
-    assert lib.snls_aggregate(FAKE, FAKE, FAKE, ctypes.byref(prm), float("inf"), FAKE, None) == B.SNLS_ERR_INVALID_ARG
-    assert lib.snls_aggregate(FAKE, None, FAKE, ctypes.byref(prm), 1.0, FAKE, None) == B.SNLS_ERR_INVALID_ARG
-    need = lib.snls_workspace_size(B.SNLS_OP_BACKWARD, ctypes.byref(prm))
+    assert lib.snls_aggregate(FAKE, FAKE, FAKE, ctypes.byref(prm), float("inf"), FAKE, FAKE, big,
+                              None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_aggregate(FAKE, None, FAKE, ctypes.byref(prm), 1.0, FAKE, FAKE, big, None) == B.SNLS_ERR_INVALID_ARG
+    agg_need = lib.snls_workspace_size(B.SNLS_OP_AGGREGATE, ctypes.byref(prm))
     nq = 1 * 2 * 3 * 16 * 17
+    assert agg_need == ((nq * 4 * 4 + 255) // 256) * 256 + 1 * 3 * 8 * 16 * 17 * 4
+    assert lib.snls_aggregate(FAKE, FAKE, FAKE, ctypes.byref(prm), 1.0, FAKE, None, big, None) == B.SNLS_ERR_WORKSPACE
+    assert lib.snls_aggregate(FAKE, FAKE, FAKE, ctypes.byref(prm), 1.0, FAKE, FAKE, agg_need - 1,
+                              None) == B.SNLS_ERR_WORKSPACE
+    need = lib.snls_workspace_size(B.SNLS_OP_BACKWARD, ctypes.byref(prm))
     assert need == nq * 4 * 4
     args = [FAKE] * 8
     st = lib.snls_backward(*args, ctypes.byref(prm), 1.0, FAKE, FAKE, FAKE, FAKE, None, 0, None)
