@@ -42,31 +42,44 @@ constexpr int HROWS = 16;               // halo rows = lanes per group
 constexpr int NGROUP = 64;              // groups per workgroup
 constexpr int NTHREADS = HROWS * NGROUP;
 constexpr int S = 6;                    // shift columns per task
-constexpr int XMAX = 14;                // halo width limit (TQW + P - 1, P <= 7)
-constexpr int CC = 8;                   // channels per staging chunk
-constexpr int KR = 40;                  // K rows in LDS
-constexpr int KP = 44;                  // K row pitch (floats)
-constexpr int QP = 20;                  // q row pitch (floats)
+constexpr int CC = 4;                   // channels per staging chunk (double-buffered)
+constexpr int KR = 36;                  // K rows in LDS
+constexpr int KP = 45;                  // K row pitch (odd: spreads the 16 rows of a group over the banks)
+constexpr int QP = 21;                  // q row pitch (odd)
 constexpr int MAXBLK = 5;               // shift-column blocks: union width <= 30
 constexpr int WSMAX = 9;
-constexpr int WIN = (WSMAX + 1) * (WSMAX + 1);
-constexpr int QMAX = HROWS * TQW;       // queries per tile (P = 1)
+constexpr int WP = WSMAX + 1;           // window-table pitch
+constexpr int WIN = WP * WP;
+constexpr int WSQ = WSMAX * WSMAX;      // candidates per query and frame
 constexpr int KLIST = 16;               // top-k capacity
 
-constexpr int KST_F = CC * KR * KP;     // 14080 floats
-constexpr int QST_F = CC * HROWS * QP;  // 2560
-constexpr int BW_F = QMAX * WIN;        // 12800
-constexpr int LIST_W = QMAX * KLIST;    // scores + ids, 2048 each
+// Each direct-to-LDS load fills a whole 64-word block, so the staging
+// buffers are padded to a multiple of 64 words (the padding reads as 0).
+constexpr int KST_F = (CC * KR * KP + 63) / 64 * 64;     // 6528 floats
+constexpr int QST_F = (CC * HROWS * QP + 63) / 64 * 64;  // 1344
+// all direct-to-LDS targets (placed first in LDS) stay below 64 KB
+static_assert((2 * KST_F + 2 * QST_F) * 4 <= 65536, "staging buffers must sit in the first 64 KB of LDS");
+constexpr int KLD = (KST_F + 64 * 16 - 1) / (64 * 16);  // 64-word LDS loads per wave for K
+constexpr int QLD = (QST_F + 64 * 16 - 1) / (64 * 16);  // ... for q
 
+
+template <int PS>
 struct Smem {
-  float kst[KST_F];  // K union region chunk; reused as the candidate score table
-  float qst[QST_F];  // q halo chunk
-  float bw[BW_F];    // per-query window of box sums, (WSMAX+1)^2 cells
-  float lst_s[LIST_W];
-  int lst_id[LIST_W];
-  int qn_h[QMAX], qn_w[QMAX];  // integer part of the offset
-  float qf_h[QMAX], qf_w[QMAX];  // the offset itself
-  int uni[4];  // min N_h, max N_h, min N_w, max N_w
+  static constexpr int QN = (HROWS - PS + 1) * TQW;  // queries per tile
+  static constexpr int NPART = QN <= 80 ? 4 : 2;     // partial top-k lists per query
+  static_assert(QN * WSQ * 5 <= 2 * KST_F * 4, "survivor lists must fit in the K staging buffers");
+  static_assert(QN * NPART <= 1024, "one thread per partial list");
+  float kst[2][KST_F];  // K union region chunks (double buffer); reused for the top-k survivors
+  float qst[2][QST_F];  // q halo chunks
+  float bw[QN * WIN];  // per-query window of box sums
+  float lst_s[QN * NPART * KLIST];  // partial lists (query-major)
+  int lst_id[QN * NPART * KLIST];
+  float thr_s[QN * NPART];  // k-th entry of each partial list
+  int thr_id[QN * NPART];
+  int nsurv[QN];
+  int qn_h[QN], qn_w[QN];    // integer part of the offset
+  float qf_h[QN], qf_w[QN];  // the offset itself
+  int uni[4];                // min N_h, max N_h, min N_w, max N_w
 };
 
 }  // namespace tile
@@ -99,7 +112,9 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
   constexpr int TQH = HROWS - PS + 1;
   constexpr int HW = TQW + PS - 1;
   constexpr int LO = -(PS / 2);
-  __shared__ Smem sm;
+  constexpr int QN = Smem<PS>::QN;
+  constexpr int NPART = Smem<PS>::NPART;
+  __shared__ Smem<PS> sm;
 
   const int tid = threadIdx.x;
   const int lane16 = tid & 15;
@@ -120,35 +135,72 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
   const int y0 = ty * TQH, x0 = tx * TQW;  // tile origin (query = pixel, stride 1)
   const int Y0 = y0 + LO, X0 = x0 + LO;    // halo origin
   const int ws = g.ws, r = g.r;
-  const int nq_tile = TQH * TQW;
 
   const float* qb = q + (((long long)b * g.T + t) * g.C + (long long)hd * g.Ch) * g.HW;
 
-  for (int i = tid; i < nq_tile * KLIST; i += NTHREADS) {
+  for (int i = tid; i < QN * NPART * KLIST; i += NTHREADS) {
     sm.lst_s[i] = -INFINITY;
     sm.lst_id[i] = 0x7fffffff;
   }
+  if (tid < QN * NPART) {
+    sm.thr_s[tid] = -INFINITY;
+    sm.thr_id[tid] = 0x7fffffff;
+  }
+  if (tid < QN) sm.nsurv[tid] = 0;
+
+  // Direct-to-LDS staging: each 64-lane buffer load fills 64 consecutive LDS
+  // words; lane i of load m carries word 64*m + i of the chunk layout
+  // [c][row][pitch].  Positions outside the frame (or padding) use an
+  // out-of-range offset, which the buffer unit returns as 0.
+  const int wave = tid >> 6, lane = tid & 63;
+  constexpr unsigned OOB = 0x80000000u;
+  unsigned q_off[QLD];
+#pragma unroll
+  for (int m = 0; m < QLD; ++m) {
+    const int wrd = (wave + 16 * m) * 64 + lane;
+    const int c = wrd / (HROWS * QP), rem = wrd % (HROWS * QP);
+    const int yy = rem / QP, xx = rem % QP;
+    const int gy = Y0 + yy, gx = X0 + xx;
+    const bool ok = c < CC && xx < HW && gy >= 0 && gy < g.H && gx >= 0 && gx < g.W;
+    q_off[m] = ok ? (unsigned)(((long long)c * g.HW + (long long)gy * g.W + gx) * 4) : OOB;
+  }
+  const __amdgpu_buffer_rsrc_t q_rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)qb, (short)0, (int)(g.Ch * g.HW * 4), 0x00020000);
+
+  // window offset of this thread's query (tid < QN) for frame step dt
+  auto fetch_flow = [&](int dtt, float& fh, float& fw) {
+    fh = 0.f;
+    fw = 0.f;
+    const int h = y0 + tid / TQW, w = x0 + tid % TQW;
+    if (dtt != 0 && tid < QN && h < g.H && w < g.W) {
+      const long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dtt, g.wt)) * 2;
+      const long long pix = (long long)h * g.W + w;
+      fh = flows[base * g.HW + pix];
+      fw = flows[(base + 1) * g.HW + pix];
+    }
+  };
+  float fh_next = 0.f, fw_next = 0.f;
+  bool first = true;
 
   for (int dt = -g.wt; dt <= g.wt; ++dt) {
     const int t2 = t + dt;
     if (t2 < 0 || t2 >= g.T) continue;
     const float* kb = k + (((long long)b * g.T + t2) * g.C + (long long)hd * g.Ch) * g.HW;
+    const __amdgpu_buffer_rsrc_t k_rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)kb, (short)0, (int)(g.Ch * g.HW * 4), 0x00020000);
 
     // ---- offsets of the tile's queries and the union of shifts ----
     if (tid < 4) sm.uni[tid] = (tid & 1) ? INT_MIN : INT_MAX;
+    if (first) {
+      fetch_flow(dt, fh_next, fw_next);
+      first = false;
+    }
     __syncthreads();
-    if (tid < nq_tile) {
+    if (tid < QN) {
       const int jh = tid / TQW, jw = tid % TQW;
-      const int h = y0 + jh, w = x0 + jw;
-      float fh = 0.f, fw = 0.f;
+      const bool inside = y0 + jh < g.H && x0 + jw < g.W;
+      const float fh = fh_next, fw = fw_next;
       int nh = 0, nw = 0;
-      const bool inside = h < g.H && w < g.W;
-      if (dt != 0 && inside) {
-        long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dt, g.wt)) * 2;
-        long long pix = (long long)h * g.W + w;
-        fh = flows[base * g.HW + pix];
-        fw = flows[(base + 1) * g.HW + pix];
-      }
       // Offsets that are not finite or absurdly large leave the union alone;
       // their candidates fail the exact validity test below.
       if (fabsf(fh) < 1.0e6f) nh = (int)floorf(fh);
@@ -164,27 +216,52 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
         atomicMax(&sm.uni[3], nw);
       }
     }
+    // next searched frame's offsets, in flight during this frame
+    {
+      int dn = dt + 1;
+      while (dn <= g.wt && (t + dn < 0 || t + dn >= g.T)) ++dn;
+      if (dn <= g.wt) fetch_flow(dn, fh_next, fw_next);
+    }
     __syncthreads();
     const int dmin_h = sm.uni[0] - r, UH = sm.uni[1] - sm.uni[0] + ws + 1;
     const int dmin_w = sm.uni[2] - r, UW = sm.uni[3] - sm.uni[2] + ws + 1;
     const int nblk = (UW + S - 1) / S;
-    float* const dbuf = sm.kst;  // candidate scores of this frame (after staging)
+    // survivors of the top-k filter, stored over the K staging area once the
+    // frame's correlations are done: score and window cell (dh*ws + dw)
+    float* const surv_s = sm.kst[0];
+    unsigned char* const surv_c = reinterpret_cast<unsigned char*>(sm.kst[0] + QN * WSQ);
 
     if (nblk <= MAXBLK) {
       const int ntask = UH * nblk;
-      const int span_max = KR - HROWS + 1;                 // shift rows per round
+      const int span_max = KR - HROWS + 1;  // shift rows per round
       const int tasks_per_round = min(NGROUP, span_max * nblk);
       for (int r0 = 0; r0 < ntask; r0 += tasks_per_round) {
         const int r1 = min(ntask, r0 + tasks_per_round);
+        // few tasks: split each task's channels over several groups
+        const int room = NGROUP / (r1 - r0);
+        const int csplit = room >= 4 ? 4 : (room >= 2 ? 2 : 1);
         const int dh_lo = dmin_h + r0 / nblk;
         const int dh_hi = dmin_h + (r1 - 1) / nblk;
         const int krows = HROWS + dh_hi - dh_lo;
         const int kcols = HW + nblk * S - 1;
-        const int task = r0 + grp;
+        const int task = r0 + grp / csplit;
+        const int part = grp % csplit;
         const bool active = task < r1;
         const int d_h = dmin_h + task / nblk;
         const int blk = task % nblk;
         const int krow = lane16 + d_h - dh_lo;
+
+        // K staging offsets of this thread for this round
+        unsigned k_off[KLD];
+#pragma unroll
+        for (int m = 0; m < KLD; ++m) {
+          const int wrd = (wave + 16 * m) * 64 + lane;
+          const int c = wrd / (KR * KP), rem = wrd % (KR * KP);
+          const int yy = rem / KP, xx = rem % KP;
+          const int gy = Y0 + dh_lo + yy, gx = X0 + dmin_w + xx;
+          const bool ok = c < CC && yy < krows && xx < kcols && gy >= 0 && gy < g.H && gx >= 0 && gx < g.W;
+          k_off[m] = ok ? (unsigned)(((long long)c * g.HW + (long long)gy * g.W + gx) * 4) : OOB;
+        }
 
         float acc[HW][S];
 #pragma unroll
@@ -192,36 +269,43 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
 #pragma unroll
           for (int i = 0; i < S; ++i) acc[x][i] = 0.f;
 
-        for (int c0 = 0; c0 < g.Ch; c0 += CC) {
-          __syncthreads();  // previous chunk consumed
-          // stage q halo: HROWS x HW per channel
-          for (int e = tid; e < CC * HROWS * HW; e += NTHREADS) {
-            const int c = e / (HROWS * HW);
-            const int rem = e % (HROWS * HW);
-            const int yy = rem / HW, xx = rem % HW;
-            const int gy = Y0 + yy, gx = X0 + xx;
-            float v = 0.f;
-            if (c0 + c < g.Ch && gy >= 0 && gy < g.H && gx >= 0 && gx < g.W)
-              v = qb[(long long)(c0 + c) * g.HW + (long long)gy * g.W + gx];
-            sm.qst[(c * HROWS + yy) * QP + xx] = v;
+        // issue the asynchronous loads of chunk c0 into buffer bsel
+        auto issue = [&](int c0, int bsel) {
+          const unsigned cshift = (unsigned)(c0 * g.HW * 4);
+          const int cvalid = g.Ch - c0;  // channels of this chunk inside the head
+#pragma unroll
+          for (int m = 0; m < KLD; ++m) {
+            const int wbase = (wave + 16 * m) * 64;
+            if (wbase < KST_F) {
+              const int c = (wbase + lane) / (KR * KP);
+              const unsigned off = (k_off[m] == OOB || c >= cvalid) ? OOB : k_off[m] + cshift;
+              __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                  k_rs, (__attribute__((address_space(3))) void*)&sm.kst[bsel][wbase], 4, off, 0, 0, 0);
+            }
           }
-          // stage K union region: krows x kcols per channel
-          for (int e = tid; e < CC * krows * kcols; e += NTHREADS) {
-            const int c = e / (krows * kcols);
-            const int rem = e % (krows * kcols);
-            const int yy = rem / kcols, xx = rem % kcols;
-            const int gy = Y0 + dh_lo + yy, gx = X0 + dmin_w + xx;
-            float v = 0.f;
-            if (c0 + c < g.Ch && gy >= 0 && gy < g.H && gx >= 0 && gx < g.W)
-              v = kb[(long long)(c0 + c) * g.HW + (long long)gy * g.W + gx];
-            sm.kst[(c * KR + yy) * KP + xx] = v;
+#pragma unroll
+          for (int m = 0; m < QLD; ++m) {
+            const int wbase = (wave + 16 * m) * 64;
+            if (wbase < QST_F) {
+              const int c = (wbase + lane) / (HROWS * QP);
+              const unsigned off = (q_off[m] == OOB || c >= cvalid) ? OOB : q_off[m] + cshift;
+              __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                  q_rs, (__attribute__((address_space(3))) void*)&sm.qst[bsel][wbase], 4, off, 0, 0, 0);
+            }
           }
-          __syncthreads();
+        };
+        __syncthreads();  // buffers of the previous round / frame are free
+        issue(0, 0);
+        int bsel = 0;
+        for (int c0 = 0; c0 < g.Ch; c0 += CC, bsel ^= 1) {
+          __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of chunk c0 have landed in LDS
+          __syncthreads();                // ... and everyone's; buffer bsel^1 is no longer read
+          if (c0 + CC < g.Ch) issue(c0 + CC, bsel ^ 1);
           if (active) {
 #pragma unroll 1
-            for (int c = 0; c < CC; ++c) {
-              const float* qr = &sm.qst[(c * HROWS + lane16) * QP];
-              const float* kr = &sm.kst[(c * KR + krow) * KP + blk * S];
+            for (int c = part; c < CC; c += csplit) {
+              const float* qr = &sm.qst[bsel][(c * HROWS + lane16) * QP];
+              const float* kr = &sm.kst[bsel][(c * KR + krow) * KP + blk * S];
               // sliding window kw[i] = K(x + i) along the halo row
               float kw[S];
 #pragma unroll
@@ -256,108 +340,136 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
             asm volatile("" : "+v"(s));  // materialise the sum here: keeps the row moves short-lived
             acc[jw][i] = s;
           }
-        if (active && lane16 < TQH) {
-          const int jh = lane16;
+        // window tables: the first channel part writes, the others add in turn
+        for (int pp = 0; pp < csplit; ++pp) {
+          if (pp > 0) __syncthreads();
+          if (active && part == pp && lane16 < TQH) {
+            const int jh = lane16;
 #pragma unroll
-          for (int jw = 0; jw < TQW; ++jw) {
-            const int j = jh * TQW + jw;
-            const int u = d_h - (sm.qn_h[j] - r);
-            const int vbase = dmin_w + blk * S - (sm.qn_w[j] - r);
-            if (u >= 0 && u <= ws) {
+            for (int jw = 0; jw < TQW; ++jw) {
+              const int j = jh * TQW + jw;
+              const int u = d_h - (sm.qn_h[j] - r);
+              const int vbase = dmin_w + blk * S - (sm.qn_w[j] - r);
+              if (u >= 0 && u <= ws) {
 #pragma unroll
-              for (int i = 0; i < S; ++i) {
-                const int v = vbase + i;
-                if (v >= 0 && v <= ws) sm.bw[j * WIN + u * (WSMAX + 1) + v] = acc[jw][i];
+                for (int i = 0; i < S; ++i) {
+                  const int v = vbase + i;
+                  if (v >= 0 && v <= ws) {
+                    float* cell = &sm.bw[j * WIN + u * WP + v];
+                    *cell = pp == 0 ? acc[jw][i] : *cell + acc[jw][i];
+                  }
+                }
               }
             }
           }
         }
       }
       __syncthreads();
-      // ---- 4-tap combination + exact validity -> candidate scores ----
-      for (int e = tid; e < nq_tile * ws; e += NTHREADS) {
+      // ---- 4-tap combination, exact validity, threshold filter ----
+      for (int e = tid; e < QN * ws; e += NTHREADS) {
         const int j = e / ws, dh = e % ws;
         const int h = y0 + j / TQW, w = x0 + j % TQW;
+        if (h >= g.H || w >= g.W) continue;
         const float fh = sm.qf_h[j], fw = sm.qf_w[j];
         const float ah = fh - (float)sm.qn_h[j];
         const float aw = fw - (float)sm.qn_w[j];
-        const float* r0p = &sm.bw[j * WIN + dh * (WSMAX + 1)];
-        const float* r1p = r0p + (WSMAX + 1);
-        const float disp_h = cand_disp(fh, 1.f, dh, r);
-        const bool okh = centre_ok(h, disp_h, g.H);
+        const float* r0p = &sm.bw[j * WIN + dh * WP];
+        const float* r1p = r0p + WP;
+        const bool okh = centre_ok(h, cand_disp(fh, 1.f, dh, r), g.H);
+        float ts = sm.thr_s[j * NPART];
+        int ti = sm.thr_id[j * NPART];
+#pragma unroll
+        for (int pp = 1; pp < NPART; ++pp)
+          if (ranks_before(sm.thr_s[j * NPART + pp], sm.thr_id[j * NPART + pp], ts, ti)) {
+            ts = sm.thr_s[j * NPART + pp];
+            ti = sm.thr_id[j * NPART + pp];
+          }
+        const int idb = ((dt + g.wt) * ws + dh) * ws;
         for (int dw = 0; dw < ws; ++dw) {
           const float top = (1.f - aw) * r0p[dw] + aw * r0p[dw + 1];
           const float bot = (1.f - aw) * r1p[dw] + aw * r1p[dw + 1];
-          const float d = (1.f - ah) * top + ah * bot;
           const bool ok = okh && centre_ok(w, cand_disp(fw, 1.f, dw, r), g.W);
-          dbuf[j * WIN + dh * ws + dw] = ok ? d : -INFINITY;
+          const float d = ok ? (1.f - ah) * top + ah * bot : -INFINITY;
+          if (ranks_before(d, idb + dw, ts, ti)) {
+            const int sl = atomicAdd(&sm.nsurv[j], 1);
+            surv_s[j * WSQ + sl] = d;
+            surv_c[j * WSQ + sl] = (unsigned char)(dh * ws + dw);
+          }
         }
       }
     } else {
       // Union too wide for the LDS layout: score this frame directly.
       __syncthreads();
-      for (int e = tid; e < nq_tile * ws; e += NTHREADS) {
+      for (int e = tid; e < QN * ws; e += NTHREADS) {
         const int j = e / ws, dh = e % ws;
         const int h = y0 + j / TQW, w = x0 + j % TQW;
         if (h >= g.H || w >= g.W) continue;
         const float fh = sm.qf_h[j], fw = sm.qf_w[j];
         const float disp_h = cand_disp(fh, 1.f, dh, r);
         const bool okh = centre_ok(h, disp_h, g.H);
+        float ts = sm.thr_s[j * NPART];
+        int ti = sm.thr_id[j * NPART];
+#pragma unroll
+        for (int pp = 1; pp < NPART; ++pp)
+          if (ranks_before(sm.thr_s[j * NPART + pp], sm.thr_id[j * NPART + pp], ts, ti)) {
+            ts = sm.thr_s[j * NPART + pp];
+            ti = sm.thr_id[j * NPART + pp];
+          }
+        const int idb = ((dt + g.wt) * ws + dh) * ws;
         for (int dw = 0; dw < ws; ++dw) {
           const float disp_w = cand_disp(fw, 1.f, dw, r);
           float d = -INFINITY;
           if (okh && centre_ok(w, disp_w, g.W)) d = score_candidate(q, k, g, b, hd, t, h, w, t2, disp_h, disp_w);
-          dbuf[j * WIN + dh * ws + dw] = d;
+          if (ranks_before(d, idb + dw, ts, ti)) {
+            const int sl = atomicAdd(&sm.nsurv[j], 1);
+            surv_s[j * WSQ + sl] = d;
+            surv_c[j * WSQ + sl] = (unsigned char)(dh * ws + dw);
+          }
         }
       }
     }
     __syncthreads();
-    // ---- top-k update, one thread per query ----
-    if (tid < nq_tile) {
-      const int j = tid;
-      TopList<KLIST> lst;
+    // ---- top-k update: NPART threads per query, survivor c goes to part c % NPART ----
+    if (tid < QN * NPART) {
+      const int j = tid / NPART, pp = tid % NPART;
+      const int ns = sm.nsurv[j];
+      if (ns > pp) {
+        TopList<KLIST> lst;
+        const int lo = tid * KLIST;
 #pragma unroll
-      for (int i = 0; i < KLIST; ++i) {
-        lst.s[i] = sm.lst_s[j * KLIST + i];
-        lst.id[i] = sm.lst_id[j * KLIST + i];
-      }
-      lst.thr_s = -INFINITY;
-      lst.thr_id = 0x7fffffff;
-#pragma unroll
-      for (int i = 0; i < KLIST; ++i)
-        if (i == g.k - 1) {
-          lst.thr_s = lst.s[i];
-          lst.thr_id = lst.id[i];
+        for (int i = 0; i < KLIST; ++i) {
+          lst.s[i] = sm.lst_s[lo + i];
+          lst.id[i] = sm.lst_id[lo + i];
         }
-      const int idb = (dt + g.wt) * ws * ws;
-      for (int c = 0; c < ws * ws; ++c) lst.push(dbuf[j * WIN + c], idb + c, g.k);
+        lst.thr_s = sm.thr_s[tid];
+        lst.thr_id = sm.thr_id[tid];
+        const int idf = (dt + g.wt) * ws * ws;
+        for (int c = pp; c < ns; c += NPART) lst.push(surv_s[j * WSQ + c], idf + surv_c[j * WSQ + c], g.k);
 #pragma unroll
-      for (int i = 0; i < KLIST; ++i) {
-        sm.lst_s[j * KLIST + i] = lst.s[i];
-        sm.lst_id[j * KLIST + i] = lst.id[i];
+        for (int i = 0; i < KLIST; ++i) {
+          sm.lst_s[lo + i] = lst.s[i];
+          sm.lst_id[lo + i] = lst.id[i];
+        }
+        sm.thr_s[tid] = lst.thr_s;
+        sm.thr_id[tid] = lst.thr_id;
       }
     }
     __syncthreads();
+    if (tid < QN) sm.nsurv[tid] = 0;
   }
 
   // ---- output: complete short lists with the frames outside the clip ----
-  if (tid < nq_tile) {
+  if (tid < QN) {
     const int j = tid;
     const int h = y0 + j / TQW, w = x0 + j % TQW;
     if (h < g.H && w < g.W) {
+      // merge the partial lists
       TopList<KLIST> lst;
-#pragma unroll
-      for (int i = 0; i < KLIST; ++i) {
-        lst.s[i] = sm.lst_s[j * KLIST + i];
-        lst.id[i] = sm.lst_id[j * KLIST + i];
-      }
-      lst.thr_s = -INFINITY;
-      lst.thr_id = 0x7fffffff;
-#pragma unroll
-      for (int i = 0; i < KLIST; ++i)
-        if (i == g.k - 1) {
-          lst.thr_s = lst.s[i];
-          lst.thr_id = lst.id[i];
+      lst.init();
+      for (int pp = 0; pp < NPART; ++pp)
+        for (int i = 0; i < g.k; ++i) {
+          const int o = (j * NPART + pp) * KLIST + i;
+          lst.push(sm.lst_s[o], sm.lst_id[o], g.k);
         }
       if (lst.thr_s == -INFINITY) {
         for (int dt = -g.wt; dt <= g.wt; ++dt) {
@@ -393,7 +505,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
 // The tiled kernel handles: inner product, S_Q = S_K = 1, P <= 7, Ws <= 9, k <= 16.
 bool tile_supported(const Geo& g) {
   return g.dist == SNLS_DIST_PROD && g.s0 == 1 && g.s1 == 1.0f && g.ps <= 7 && g.ws <= tile::WSMAX &&
-         g.k >= 1 && g.k <= tile::KLIST;
+         g.k >= 1 && g.k <= tile::KLIST && (long long)g.Ch * g.HW * 4 < (1LL << 31);
 }
 
 snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
