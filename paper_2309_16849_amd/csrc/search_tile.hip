@@ -48,10 +48,11 @@ constexpr int KP = 45;                  // K row pitch (odd: spreads the 16 rows
 constexpr int QP = 21;                  // q row pitch (odd)
 constexpr int MAXBLK = 5;               // shift-column blocks: union width <= 30
 constexpr int WSMAX = 9;
+constexpr int MAXSLOT = 7;              // frames per window kept for the output (2*wt + 1 <= 7)
 constexpr int WP = WSMAX + 1;           // window-table pitch
 constexpr int WIN = WP * WP;
 constexpr int WSQ = WSMAX * WSMAX;      // candidates per query and frame
-constexpr int KLIST = 16;               // top-k capacity
+constexpr int KLIST = 16;               // largest top-k capacity
 
 // Each direct-to-LDS load fills a whole 64-word block, so the staging
 // buffers are padded to a multiple of 64 words (the padding reads as 0).
@@ -63,7 +64,7 @@ constexpr int KLD = (KST_F + 64 * 16 - 1) / (64 * 16);  // 64-word LDS loads per
 constexpr int QLD = (QST_F + 64 * 16 - 1) / (64 * 16);  // ... for q
 
 
-template <int PS>
+template <int PS, int KL>
 struct Smem {
   static constexpr int QN = (HROWS - PS + 1) * TQW;  // queries per tile
   static constexpr int NPART = QN <= 80 ? 4 : 2;     // partial top-k lists per query
@@ -72,13 +73,14 @@ struct Smem {
   float kst[2][KST_F];  // K union region chunks (double buffer); reused for the top-k survivors
   float qst[2][QST_F];  // q halo chunks
   float bw[QN * WIN];  // per-query window of box sums
-  float lst_s[QN * NPART * KLIST];  // partial lists (query-major)
-  int lst_id[QN * NPART * KLIST];
+  float lst_s[QN * NPART * KL];  // partial lists (query-major)
+  int lst_id[QN * NPART * KL];
   float thr_s[QN * NPART];  // k-th entry of each partial list
   int thr_id[QN * NPART];
   int nsurv[QN];
   int qn_h[QN], qn_w[QN];    // integer part of the offset
   float qf_h[QN], qf_w[QN];  // the offset itself
+  float fo_h[MAXSLOT * QN], fo_w[MAXSLOT * QN];  // offsets of every searched frame (for the output)
   int uni[4];                // min N_h, max N_h, min N_w, max N_w
 };
 
@@ -101,7 +103,7 @@ struct RowBox<1> {
   static SNLS_DEV float sum(float v) { return v; }
 };
 
-template <int PS>
+template <int PS, int KL>
 __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float* __restrict__ q,
                                                                       const float* __restrict__ k,
                                                                       const float* __restrict__ flows, Geo g,
@@ -112,9 +114,9 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
   constexpr int TQH = HROWS - PS + 1;
   constexpr int HW = TQW + PS - 1;
   constexpr int LO = -(PS / 2);
-  constexpr int QN = Smem<PS>::QN;
-  constexpr int NPART = Smem<PS>::NPART;
-  __shared__ Smem<PS> sm;
+  constexpr int QN = Smem<PS, KL>::QN;
+  constexpr int NPART = Smem<PS, KL>::NPART;
+  __shared__ Smem<PS, KL> sm;
 
   const int tid = threadIdx.x;
   const int lane16 = tid & 15;
@@ -138,7 +140,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
 
   const float* qb = q + (((long long)b * g.T + t) * g.C + (long long)hd * g.Ch) * g.HW;
 
-  for (int i = tid; i < QN * NPART * KLIST; i += NTHREADS) {
+  for (int i = tid; i < QN * NPART * KL; i += NTHREADS) {
     sm.lst_s[i] = -INFINITY;
     sm.lst_id[i] = 0x7fffffff;
   }
@@ -196,24 +198,40 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
       first = false;
     }
     __syncthreads();
-    if (tid < QN) {
+    {
       const int jh = tid / TQW, jw = tid % TQW;
-      const bool inside = y0 + jh < g.H && x0 + jw < g.W;
+      const bool inside = tid < QN && y0 + jh < g.H && x0 + jw < g.W;
       const float fh = fh_next, fw = fw_next;
       int nh = 0, nw = 0;
       // Offsets that are not finite or absurdly large leave the union alone;
       // their candidates fail the exact validity test below.
       if (fabsf(fh) < 1.0e6f) nh = (int)floorf(fh);
       if (fabsf(fw) < 1.0e6f) nw = (int)floorf(fw);
-      sm.qn_h[tid] = nh;
-      sm.qn_w[tid] = nw;
-      sm.qf_h[tid] = fh;
-      sm.qf_w[tid] = fw;
-      if (inside) {
-        atomicMin(&sm.uni[0], nh);
-        atomicMax(&sm.uni[1], nh);
-        atomicMin(&sm.uni[2], nw);
-        atomicMax(&sm.uni[3], nw);
+      if (tid < QN) {
+        sm.qn_h[tid] = nh;
+        sm.qn_w[tid] = nw;
+        sm.qf_h[tid] = fh;
+        sm.qf_w[tid] = fw;
+        sm.fo_h[(dt + g.wt) * QN + tid] = fh;
+        sm.fo_w[(dt + g.wt) * QN + tid] = fw;
+      }
+      // union bounds: wave reductions, then one LDS atomic per wave
+      if (tid < ((QN + 63) & ~63)) {
+        int a0 = inside ? nh : INT_MAX, a1 = inside ? nh : INT_MIN;
+        int a2 = inside ? nw : INT_MAX, a3 = inside ? nw : INT_MIN;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+          a0 = min(a0, __shfl_xor(a0, off));
+          a1 = max(a1, __shfl_xor(a1, off));
+          a2 = min(a2, __shfl_xor(a2, off));
+          a3 = max(a3, __shfl_xor(a3, off));
+        }
+        if ((tid & 63) == 0) {
+          atomicMin(&sm.uni[0], a0);
+          atomicMax(&sm.uni[1], a1);
+          atomicMin(&sm.uni[2], a2);
+          atomicMax(&sm.uni[3], a3);
+        }
       }
     }
     // next searched frame's offsets, in flight during this frame
@@ -434,10 +452,10 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
       const int j = tid / NPART, pp = tid % NPART;
       const int ns = sm.nsurv[j];
       if (ns > pp) {
-        TopList<KLIST> lst;
-        const int lo = tid * KLIST;
+        TopList<KL> lst;
+        const int lo = tid * KL;
 #pragma unroll
-        for (int i = 0; i < KLIST; ++i) {
+        for (int i = 0; i < KL; ++i) {
           lst.s[i] = sm.lst_s[lo + i];
           lst.id[i] = sm.lst_id[lo + i];
         }
@@ -446,7 +464,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
         const int idf = (dt + g.wt) * ws * ws;
         for (int c = pp; c < ns; c += NPART) lst.push(surv_s[j * WSQ + c], idf + surv_c[j * WSQ + c], g.k);
 #pragma unroll
-        for (int i = 0; i < KLIST; ++i) {
+        for (int i = 0; i < KL; ++i) {
           sm.lst_s[lo + i] = lst.s[i];
           sm.lst_id[lo + i] = lst.id[i];
         }
@@ -464,11 +482,11 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
     const int h = y0 + j / TQW, w = x0 + j % TQW;
     if (h < g.H && w < g.W) {
       // merge the partial lists
-      TopList<KLIST> lst;
+      TopList<KL> lst;
       lst.init();
       for (int pp = 0; pp < NPART; ++pp)
         for (int i = 0; i < g.k; ++i) {
-          const int o = (j * NPART + pp) * KLIST + i;
+          const int o = (j * NPART + pp) * KL + i;
           lst.push(sm.lst_s[o], sm.lst_id[o], g.k);
         }
       if (lst.thr_s == -INFINITY) {
@@ -482,15 +500,20 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
       float* irow = inds + row * g.k * 3;
       const long long pix = (long long)h * g.W + w;
 #pragma unroll
-      for (int i = 0; i < KLIST; ++i) {
+      for (int i = 0; i < KL; ++i) {
         if (i < g.k) {
           const int cid = lst.id[i];
           const int dw = cid % ws, dh = (cid / ws) % ws, dt = cid / (ws * ws) - g.wt;
           float fh = 0.f, fw = 0.f;
           if (dt != 0) {
-            long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dt, g.wt)) * 2;
-            fh = flows[base * g.HW + pix];
-            fw = flows[(base + 1) * g.HW + pix];
+            if (t + dt >= 0 && t + dt < g.T) {  // searched: offsets kept in LDS
+              fh = sm.fo_h[(dt + g.wt) * QN + j];
+              fw = sm.fo_w[(dt + g.wt) * QN + j];
+            } else {
+              long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dt, g.wt)) * 2;
+              fh = flows[base * g.HW + pix];
+              fw = flows[(base + 1) * g.HW + pix];
+            }
           }
           drow[i] = lst.s[i];
           irow[3 * i + 0] = (float)(t + dt);
@@ -505,7 +528,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
 // The tiled kernel handles: inner product, S_Q = S_K = 1, P <= 7, Ws <= 9, k <= 16.
 bool tile_supported(const Geo& g) {
   return g.dist == SNLS_DIST_PROD && g.s0 == 1 && g.s1 == 1.0f && g.ps <= 7 && g.ws <= tile::WSMAX &&
-         g.k >= 1 && g.k <= tile::KLIST && (long long)g.Ch * g.HW * 4 < (1LL << 31);
+         g.k >= 1 && g.k <= tile::KLIST && 2 * g.wt + 1 <= tile::MAXSLOT && (long long)g.Ch * g.HW * 4 < (1LL << 31);
 }
 
 snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
@@ -517,11 +540,16 @@ snls_status launch_search_tile(const float* q, const float* k, const float* flow
   if (nwg == 0) return SNLS_OK;
   if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
   dim3 grid((unsigned)nwg), block(tile::NTHREADS);
+  const bool small_k = g.k <= 12;
   switch (g.ps) {
-#define SNLS_TILE_CASE(P)                                                                                  \
-  case P:                                                                                                  \
-    hipLaunchKernelGGL(search_tile_kernel<P>, grid, block, 0, s, q, k, flows, g, tiles_x, tiles_y, dists, \
-                       inds);                                                                              \
+#define SNLS_TILE_CASE(P)                                                                                     \
+  case P:                                                                                                     \
+    if (small_k)                                                                                              \
+      hipLaunchKernelGGL((search_tile_kernel<P, 12>), grid, block, 0, s, q, k, flows, g, tiles_x, tiles_y,     \
+                         dists, inds);                                                                        \
+    else                                                                                                      \
+      hipLaunchKernelGGL((search_tile_kernel<P, 16>), grid, block, 0, s, q, k, flows, g, tiles_x, tiles_y,     \
+                         dists, inds);                                                                        \
     break;
     SNLS_TILE_CASE(1)
     SNLS_TILE_CASE(2)
