@@ -69,6 +69,86 @@ def measured_traffic():
     return rec.get("bytes_per_launch")
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "search_denoise480x854_traffic.json")
+SEARCH_KERNEL = "search_tile_kernel"
+COPY_KERNEL_HINT = "mulfunctor"  # torch.mul(src, 1, out=dst): one read and one write per element
+
+
+def _read_csv(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def _find(dirpath, suffix):
+    for root, _, files in os.walk(dirpath):
+        for fn in files:
+            if fn.endswith(suffix):
+                return os.path.join(root, fn)
+    raise FileNotFoundError("%s*%s" % (dirpath, suffix))
+
+
+def summarize_profiles(outdir, copy_mib):
+    """Turn the rocprofv3 outputs of the profiling commands (kernel trace,
+    FETCH_SIZE pass, WRITE_SIZE pass, counter passes) into the summaries kept
+    under profiles/.  HBM traffic per search launch = counter KiB scaled by
+    what the same counter reads for a plain copy of copy_mib MiB."""
+    import collections
+    cmd = ("cd /tmp && rocprofv3 {opts} --output-format csv -d $R/gpurun_out/{d} -o run -- "
+           "python3 $R/bench.py --steps {s} --warmup {w} --no-cpu-baseline --copy-probe-mib %d" % copy_mib)
+    lines = ["# rocprofv3 summary: 480x854 denoising workload (search + top-k + aggregation)", "",
+             "Commands (R = repository root on the GPU box):", ""]
+    lines.append("    " + cmd.format(opts="--kernel-trace --stats", d="prof_trace", s=10, w=2))
+    trace = _read_csv(_find(os.path.join(outdir, "prof_trace"), "kernel_stats.csv"))
+    lines += ["", "| kernel | calls | avg us | min us | max us | total % |", "|---|---|---|---|---|---|"]
+    for r in trace:
+        name = r["Name"]
+        short = name.split("(")[0].replace("void ", "")[:70]
+        lines.append("| %s | %s | %.1f | %.1f | %.1f | %.1f |" % (
+            short, r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3,
+            float(r["Percentage"])))
+    counters = collections.defaultdict(dict)
+    for d in sorted(os.listdir(outdir)):
+        if not d.startswith("prof_pmc") or not os.path.isdir(os.path.join(outdir, d)):
+            continue
+        rows = _read_csv(_find(os.path.join(outdir, d), "counter_collection.csv"))
+        names = sorted({r["Counter_Name"] for r in rows})
+        lines += ["", "    " + cmd.format(opts="--pmc " + " ".join(names), d=d, s=2, w=1)]
+        acc = collections.defaultdict(list)
+        for r in rows:
+            acc[(r["Kernel_Name"], r["Counter_Name"])].append(float(r["Counter_Value"]))
+        for (kn, cn), v in acc.items():
+            counters[kn][cn] = sum(v) / len(v)
+    lines += ["", "Counters, mean per dispatch:", "", "| kernel | counter | value |", "|---|---|---|"]
+    for kn in sorted(counters):
+        for cn in sorted(counters[kn]):
+            lines.append("| %s | %s | %.6g |" % (kn.split("(")[0].replace("void ", "")[:60], cn, counters[kn][cn]))
+    search = [kn for kn in counters if SEARCH_KERNEL in kn]
+    copy = [kn for kn in counters if COPY_KERNEL_HINT in kn.lower() and "FETCH_SIZE" in counters[kn]]
+    rec = None
+    if search and copy:
+        s, cpy = counters[search[0]], counters[copy[0]]
+        exp_kib = copy_mib * 1024.0
+        f_fetch = exp_kib / cpy["FETCH_SIZE"]
+        f_write = exp_kib / cpy["WRITE_SIZE"]
+        fetch_b = s["FETCH_SIZE"] * f_fetch * 1024.0
+        write_b = s["WRITE_SIZE"] * f_write * 1024.0
+        rec = {"kernel": search[0], "kernel_source_hash": kernel_source_hash(), "copy_kernel": copy[0],
+               "copy_mib": copy_mib, "copy_fetch_kib": cpy["FETCH_SIZE"], "copy_write_kib": cpy["WRITE_SIZE"],
+               "fetch_scale": f_fetch, "write_scale": f_write, "search_fetch_kib": s["FETCH_SIZE"],
+               "search_write_kib": s["WRITE_SIZE"], "fetch_bytes_per_launch": fetch_b,
+               "write_bytes_per_launch": write_b, "bytes_per_launch": fetch_b + write_b}
+        with open(TRAFFIC_FILE, "w") as f:
+            json.dump(rec, f, indent=1)
+        lines += ["", "HBM traffic of one search launch: FETCH %.1f MB + WRITE %.1f MB = %.1f MB "
+                  "(counter KiB x %.3f / %.3f, from a %d MiB copy)." % (
+                      fetch_b / 1e6, write_b / 1e6, (fetch_b + write_b) / 1e6, f_fetch, f_write, copy_mib)]
+    md = os.path.join(ROOT, "profiles", "search_denoise480x854_rocprofv3.md")
+    with open(md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    return md, rec
+
+
 def cpu_baseline(c, budget_s=12.0):
     """The oracle on the host cores: search + top-k + aggregation for a band of
     query rows of the middle frame, scaled to queries/s."""
@@ -120,7 +200,16 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="also run one plain device copy of this size (calibrates the HBM byte counters)")
+    ap.add_argument("--summarize-profiles", metavar="DIR", default=None,
+                    help="write profiles/ summaries from the rocprofv3 outputs under DIR and exit")
     args = ap.parse_args()
+    if args.summarize_profiles:
+        md, rec = summarize_profiles(args.summarize_profiles, args.copy_probe_mib or 256)
+        print(md)
+        print(json.dumps(rec, indent=1))
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the path has no multi-GPU mode in this build "
               "(see DESIGN.md for how it would shard)", file=sys.stderr)
@@ -153,6 +242,14 @@ def main():
         if ev is not None:
             ev[2].record()
 
+    if args.copy_probe_mib:
+        src = torch.empty(args.copy_probe_mib * (1 << 20) // 4, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1.0)
+        torch.cuda.synchronize()
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()

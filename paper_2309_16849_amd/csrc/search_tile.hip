@@ -41,6 +41,7 @@ constexpr int TQW = 8;                  // tile width (queries)
 constexpr int HROWS = 16;               // halo rows = lanes per group
 constexpr int NGROUP = 64;              // groups per workgroup
 constexpr int NTHREADS = HROWS * NGROUP;
+static_assert(NTHREADS / 64 == HROWS, "q staging maps one halo row to each wave");
 constexpr int S = 6;                    // shift columns per task
 constexpr int CC = 4;                   // channels per staging chunk (double-buffered)
 constexpr int KR = 36;                  // K rows in LDS
@@ -60,8 +61,6 @@ constexpr int KST_F = (CC * KR * KP + 63) / 64 * 64;     // 6528 floats
 constexpr int QST_F = (CC * HROWS * QP + 63) / 64 * 64;  // 1344
 // all direct-to-LDS targets (placed first in LDS) stay below 64 KB
 static_assert((2 * KST_F + 2 * QST_F) * 4 <= 65536, "staging buffers must sit in the first 64 KB of LDS");
-constexpr int KLD = (KST_F + 64 * 16 - 1) / (64 * 16);  // 64-word LDS loads per wave for K
-constexpr int QLD = (QST_F + 64 * 16 - 1) / (64 * 16);  // ... for q
 
 
 template <int PS, int KL>
@@ -127,9 +126,11 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
   const long long nwg = (long long)gridDim.x;
   const long long xcd = blockIdx.x % 8, xq = nwg / 8, xrem = nwg % 8;
   const long long wg = xcd * xq + (xcd < xrem ? xcd : xrem) + blockIdx.x / 8;
-  const long long tiles_img = (long long)tiles_x * tiles_y;
-  const int img = (int)(wg / tiles_img);
-  const int trem = (int)(wg % tiles_img);
+  // The query frames (and heads, batch entries) of one tile are consecutive
+  // workgroups, so the key frames they share stay in the XCD's L2.
+  const int nimg = g.B * g.HD * g.T;
+  const int img = (int)(wg % nimg);
+  const int trem = (int)(wg / nimg);
   const int ty = trem / tiles_x, tx = trem % tiles_x;
   const int t = img % g.T;
   const int hd = (img / g.T) % g.HD;
@@ -150,22 +151,13 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
   }
   if (tid < QN) sm.nsurv[tid] = 0;
 
-  // Direct-to-LDS staging: each 64-lane buffer load fills 64 consecutive LDS
-  // words; lane i of load m carries word 64*m + i of the chunk layout
-  // [c][row][pitch].  Positions outside the frame (or padding) use an
-  // out-of-range offset, which the buffer unit returns as 0.
+  // Direct-to-LDS staging: one 64-lane buffer load fills one LDS row of a
+  // chunk (lane = column; lanes past the row width are masked off), so the
+  // row part of the address is wave-uniform and a lane only keeps its column.
+  // Positions outside the frame use an out-of-range offset, read as 0.
   const int wave = tid >> 6, lane = tid & 63;
   constexpr unsigned OOB = 0x80000000u;
-  unsigned q_off[QLD];
-#pragma unroll
-  for (int m = 0; m < QLD; ++m) {
-    const int wrd = (wave + 16 * m) * 64 + lane;
-    const int c = wrd / (HROWS * QP), rem = wrd % (HROWS * QP);
-    const int yy = rem / QP, xx = rem % QP;
-    const int gy = Y0 + yy, gx = X0 + xx;
-    const bool ok = c < CC && xx < HW && gy >= 0 && gy < g.H && gx >= 0 && gx < g.W;
-    q_off[m] = ok ? (unsigned)(((long long)c * g.HW + (long long)gy * g.W + gx) * 4) : OOB;
-  }
+  const bool q_col_in = lane < HW && X0 + lane >= 0 && X0 + lane < g.W;
   const __amdgpu_buffer_rsrc_t q_rs =
       __builtin_amdgcn_make_buffer_rsrc((void*)qb, (short)0, (int)(g.Ch * g.HW * 4), 0x00020000);
 
@@ -269,17 +261,9 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
         const int blk = task % nblk;
         const int krow = lane16 + d_h - dh_lo;
 
-        // K staging offsets of this thread for this round
-        unsigned k_off[KLD];
-#pragma unroll
-        for (int m = 0; m < KLD; ++m) {
-          const int wrd = (wave + 16 * m) * 64 + lane;
-          const int c = wrd / (KR * KP), rem = wrd % (KR * KP);
-          const int yy = rem / KP, xx = rem % KP;
-          const int gy = Y0 + dh_lo + yy, gx = X0 + dmin_w + xx;
-          const bool ok = c < CC && yy < krows && xx < kcols && gy >= 0 && gy < g.H && gx >= 0 && gx < g.W;
-          k_off[m] = ok ? (unsigned)(((long long)c * g.HW + (long long)gy * g.W + gx) * 4) : OOB;
-        }
+        // K staging: this lane's column of the round's region
+        const int k_gx = X0 + dmin_w + lane;
+        const bool k_col_in = lane < kcols && k_gx >= 0 && k_gx < g.W;
 
         float acc[HW][S];
 #pragma unroll
@@ -287,29 +271,40 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
 #pragma unroll
           for (int i = 0; i < S; ++i) acc[x][i] = 0.f;
 
-        // issue the asynchronous loads of chunk c0 into buffer bsel
+        // issue the asynchronous loads of chunk c0 into buffer bsel: K rows
+        // (c, row) and q rows (c, row) are spread over the 16 waves
         auto issue = [&](int c0, int bsel) {
-          const unsigned cshift = (unsigned)(c0 * g.HW * 4);
-          const int cvalid = g.Ch - c0;  // channels of this chunk inside the head
-#pragma unroll
-          for (int m = 0; m < KLD; ++m) {
-            const int wbase = (wave + 16 * m) * 64;
-            if (wbase < KST_F) {
-              const int c = (wbase + lane) / (KR * KP);
-              const unsigned off = (k_off[m] == OOB || c >= cvalid) ? OOB : k_off[m] + cshift;
+          const int nk = CC * krows;
+          int c = 0, row = wave;  // (channel, row) of K row rr = wave + 16*i, kept incrementally
+          while (row >= krows) {
+            row -= krows;
+            ++c;
+          }
+          for (int rr = wave; rr < nk; rr += 16) {
+            const int gy = Y0 + dh_lo + row;
+            const bool rin = c0 + c < g.Ch && gy >= 0 && gy < g.H;
+            const unsigned off = (rin && k_col_in)
+                ? (unsigned)(((long long)(c0 + c) * g.HW + (long long)gy * g.W + k_gx) * 4) : OOB;
+            if (lane < kcols)
               __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                  k_rs, (__attribute__((address_space(3))) void*)&sm.kst[bsel][wbase], 4, off, 0, 0, 0);
+                  k_rs, (__attribute__((address_space(3))) void*)&sm.kst[bsel][(c * KR + row) * KP], 4, off, 0, 0, 0);
+            row += 16;
+            while (row >= krows) {
+              row -= krows;
+              ++c;
             }
           }
+          // q: HROWS == 16 rows per channel, so wave w loads row w of every channel
 #pragma unroll
-          for (int m = 0; m < QLD; ++m) {
-            const int wbase = (wave + 16 * m) * 64;
-            if (wbase < QST_F) {
-              const int c = (wbase + lane) / (HROWS * QP);
-              const unsigned off = (q_off[m] == OOB || c >= cvalid) ? OOB : q_off[m] + cshift;
+          for (int cq = 0; cq < CC; ++cq) {
+            const int gy = Y0 + wave;
+            const bool rin = c0 + cq < g.Ch && gy >= 0 && gy < g.H;
+            const unsigned off = (rin && q_col_in)
+                ? (unsigned)(((long long)(c0 + cq) * g.HW + (long long)gy * g.W + X0 + lane) * 4) : OOB;
+            if (lane < HW)
               __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                  q_rs, (__attribute__((address_space(3))) void*)&sm.qst[bsel][wbase], 4, off, 0, 0, 0);
-            }
+                  q_rs, (__attribute__((address_space(3))) void*)&sm.qst[bsel][(cq * HROWS + wave) * QP], 4, off, 0, 0,
+                  0);
           }
         };
         __syncthreads();  // buffers of the previous round / frame are free
