@@ -89,18 +89,77 @@ struct Smem {
 // source lies past the end of the row read 0.
 template <int N>
 SNLS_DEV float row_shl(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + N, 0xf, 0xf, true));
+  if constexpr (N == 0) return v;
+  else return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x100 + N, 0xf, 0xf, true));
 }
+
+// Box sums of width P <= 7 as a sum of power-of-two boxes (P = 4a + 2b + c):
+// b2(i) = v(i) + v(i+1), b4(i) = b2(i) + b2(i+2), box(i) = b4(i) + b2(i+4a)
+// + v(i+4a+2b) for the terms present.  At most 4 additions instead of P-1.
+template <int P>
+struct Pow2Box {
+  static_assert(P >= 1 && P <= 7, "box width");
+  static constexpr int O2 = (P & 4) ? 4 : 0;          // offset of the width-2 term
+  static constexpr int O1 = O2 + ((P & 2) ? 2 : 0);   // offset of the width-1 term
+};
 
 // Sum of lanes i .. i+P-1 of the 16-lane row (a box sum down the halo rows).
 template <int P>
-struct RowBox {
-  static SNLS_DEV float sum(float v) { return RowBox<P - 1>::sum(v) + row_shl<P - 1>(v); }
-};
-template <>
-struct RowBox<1> {
-  static SNLS_DEV float sum(float v) { return v; }
-};
+SNLS_DEV float row_box(float v) {
+  using B = Pow2Box<P>;
+  if constexpr (P == 1) {
+    return v;
+  } else {
+    const float b2 = v + row_shl<1>(v);
+    float r;
+    if constexpr ((P & 4) != 0) {
+      r = b2 + row_shl<2>(b2);
+      if constexpr ((P & 2) != 0) r += row_shl<B::O2>(b2);
+    } else {
+      r = b2;
+    }
+    if constexpr ((P & 1) != 0) r += row_shl<B::O1>(v);
+    return r;
+  }
+}
+
+// In-place horizontal box sums of one shift column: a[x] becomes
+// a[x] + ... + a[x+P-1] for x < N (the array holds N + P - 1 values).
+template <int P, int N, int L, int S, int I>
+SNLS_DEV void row_box_regs(float (&a)[L][S]) {
+  static_assert(L == N + P - 1, "array length");
+  using B = Pow2Box<P>;
+  if constexpr (P > 1) {
+    float b2[L - 1];
+#pragma unroll
+    for (int x = 0; x < L - 1; ++x) b2[x] = a[x][I] + a[x + 1][I];
+    float b4[(P & 4) ? L - 3 : 1];
+    if constexpr ((P & 4) != 0) {
+#pragma unroll
+      for (int x = 0; x < L - 3; ++x) b4[x] = b2[x] + b2[x + 2];
+    }
+#pragma unroll
+    for (int x = 0; x < N; ++x) {  // ascending x: a[x + O1] (O1 >= 1) is not yet overwritten
+      float r;
+      if constexpr ((P & 4) != 0) {
+        r = b4[x];
+        if constexpr ((P & 2) != 0) r += b2[x + B::O2];
+      } else {
+        r = b2[x];
+      }
+      if constexpr ((P & 1) != 0) r += a[x + B::O1][I];
+      a[x][I] = r;
+    }
+  }
+}
+
+template <int P, int N, int L, int S, int I = 0>
+SNLS_DEV void box_cols(float (&a)[L][S]) {
+  if constexpr (I < S) {
+    row_box_regs<P, N, L, S, I>(a);
+    box_cols<P, N, L, S, I + 1>(a);
+  }
+}
 
 template <int PS, int KL>
 __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float* __restrict__ q,
@@ -176,7 +235,13 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
   float fh_next = 0.f, fw_next = 0.f;
   bool first = true;
 
-  for (int dt = -g.wt; dt <= g.wt; ++dt) {
+  // Frames are searched nearest first (dt = 0, -1, +1, -2, +2, ...): the
+  // query frame's own matches raise the top-k thresholds early, so fewer
+  // candidates of the later frames survive the filter.  Candidate ids do
+  // not depend on this order, and neither does the result.
+  auto frame_dt = [](int s) { return (s & 1) ? -((s + 1) >> 1) : (s >> 1); };
+  for (int si = 0; si <= 2 * g.wt; ++si) {
+    const int dt = frame_dt(si);
     const int t2 = t + dt;
     if (t2 < 0 || t2 >= g.T) continue;
     const float* kb = k + (((long long)b * g.T + t2) * g.C + (long long)hd * g.Ch) * g.HW;
@@ -228,9 +293,9 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
     }
     // next searched frame's offsets, in flight during this frame
     {
-      int dn = dt + 1;
-      while (dn <= g.wt && (t + dn < 0 || t + dn >= g.T)) ++dn;
-      if (dn <= g.wt) fetch_flow(dn, fh_next, fw_next);
+      int sn = si + 1;
+      while (sn <= 2 * g.wt && (t + frame_dt(sn) < 0 || t + frame_dt(sn) >= g.T)) ++sn;
+      if (sn <= 2 * g.wt) fetch_flow(frame_dt(sn), fh_next, fw_next);
     }
     __syncthreads();
     const int dmin_h = sm.uni[0] - r, UH = sm.uni[1] - sm.uni[0] + ws + 1;
@@ -337,19 +402,13 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
         }
 
         // horizontal box over the patch width, in place (registers)
-#pragma unroll
-        for (int jw = 0; jw < TQW; ++jw)
-#pragma unroll
-          for (int i = 0; i < S; ++i) {
-#pragma unroll
-            for (int pw = 1; pw < PS; ++pw) acc[jw][i] += acc[jw + pw][i];
-          }
+        box_cols<PS, TQW, HW, S>(acc);
         // vertical box over the patch height, across the 16 lanes of the group
 #pragma unroll
         for (int jw = 0; jw < TQW; ++jw)
 #pragma unroll
           for (int i = 0; i < S; ++i) {
-            float s = RowBox<PS>::sum(acc[jw][i]);
+            float s = row_box<PS>(acc[jw][i]);
             asm volatile("" : "+v"(s));  // materialise the sum here: keeps the row moves short-lived
             acc[jw][i] = s;
           }
@@ -476,14 +535,52 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
     const int j = tid;
     const int h = y0 + j / TQW, w = x0 + j % TQW;
     if (h < g.H && w < g.W) {
-      // merge the partial lists
+      // merge the sorted partial lists (only their first k entries are kept)
       TopList<KL> lst;
       lst.init();
-      for (int pp = 0; pp < NPART; ++pp)
-        for (int i = 0; i < g.k; ++i) {
-          const int o = (j * NPART + pp) * KL + i;
-          lst.push(sm.lst_s[o], sm.lst_id[o], g.k);
+      {
+        float hs[NPART];
+        int hid[NPART], hp[NPART];
+#pragma unroll
+        for (int pp = 0; pp < NPART; ++pp) {
+          hp[pp] = 0;
+          hs[pp] = sm.lst_s[(j * NPART + pp) * KL];
+          hid[pp] = sm.lst_id[(j * NPART + pp) * KL];
         }
+#pragma unroll
+        for (int i = 0; i < KL; ++i) {
+          if (i < g.k) {
+            float bs = hs[0];
+            int bi = hid[0], bp = 0, np = hp[0] + 1;
+#pragma unroll
+            for (int pp = 1; pp < NPART; ++pp)
+              if (ranks_before(hs[pp], hid[pp], bs, bi)) {
+                bs = hs[pp];
+                bi = hid[pp];
+                bp = pp;
+                np = hp[pp] + 1;
+              }
+            lst.s[i] = bs;
+            lst.id[i] = bi;
+            const int o = (j * NPART + bp) * KL + min(np, KL - 1);
+            const float ns = np < g.k ? sm.lst_s[o] : -INFINITY;
+            const int nid = np < g.k ? sm.lst_id[o] : 0x7fffffff;
+#pragma unroll
+            for (int pp = 0; pp < NPART; ++pp)
+              if (pp == bp) {
+                hp[pp] = np;
+                hs[pp] = ns;
+                hid[pp] = nid;
+              }
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < KL; ++i)
+          if (i == g.k - 1) {
+            lst.thr_s = lst.s[i];
+            lst.thr_id = lst.id[i];
+          }
+      }
       if (lst.thr_s == -INFINITY) {
         for (int dt = -g.wt; dt <= g.wt; ++dt) {
           if (t + dt >= 0 && t + dt < g.T) continue;
