@@ -37,7 +37,11 @@
  *    (F = 0 for dt = 0); its id is ((dt+wt)*ws + d_h)*ws + d_w.  It is
  *    invalid when frame t+dt is outside [0,T) or its centre (h+disp_h,
  *    w+disp_w) is outside [0,H-1]x[0,W-1]; invalid candidates score -inf
- *    (inner product) or +inf (squared L2).
+ *    (inner product) or +inf (squared L2).  A candidate whose similarity is
+ *    NaN (only with non-finite inputs) scores as an invalid one, so no NaN
+ *    score is ever returned or ranked.  With non-finite inputs the scores are
+ *    otherwise unspecified, but every kept neighbour is a candidate of the
+ *    query's own window.
  *  - Similarity of a valid candidate: sum over patch offsets
  *    p in {-(ps/2) .. ps-1-(ps/2)}^2 with the query pixel (h+p_h, w+p_w)
  *    inside the frame, and over the head's channels, of q*k~ (inner product,

@@ -32,7 +32,9 @@
  *  - bilinear sampling with pixel centres on integers, taps outside the frame
  *    read 0, query patch pixels outside the frame are skipped;
  *  - a candidate whose centre lies outside [0,H-1]x[0,W-1] is invalid and
- *    scores -inf (inner product) or +inf (squared L2);
+ *    scores -inf (inner product) or +inf (squared L2); so does a candidate
+ *    whose similarity is not a number (non-finite inputs), so that every
+ *    score is ordered;
  *  - top-k is joint over all frames of the window, best first, ties to the
  *    smaller candidate id ((dt+wt)*Ws + dh)*Ws + dw;
  *  - aggregation weights are softmax(sign*scale*d) over the k entries
@@ -212,7 +214,8 @@ void oracle_search(const double* q, const double* k, const double* flows, const 
           if (tk < 0 || tk >= p->T || !centre_in_frame(p, h, w, disp_h, disp_w)) {
             dists[o] = bad;
           } else {
-            dists[o] = similarity(q, k, p, b, hd, t, h, w, tk, disp_h, disp_w);
+            double d = similarity(q, k, p, b, hd, t, h, w, tk, disp_h, disp_w);
+            dists[o] = isnan(d) ? bad : d;
           }
         }
       }

@@ -109,7 +109,7 @@ __global__ void __launch_bounds__(128) search_topk_direct_kernel(const float* __
 #pragma unroll
   for (int i = 0; i < KMAX; ++i) {
     if (i < g.k) {
-      int cid = lst.id[i];
+      int cid = min(lst.id[i], g.ncand - 1);  // every candidate was ranked: ids are real
       int dw = cid % g.ws;
       int dh = (cid / g.ws) % g.ws;
       int dt = cid / (g.ws * g.ws) - g.wt;

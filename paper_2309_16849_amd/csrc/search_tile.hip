@@ -461,7 +461,8 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
           const float top = (1.f - aw) * r0p[dw] + aw * r0p[dw + 1];
           const float bot = (1.f - aw) * r1p[dw] + aw * r1p[dw + 1];
           const bool ok = okh && centre_ok(w, cand_disp(fw, 1.f, dw, r), g.W);
-          const float d = ok ? (1.f - ah) * top + ah * bot : -INFINITY;
+          const float dv = (1.f - ah) * top + ah * bot;
+          const float d = ok && dv == dv ? dv : -INFINITY;  // NaN scores as invalid
           if (ranks_before(d, idb + dw, ts, ti)) {
             const int sl = atomicAdd(&sm.nsurv[j], 1);
             surv_s[j * WSQ + sl] = d;
@@ -594,7 +595,9 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
 #pragma unroll
       for (int i = 0; i < KL; ++i) {
         if (i < g.k) {
-          const int cid = lst.id[i];
+          // every candidate of the window was ranked, so the k best are real
+          // candidates; the clamp only keeps a placeholder id in bounds
+          const int cid = min(lst.id[i], g.ncand - 1);
           const int dw = cid % ws, dh = (cid / ws) % ws, dt = cid / (ws * ws) - g.wt;
           float fh = 0.f, fw = 0.f;
           if (dt != 0) {

@@ -146,7 +146,8 @@ SNLS_DEV float score_candidate(const float* __restrict__ q, const float* __restr
       }
     }
   }
-  return acc;
+  // a NaN similarity (non-finite inputs) scores as an invalid candidate
+  return acc != acc ? from_score(-INFINITY, g.dist) : acc;
 }
 
 // Sorted top-K list in registers, best first.  KMAX is the capacity; only

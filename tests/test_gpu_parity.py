@@ -145,6 +145,113 @@ def _swap_mask(p, swaps):
     return mask
 
 
+# ------------------------------------------------------ tiled kernel --
+# Cases inside the tiled kernel's domain (inner product, S_Q = S_K = 1,
+# P <= 7, Ws <= 9, k <= 16, 2wt+1 <= 7): every patch size, ragged tiles and
+# channel chunks, narrow shift unions (few tasks: channel-split groups),
+# wide ones (several rounds) and unions too wide for the LDS layout (the
+# per-candidate fallback).
+
+def _tile_cases(n=18, seed=31):
+    r = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        HD = int(r.choice([1, 2]))
+        ps = 1 + i % 7
+        p = small_params(B=int(r.choice([1, 2])), T=int(r.choice([1, 2, 3, 5])), HD=HD,
+                         C=HD * int(r.choice([1, 3, 4, 6, 9])), H=int(r.choice([5, 17, 23, 31])),
+                         W=int(r.choice([6, 16, 19, 41])), ws=int(r.choice([1, 2, 4, 5, 7, 8, 9])),
+                         wt=int(r.choice([0, 1, 2, 3])), ps=ps, stride0=1, stride1=1.0, dist_type=0)
+        nc = (2 * p["wt"] + 1) * p["ws"] ** 2
+        p["k"] = int(min(nc, r.choice([1, 5, 10, 12, 13, 16])))
+        kind = ["frac", "smooth", "int", "wide", "far"][i % 5]
+        cases.append((p, kind))
+    return cases
+
+
+TILE_CASES = _tile_cases()
+TILE_IDS = ["t%d-ws%d-wt%d-ps%d-k%d-%s" % (i, p["ws"], p["wt"], p["ps"], p["k"], kd)
+            for i, (p, kd) in enumerate(TILE_CASES)]
+
+
+def _tile_flows(p, kind, r):
+    fshp = (p["B"], p["T"], 2 * p["wt"], 2, p["H"], p["W"])
+    if kind == "smooth":  # one offset per frame pair plus a little jitter: small union
+        base = r.uniform(-4, 4, fshp[:4] + (1, 1))
+        return (base + r.uniform(-0.4, 0.4, fshp)).astype(np.float32)
+    if kind == "wide":  # spread of about 14 px: several rounds of shift rows
+        return r.uniform(-7, 7, fshp).astype(np.float32)
+    if kind == "far":  # +-60 px: the union exceeds the LDS layout
+        return (r.choice([-1.0, 1.0], fshp) * 60.0 + r.uniform(-1, 1, fshp)).astype(np.float32)
+    if kind == "int":
+        return r.integers(-3, 4, fshp).astype(np.float32)
+    return r.uniform(-3, 3, fshp).astype(np.float32)
+
+
+@pytest.mark.parametrize("case", range(len(TILE_CASES)), ids=TILE_IDS)
+def test_tiled_search_topk(dev, case):
+    p, kind = TILE_CASES[case]
+    r = np.random.default_rng(8000 + case)
+    shp = (p["B"], p["T"], p["C"], p["H"], p["W"])
+    q = r.standard_normal(shp, dtype=np.float32)
+    k = r.standard_normal(shp, dtype=np.float32)
+    flows = _tile_flows(p, kind, r)
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    torch.cuda.synchronize()
+    res = oracle.search(q, k, flows, p)
+    compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
+
+
+# --------------------------------------------------- non-finite inputs --
+
+@pytest.mark.parametrize("dist_type,ps,ws", [(0, 3, 5), (0, 7, 9), (1, 3, 5), (0, 4, 8)])
+def test_nan_features_match_oracle(dev, dist_type, ps, ws):
+    """NaN feature values away from the borders: every candidate whose patch
+    reads one is invalid (a NaN similarity ranks as an invalid candidate), as
+    in the oracle; both the tiled and the direct kernels."""
+    p = small_params(T=3, C=8, H=40, W=42, ws=ws, wt=1, ps=ps, k=10, dist_type=dist_type)
+    r = np.random.default_rng(8100 + ps)
+    q, k, v, flows = _inputs(p, 8200 + ps)
+    m = ws // 2 + 6
+    for arr in (q, k):
+        for _ in range(4):
+            arr[0, r.integers(0, 3), r.integers(0, 8), r.integers(m, 40 - m), r.integers(m, 42 - m)] = np.nan
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    torch.cuda.synchronize()
+    assert not np.isnan(_h(gd)).any()
+    res = oracle.search(q, k, flows, p)
+    assert np.isinf(res["all_dists"]).sum() > np.isinf(oracle.search(
+        np.nan_to_num(q), np.nan_to_num(k), flows, p)["all_dists"]).sum()
+    compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
+
+
+@pytest.mark.parametrize("dist_type,ps,ws,stride0", [(0, 7, 9, 1), (0, 3, 5, 1), (1, 3, 5, 2)])
+def test_nonfinite_inputs_stay_in_bounds(dev, dist_type, ps, ws, stride0):
+    """NaN and +-inf anywhere in q, k and the flows (scores are then not
+    specified): no NaN score is kept, and every kept neighbour is a distinct
+    candidate of the query's own window."""
+    p = small_params(T=4, C=8, H=23, W=30, ws=ws, wt=2, ps=ps, k=12, stride0=stride0, dist_type=dist_type)
+    r = np.random.default_rng(8300 + ps + stride0)
+    q, k, v, flows = _inputs(p, 8400 + ps)
+    for arr in (q, k, flows):
+        flat = arr.reshape(-1)
+        idx = r.choice(flat.size, size=flat.size // 50, replace=False)
+        flat[idx] = r.choice([np.nan, np.inf, -np.inf], size=idx.size)
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    torch.cuda.synchronize()
+    gd_h, gi_h = _h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3)
+    assert not np.isnan(gd_h).any()
+    _, cand = oracle.search_all(np.zeros_like(q), np.zeros_like(k), flows, p)
+    cand = cand.reshape(gi_h.shape[0], -1, 3).astype(np.float32)
+    key = lambda a: tuple("nan" if np.isnan(x) else float(x) for x in a)
+    for row in range(gi_h.shape[0]):
+        valid = {key(c): j for j, c in enumerate(cand[row])}
+        ids = [valid.get(key(gi_h[row, i])) for i in range(p["k"])]
+        assert None not in ids, "row %d keeps a position outside its window" % row
+        if np.isfinite(gi_h[row]).all():  # non-finite offsets make positions of one frame coincide
+            assert len(set(ids)) == p["k"], "row %d repeats a candidate" % row
+
+
 def test_deterministic(dev):
     p = small_params(T=3, C=8, H=33, W=33, HD=2, ws=5, wt=1, ps=3, k=7)
     q, k, v, flows = _inputs(p, 5000)

@@ -536,3 +536,25 @@ def test_backward_adjoint_identities(oracle_lib):
     fin = np.isfinite(dq)
     assert (dq[fin] * gd[fin]).sum() == pytest.approx((x * gq).sum(), rel=1e-10)
     assert (dk[fin] * gd[fin]).sum() == pytest.approx((x * gk).sum(), rel=1e-10)
+
+
+def test_nan_similarity_scores_as_invalid():
+    """A NaN feature makes the similarity of every candidate reading it NaN;
+    those candidates score like invalid ones (-inf / +inf) so that every score
+    is ordered, and all other candidates are unchanged."""
+    p = small_params(T=2, C=3, H=9, W=10, ws=3, wt=1, ps=3, k=4)
+    r = np.random.default_rng(5)
+    q = r.standard_normal((1, 2, 3, 9, 10))
+    k = r.standard_normal((1, 2, 3, 9, 10))
+    flows = r.uniform(-1, 1, (1, 2, 2, 2, 9, 10))
+    k_nan = k.copy()
+    k_nan[0, 1, 2, 4, 5] = np.nan
+    for dist in (0, 1):
+        pp = dict(p, dist_type=dist)
+        d0, _ = oracle.search_all(q, k, flows, pp)
+        d1, _ = oracle.search_all(q, k_nan, flows, pp)
+        assert not np.isnan(d1).any()
+        changed = d1 != d0
+        assert changed.any()
+        assert np.all(d1[changed] == (-np.inf if dist == 0 else np.inf))
+        assert np.all(np.isfinite(d0[changed]))
