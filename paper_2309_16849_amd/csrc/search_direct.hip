@@ -78,7 +78,7 @@ __global__ void __launch_bounds__(128) search_topk_direct_kernel(const float* __
   if (row >= g.rows) return;
   QueryPos qp = decode_row(row, g);
   TopList<KMAX> lst;
-  lst.init();
+  lst.init(g.k);
   for (int dt = -g.wt; dt <= g.wt; ++dt) {
     int t2 = qp.t + dt;
     if (t2 < 0 || t2 >= g.T) continue;  // frame outside the clip: never selected ahead of a valid one
@@ -92,7 +92,7 @@ __global__ void __launch_bounds__(128) search_topk_direct_kernel(const float* __
         int cid = ((dt + g.wt) * g.ws + dh) * g.ws + dw;
         float sc = -INFINITY;
         if (okh && centre_ok(qp.w, disp_w, g.W)) sc = to_score(score_candidate(q, k, g, qp.b, qp.hd, qp.t, qp.h, qp.w, t2, disp_h, disp_w), g.dist);
-        lst.push(sc, cid, g.k);
+        lst.push(sc, cid);
       }
     }
   }
@@ -102,20 +102,22 @@ __global__ void __launch_bounds__(128) search_topk_direct_kernel(const float* __
   for (int dt = -g.wt; dt <= g.wt; ++dt) {
     int t2 = qp.t + dt;
     if (t2 >= 0 && t2 < g.T) continue;
-    for (int c = 0; c < g.ws * g.ws; ++c) lst.push(-INFINITY, (dt + g.wt) * g.ws * g.ws + c, g.k);
+    for (int c = 0; c < g.ws * g.ws; ++c) lst.push(-INFINITY, (dt + g.wt) * g.ws * g.ws + c);
   }
   float* drow = dists + row * g.k;
   float* irow = inds + row * g.k * 3;
+  const int first = KMAX - g.k;  // slot of the best entry
 #pragma unroll
-  for (int i = 0; i < KMAX; ++i) {
-    if (i < g.k) {
-      int cid = min(lst.id[i], g.ncand - 1);  // every candidate was ranked: ids are real
+  for (int e = 0; e < KMAX; ++e) {
+    if (e >= first) {
+      const int i = e - first;
+      int cid = min(lst.id[e], g.ncand - 1);  // every candidate was ranked: ids are real
       int dw = cid % g.ws;
       int dh = (cid / g.ws) % g.ws;
       int dt = cid / (g.ws * g.ws) - g.wt;
       float fh, fw;
       read_shift(flows, g, qp, dt, &fh, &fw);
-      drow[i] = from_score(lst.s[i], g.dist);
+      drow[i] = from_score(lst.s[e], g.dist);
       irow[3 * i + 0] = (float)(qp.t + dt);
       irow[3 * i + 1] = cand_disp(fh, g.s1, dh, g.r);
       irow[3 * i + 2] = cand_disp(fw, g.s1, dw, g.r);

@@ -72,10 +72,10 @@ struct Smem {
   float kst[2][KST_F];  // K union region chunks (double buffer); reused for the top-k survivors
   float qst[2][QST_F];  // q halo chunks
   float bw[QN * WIN];  // per-query window of box sums
-  float lst_s[QN * NPART * KL];  // partial lists (query-major)
+  float lst_s[QN * NPART * KL];  // partial lists (query-major), TopList slot layout
   int lst_id[QN * NPART * KL];
-  float thr_s[QN * NPART];  // k-th entry of each partial list
-  int thr_id[QN * NPART];
+  float gthr_s[QN];  // k-th best so far over all partial lists of a query
+  int gthr_id[QN];
   int nsurv[QN];
   int qn_h[QN], qn_w[QN];    // integer part of the offset
   float qf_h[QN], qf_w[QN];  // the offset itself
@@ -201,22 +201,62 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
   const float* qb = q + (((long long)b * g.T + t) * g.C + (long long)hd * g.Ch) * g.HW;
 
   for (int i = tid; i < QN * NPART * KL; i += NTHREADS) {
-    sm.lst_s[i] = -INFINITY;
-    sm.lst_id[i] = 0x7fffffff;
+    const bool sentinel = i % KL < KL - g.k;  // see TopList
+    sm.lst_s[i] = sentinel ? INFINITY : -INFINITY;
+    sm.lst_id[i] = sentinel ? -1 : 0x7fffffff;
   }
-  if (tid < QN * NPART) {
-    sm.thr_s[tid] = -INFINITY;
-    sm.thr_id[tid] = 0x7fffffff;
+  if (tid < QN) {
+    sm.gthr_s[tid] = -INFINITY;
+    sm.gthr_id[tid] = 0x7fffffff;
   }
+
+  // The k best entries of the union of query j's sorted partial lists, best
+  // first: emit(i, score, id) for i = 0 .. k-1 (a k-way merge).
+  auto merge_parts = [&](int j, auto&& emit) {
+    const int first = KL - g.k;
+    float hs[NPART];
+    int hid[NPART], hp[NPART];
+#pragma unroll
+    for (int pp = 0; pp < NPART; ++pp) {
+      hp[pp] = first;
+      hs[pp] = sm.lst_s[(j * NPART + pp) * KL + first];
+      hid[pp] = sm.lst_id[(j * NPART + pp) * KL + first];
+    }
+    for (int i = 0; i < g.k; ++i) {
+      float bs = hs[0];
+      int bi = hid[0], bp = 0, np = hp[0] + 1;
+#pragma unroll
+      for (int pp = 1; pp < NPART; ++pp)
+        if (ranks_before(hs[pp], hid[pp], bs, bi)) {
+          bs = hs[pp];
+          bi = hid[pp];
+          bp = pp;
+          np = hp[pp] + 1;
+        }
+      emit(i, bs, bi);
+      const int o = (j * NPART + bp) * KL + min(np, KL - 1);
+      const float ns = np < KL ? sm.lst_s[o] : -INFINITY;
+      const int nid = np < KL ? sm.lst_id[o] : 0x7fffffff;
+#pragma unroll
+      for (int pp = 0; pp < NPART; ++pp)
+        if (pp == bp) {
+          hp[pp] = np;
+          hs[pp] = ns;
+          hid[pp] = nid;
+        }
+    }
+  };
   if (tid < QN) sm.nsurv[tid] = 0;
 
   // Direct-to-LDS staging: one 64-lane buffer load fills one LDS row of a
   // chunk (lane = column; lanes past the row width are masked off), so the
   // row part of the address is wave-uniform and a lane only keeps its column.
   // Positions outside the frame use an out-of-range offset, read as 0.
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   constexpr unsigned OOB = 0x80000000u;
   const bool q_col_in = lane < HW && X0 + lane >= 0 && X0 + lane < g.W;
+  const unsigned q_lane_off = q_col_in ? (unsigned)(X0 + lane) * 4u : OOB;
+  const int HWi = (int)g.HW;
   const __amdgpu_buffer_rsrc_t q_rs =
       __builtin_amdgcn_make_buffer_rsrc((void*)qb, (short)0, (int)(g.Ch * g.HW * 4), 0x00020000);
 
@@ -298,8 +338,11 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
       if (sn <= 2 * g.wt) fetch_flow(frame_dt(sn), fh_next, fw_next);
     }
     __syncthreads();
-    const int dmin_h = sm.uni[0] - r, UH = sm.uni[1] - sm.uni[0] + ws + 1;
-    const int dmin_w = sm.uni[2] - r, UW = sm.uni[3] - sm.uni[2] + ws + 1;
+    // (uniform values: kept in scalar registers)
+    const int u0 = __builtin_amdgcn_readfirstlane(sm.uni[0]), u1 = __builtin_amdgcn_readfirstlane(sm.uni[1]);
+    const int u2 = __builtin_amdgcn_readfirstlane(sm.uni[2]), u3 = __builtin_amdgcn_readfirstlane(sm.uni[3]);
+    const int dmin_h = u0 - r, UH = u1 - u0 + ws + 1;
+    const int dmin_w = u2 - r, UW = u3 - u2 + ws + 1;
     const int nblk = (UW + S - 1) / S;
     // survivors of the top-k filter, stored over the K staging area once the
     // frame's correlations are done: score and window cell (dh*ws + dw)
@@ -307,28 +350,33 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
     unsigned char* const surv_c = reinterpret_cast<unsigned char*>(sm.kst[0] + QN * WSQ);
 
     if (nblk <= MAXBLK) {
-      const int ntask = UH * nblk;
-      const int span_max = KR - HROWS + 1;  // shift rows per round
-      const int tasks_per_round = min(NGROUP, span_max * nblk);
-      for (int r0 = 0; r0 < ntask; r0 += tasks_per_round) {
-        const int r1 = min(ntask, r0 + tasks_per_round);
-        // few tasks: split each task's channels over several groups
-        const int room = NGROUP / (r1 - r0);
-        const int csplit = room >= 4 ? 4 : (room >= 2 ? 2 : 1);
-        const int dh_lo = dmin_h + r0 / nblk;
-        const int dh_hi = dmin_h + (r1 - 1) / nblk;
-        const int krows = HROWS + dh_hi - dh_lo;
+      // A wave's 4 groups take 4 consecutive shift rows of one column block:
+      // their K reads then hit overlapping rows (broadcast) in distinct banks.
+      // A round covers as many shift rows as the waves and the K rows of the
+      // LDS layout allow; when a round has few tasks, the channels of each
+      // task are split over several waves (csplit parts).
+      const int span_max = KR - HROWS + 1;
+      const int rows_per_round = min(span_max, 4 * (NTHREADS / 64 / nblk));
+      for (int rr0 = 0; rr0 < UH; rr0 += rows_per_round) {
+        const int nrows = min(rows_per_round, UH - rr0);
+        const int units = nblk * ((nrows + 3) / 4);  // waves per channel part
+        const int csplit = units <= 4 ? 4 : (units <= 8 ? 2 : 1);
+        const int part = wave / units;
+        const int unit = wave - part * units;
+        const int blk = unit % nblk;
+        const int d_row = (unit / nblk) * 4 + (grp & 3);
+        const bool active = part < csplit && d_row < nrows;
+        const int dh_lo = dmin_h + rr0;
+        const int krows = HROWS + nrows - 1;
         const int kcols = HW + nblk * S - 1;
-        const int task = r0 + grp / csplit;
-        const int part = grp % csplit;
-        const bool active = task < r1;
-        const int d_h = dmin_h + task / nblk;
-        const int blk = task % nblk;
-        const int krow = lane16 + d_h - dh_lo;
+        const int d_h = dh_lo + d_row;
+        const int krow = lane16 + d_row;
 
-        // K staging: this lane's column of the round's region
+        // K staging: this lane's column of the round's region; the lane part
+        // of every row's offset (out of range for columns outside the frame)
         const int k_gx = X0 + dmin_w + lane;
-        const bool k_col_in = lane < kcols && k_gx >= 0 && k_gx < g.W;
+        const unsigned k_lane_off = (k_gx >= 0 && k_gx < g.W) ? (unsigned)k_gx * 4u : OOB;
+        const bool k_lane_on = lane < kcols;
 
         float acc[HW][S];
 #pragma unroll
@@ -337,7 +385,10 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
           for (int i = 0; i < S; ++i) acc[x][i] = 0.f;
 
         // issue the asynchronous loads of chunk c0 into buffer bsel: K rows
-        // (c, row) and q rows (c, row) are spread over the 16 waves
+        // (c, row) and q rows (c, row) are spread over the 16 waves.  The row
+        // part of an offset is wave-uniform (scalar offset, computed on the
+        // scalar unit); a lane adds its column (vector offset).  Offsets stay
+        // below 2^31: the tiled kernel requires Ch*H*W*4 < 2^31.
         auto issue = [&](int c0, int bsel) {
           const int nk = CC * krows;
           int c = 0, row = wave;  // (channel, row) of K row rr = wave + 16*i, kept incrementally
@@ -348,11 +399,12 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
           for (int rr = wave; rr < nk; rr += 16) {
             const int gy = Y0 + dh_lo + row;
             const bool rin = c0 + c < g.Ch && gy >= 0 && gy < g.H;
-            const unsigned off = (rin && k_col_in)
-                ? (unsigned)(((long long)(c0 + c) * g.HW + (long long)gy * g.W + k_gx) * 4) : OOB;
-            if (lane < kcols)
+            const int soff = rin ? ((c0 + c) * HWi + gy * g.W) * 4 : 0;
+            const unsigned voff = rin ? k_lane_off : OOB;
+            if (k_lane_on)
               __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                  k_rs, (__attribute__((address_space(3))) void*)&sm.kst[bsel][(c * KR + row) * KP], 4, off, 0, 0, 0);
+                  k_rs, (__attribute__((address_space(3))) void*)&sm.kst[bsel][(c * KR + row) * KP], 4, voff, soff, 0,
+                  0);
             row += 16;
             while (row >= krows) {
               row -= krows;
@@ -364,12 +416,12 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
           for (int cq = 0; cq < CC; ++cq) {
             const int gy = Y0 + wave;
             const bool rin = c0 + cq < g.Ch && gy >= 0 && gy < g.H;
-            const unsigned off = (rin && q_col_in)
-                ? (unsigned)(((long long)(c0 + cq) * g.HW + (long long)gy * g.W + X0 + lane) * 4) : OOB;
+            const int soff = rin ? ((c0 + cq) * HWi + gy * g.W) * 4 : 0;
+            const unsigned voff = rin ? q_lane_off : OOB;
             if (lane < HW)
               __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                  q_rs, (__attribute__((address_space(3))) void*)&sm.qst[bsel][(cq * HROWS + wave) * QP], 4, off, 0, 0,
-                  0);
+                  q_rs, (__attribute__((address_space(3))) void*)&sm.qst[bsel][(cq * HROWS + wave) * QP], 4, voff, soff,
+                  0, 0);
           }
         };
         __syncthreads();  // buffers of the previous round / frame are free
@@ -448,14 +500,8 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
         const float* r0p = &sm.bw[j * WIN + dh * WP];
         const float* r1p = r0p + WP;
         const bool okh = centre_ok(h, cand_disp(fh, 1.f, dh, r), g.H);
-        float ts = sm.thr_s[j * NPART];
-        int ti = sm.thr_id[j * NPART];
-#pragma unroll
-        for (int pp = 1; pp < NPART; ++pp)
-          if (ranks_before(sm.thr_s[j * NPART + pp], sm.thr_id[j * NPART + pp], ts, ti)) {
-            ts = sm.thr_s[j * NPART + pp];
-            ti = sm.thr_id[j * NPART + pp];
-          }
+        const float ts = sm.gthr_s[j];
+        const int ti = sm.gthr_id[j];
         const int idb = ((dt + g.wt) * ws + dh) * ws;
         for (int dw = 0; dw < ws; ++dw) {
           const float top = (1.f - aw) * r0p[dw] + aw * r0p[dw + 1];
@@ -480,14 +526,8 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
         const float fh = sm.qf_h[j], fw = sm.qf_w[j];
         const float disp_h = cand_disp(fh, 1.f, dh, r);
         const bool okh = centre_ok(h, disp_h, g.H);
-        float ts = sm.thr_s[j * NPART];
-        int ti = sm.thr_id[j * NPART];
-#pragma unroll
-        for (int pp = 1; pp < NPART; ++pp)
-          if (ranks_before(sm.thr_s[j * NPART + pp], sm.thr_id[j * NPART + pp], ts, ti)) {
-            ts = sm.thr_s[j * NPART + pp];
-            ti = sm.thr_id[j * NPART + pp];
-          }
+        const float ts = sm.gthr_s[j];
+        const int ti = sm.gthr_id[j];
         const int idb = ((dt + g.wt) * ws + dh) * ws;
         for (int dw = 0; dw < ws; ++dw) {
           const float disp_w = cand_disp(fw, 1.f, dw, r);
@@ -514,21 +554,29 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
           lst.s[i] = sm.lst_s[lo + i];
           lst.id[i] = sm.lst_id[lo + i];
         }
-        lst.thr_s = sm.thr_s[tid];
-        lst.thr_id = sm.thr_id[tid];
         const int idf = (dt + g.wt) * ws * ws;
-        for (int c = pp; c < ns; c += NPART) lst.push(surv_s[j * WSQ + c], idf + surv_c[j * WSQ + c], g.k);
+        for (int c = pp; c < ns; c += NPART) lst.push(surv_s[j * WSQ + c], idf + surv_c[j * WSQ + c]);
 #pragma unroll
         for (int i = 0; i < KL; ++i) {
           sm.lst_s[lo + i] = lst.s[i];
           sm.lst_id[lo + i] = lst.id[i];
         }
-        sm.thr_s[tid] = lst.thr_s;
-        sm.thr_id[tid] = lst.thr_id;
       }
     }
     __syncthreads();
-    if (tid < QN) sm.nsurv[tid] = 0;
+    if (tid < QN) {
+      // exact k-th best so far: the next frames keep only candidates that
+      // rank before it (a candidate that does not cannot enter the top k)
+      sm.nsurv[tid] = 0;
+      float ks = -INFINITY;
+      int kid = 0x7fffffff;
+      merge_parts(tid, [&](int, float sc, int id) {
+        ks = sc;
+        kid = id;
+      });
+      sm.gthr_s[tid] = ks;
+      sm.gthr_id[tid] = kid;
+    }
   }
 
   // ---- output: complete short lists with the frames outside the clip ----
@@ -536,56 +584,22 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
     const int j = tid;
     const int h = y0 + j / TQW, w = x0 + j % TQW;
     if (h < g.H && w < g.W) {
-      // merge the sorted partial lists (only their first k entries are kept)
+      // merge the sorted partial lists into one list (TopList slot layout)
       TopList<KL> lst;
-      lst.init();
-      {
-        float hs[NPART];
-        int hid[NPART], hp[NPART];
+      lst.init(g.k);
+      const int first = KL - g.k;
+      merge_parts(j, [&](int i, float sc, int id) {
 #pragma unroll
-        for (int pp = 0; pp < NPART; ++pp) {
-          hp[pp] = 0;
-          hs[pp] = sm.lst_s[(j * NPART + pp) * KL];
-          hid[pp] = sm.lst_id[(j * NPART + pp) * KL];
-        }
-#pragma unroll
-        for (int i = 0; i < KL; ++i) {
-          if (i < g.k) {
-            float bs = hs[0];
-            int bi = hid[0], bp = 0, np = hp[0] + 1;
-#pragma unroll
-            for (int pp = 1; pp < NPART; ++pp)
-              if (ranks_before(hs[pp], hid[pp], bs, bi)) {
-                bs = hs[pp];
-                bi = hid[pp];
-                bp = pp;
-                np = hp[pp] + 1;
-              }
-            lst.s[i] = bs;
-            lst.id[i] = bi;
-            const int o = (j * NPART + bp) * KL + min(np, KL - 1);
-            const float ns = np < g.k ? sm.lst_s[o] : -INFINITY;
-            const int nid = np < g.k ? sm.lst_id[o] : 0x7fffffff;
-#pragma unroll
-            for (int pp = 0; pp < NPART; ++pp)
-              if (pp == bp) {
-                hp[pp] = np;
-                hs[pp] = ns;
-                hid[pp] = nid;
-              }
+        for (int e = 0; e < KL; ++e)
+          if (e == first + i) {
+            lst.s[e] = sc;
+            lst.id[e] = id;
           }
-        }
-#pragma unroll
-        for (int i = 0; i < KL; ++i)
-          if (i == g.k - 1) {
-            lst.thr_s = lst.s[i];
-            lst.thr_id = lst.id[i];
-          }
-      }
-      if (lst.thr_s == -INFINITY) {
+      });
+      if (lst.thr_s() == -INFINITY) {
         for (int dt = -g.wt; dt <= g.wt; ++dt) {
           if (t + dt >= 0 && t + dt < g.T) continue;
-          for (int c = 0; c < ws * ws; ++c) lst.push(-INFINITY, (dt + g.wt) * ws * ws + c, g.k);
+          for (int c = 0; c < ws * ws; ++c) lst.push(-INFINITY, (dt + g.wt) * ws * ws + c);
         }
       }
       const long long row = ((((long long)b * g.HD + hd) * g.T + t) * g.nH + h) * g.nW + w;
@@ -593,11 +607,12 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
       float* irow = inds + row * g.k * 3;
       const long long pix = (long long)h * g.W + w;
 #pragma unroll
-      for (int i = 0; i < KL; ++i) {
-        if (i < g.k) {
+      for (int e = 0; e < KL; ++e) {
+        if (e >= first) {
+          const int i = e - first;
           // every candidate of the window was ranked, so the k best are real
           // candidates; the clamp only keeps a placeholder id in bounds
-          const int cid = min(lst.id[i], g.ncand - 1);
+          const int cid = min(lst.id[e], g.ncand - 1);
           const int dw = cid % ws, dh = (cid / ws) % ws, dt = cid / (ws * ws) - g.wt;
           float fh = 0.f, fw = 0.f;
           if (dt != 0) {
@@ -610,7 +625,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
               fw = flows[(base + 1) * g.HW + pix];
             }
           }
-          drow[i] = lst.s[i];
+          drow[i] = lst.s[e];
           irow[3 * i + 0] = (float)(t + dt);
           irow[3 * i + 1] = cand_disp(fh, 1.f, dh, r);
           irow[3 * i + 2] = cand_disp(fw, 1.f, dw, r);

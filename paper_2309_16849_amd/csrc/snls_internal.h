@@ -150,27 +150,28 @@ SNLS_DEV float score_candidate(const float* __restrict__ q, const float* __restr
   return acc != acc ? from_score(-INFINITY, g.dist) : acc;
 }
 
-// Sorted top-K list in registers, best first.  KMAX is the capacity; only
-// the first k entries are kept meaningful, the threshold test uses entry k-1.
+// Sorted top-k list in registers, best first, for 1 <= k <= KMAX.  The
+// first KMAX - k slots hold sentinels (+inf, id -1) that rank before every
+// candidate and never move, so the k kept entries are slots KMAX-k .. KMAX-1
+// and the k-th best is always the last slot (a fixed register).
 template <int KMAX>
 struct TopList {
   float s[KMAX];
   int id[KMAX];
-  float thr_s;  // score of entry k-1
-  int thr_id;
 
-  SNLS_DEV void init() {
+  SNLS_DEV void init(int k) {
 #pragma unroll
     for (int i = 0; i < KMAX; ++i) {
-      s[i] = -INFINITY;
-      id[i] = 0x7fffffff;
+      const bool sentinel = i < KMAX - k;
+      s[i] = sentinel ? INFINITY : -INFINITY;
+      id[i] = sentinel ? -1 : 0x7fffffff;
     }
-    thr_s = -INFINITY;
-    thr_id = 0x7fffffff;
   }
+  SNLS_DEV float thr_s() const { return s[KMAX - 1]; }
+  SNLS_DEV int thr_id() const { return id[KMAX - 1]; }
   // Insert (sc, cid) if it ranks before the current k-th entry.
-  SNLS_DEV void push(float sc, int cid, int k) {
-    if (!ranks_before(sc, cid, thr_s, thr_id)) return;
+  SNLS_DEV void push(float sc, int cid) {
+    if (!ranks_before(sc, cid, s[KMAX - 1], id[KMAX - 1])) return;
 #pragma unroll
     for (int i = 0; i < KMAX; ++i) {
       bool sw = ranks_before(sc, cid, s[i], id[i]);
@@ -180,13 +181,6 @@ struct TopList {
       id[i] = sw ? cid : ti;
       sc = sw ? ts : sc;
       cid = sw ? ti : cid;
-    }
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) {
-      if (i == k - 1) {
-        thr_s = s[i];
-        thr_id = id[i];
-      }
     }
   }
 };

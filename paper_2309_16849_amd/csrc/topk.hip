@@ -15,15 +15,15 @@ __global__ void __launch_bounds__(256) topk_kernel(const float* __restrict__ dal
   if (row >= rows) return;  // whole wave leaves together
   const float* drow = dall + row * ncand;
   TopList<KMAX> lst;
-  lst.init();
+  lst.init(k);
   for (int j = lane; j < ncand; j += 64) {
     float d = drow[j];
     float sc = to_score(d, dist);
     if (sc != sc) sc = -INFINITY;  // NaN ranks last
-    lst.push(sc, j, k);
+    lst.push(sc, j);
   }
   // Merge: k rounds of wave arg-best over the lanes' list heads.
-  int head = 0;
+  int head = KMAX - k;  // slot of the lane's best entry
   for (int i = 0; i < k; ++i) {
     float hs = -INFINITY;
     int hid = 0x7fffffff;
