@@ -1,19 +1,22 @@
 // search_tile.hip -- tiled shifted non-local search with fused top-k for
-// the inner-product distance, query stride 1 and key stride 1 (Sec. 3.2).
+// the inner-product distance, query stride 1 and key stride S_K <= 1
+// (Sec. 3.2).
 //
-// With S_K = 1 every window cell of a query shares the fractional part a of
-// its offset F (Sec. 3.2 reads fractional positions bilinearly), so with
-// N = floor(F) the score of cell d is an exact 4-tap combination
-//     S(d) = sum_e w_e(a) * B_{N + d - r + e}(j),      e in {0,1}^2,
+// Window cell d of a query sits at displacement disp_d = F + S_K (d - r);
+// with n_d = floor(disp_d) and a_d = disp_d - n_d its bilinear score is an
+// exact 4-tap combination
+//     S(d) = sum_e w_e(a_d) * B_{n_d + e}(j),      e in {0,1}^2,
 // of box sums over the patch of pixel correlations
 //     B_D(j) = sum_p c_D(j + p),   c_D(x) = <q(x), K(x + D)>  (head channels,
 //     query pixels outside the frame and key pixels outside the frame give 0).
-// A tile of queries needs c_D only on its halo (tile + patch - 1) and only
-// for the union of integer shifts D its windows cover.  Computing c_D once
-// per (halo pixel, shift) instead of once per (query, patch pixel, cell) is
-// what removes the redundancy of the in-place search (Sec. 3.4 notes that
-// shifted windows defeat plain tiling; the union of the shifted windows is
-// still shared by neighbouring queries).
+// All integer shifts D of a query lie in [floor(disp_0), floor(disp_last)+1]
+// (at most Ws + 1 per axis for S_K <= 1; for S_K = 1/2 about half that), so
+// a tile of queries needs c_D only on its halo (tile + patch - 1) and only
+// for the union of those shift ranges.  Computing c_D once per (halo pixel,
+// shift) instead of once per (query, patch pixel, cell) is what removes the
+// redundancy of the in-place search (Sec. 3.4 notes that shifted windows
+// defeat plain tiling; the union of the shifted windows is still shared by
+// neighbouring queries).
 //
 // Work split (one workgroup = one 10 x 8 query tile of one (b, head, t),
 // looping over the frames of the temporal window):
@@ -27,8 +30,9 @@
 //    vertical one across the lanes of the group (shuffles), and lane j_h
 //    writes B for its tile row into the per-query window table Bw (every
 //    (query, cell) entry is written by exactly one lane: deterministic);
-//  * the 4-tap combination, the exact validity test and the top-k update
-//    then run per query.
+//  * the 4-tap combination (positions and weights from disp_d exactly as
+//    the output reports them), the exact validity test and the top-k
+//    update then run per query.
 // A frame whose union of shifts is too wide for the LDS layout is scored
 // directly instead (per candidate, canonical positions).
 #include "snls_internal.h"
@@ -49,8 +53,7 @@ constexpr int KP = 45;                  // K row pitch (odd: spreads the 16 rows
 constexpr int QP = 21;                  // q row pitch (odd)
 constexpr int MAXBLK = 5;               // shift-column blocks: union width <= 30
 constexpr int WSMAX = 9;
-constexpr int MAXSLOT = 7;              // frames per window kept for the output (2*wt + 1 <= 7)
-constexpr int WP = WSMAX + 1;           // window-table pitch
+constexpr int WP = WSMAX + 2;           // window-table pitch (shifts floor(disp_0) .. floor(disp_last) + 1)
 constexpr int WIN = WP * WP;
 constexpr int WSQ = WSMAX * WSMAX;      // candidates per query and frame
 constexpr int KLIST = 16;               // largest top-k capacity
@@ -77,9 +80,8 @@ struct Smem {
   float gthr_s[QN];  // k-th best so far over all partial lists of a query
   int gthr_id[QN];
   int nsurv[QN];
-  int qn_h[QN], qn_w[QN];    // integer part of the offset
+  int qlo_h[QN], qlo_w[QN];  // smallest integer shift of the query's window (table origin)
   float qf_h[QN], qf_w[QN];  // the offset itself
-  float fo_h[MAXSLOT * QN], fo_w[MAXSLOT * QN];  // offsets of every searched frame (for the output)
   int uni[4];                // min N_h, max N_h, min N_w, max N_w
 };
 
@@ -299,23 +301,25 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
       const int jh = tid / TQW, jw = tid % TQW;
       const bool inside = tid < QN && y0 + jh < g.H && x0 + jw < g.W;
       const float fh = fh_next, fw = fw_next;
-      int nh = 0, nw = 0;
-      // Offsets that are not finite or absurdly large leave the union alone;
+      // Integer shifts a query's window reads: floor(disp) .. floor(disp) + 1
+      // for its first .. last cell (disp grows with the cell index).
+      // Offsets that are not finite or absurdly large count as zero here;
       // their candidates fail the exact validity test below.
-      if (fabsf(fh) < 1.0e6f) nh = (int)floorf(fh);
-      if (fabsf(fw) < 1.0e6f) nw = (int)floorf(fw);
+      const float fh_u = fabsf(fh) < 1.0e6f ? fh : 0.f, fw_u = fabsf(fw) < 1.0e6f ? fw : 0.f;
+      const int lo_h = (int)floorf(cand_disp(fh_u, g.s1, 0, r));
+      const int hi_h = (int)floorf(cand_disp(fh_u, g.s1, ws - 1, r)) + 1;
+      const int lo_w = (int)floorf(cand_disp(fw_u, g.s1, 0, r));
+      const int hi_w = (int)floorf(cand_disp(fw_u, g.s1, ws - 1, r)) + 1;
       if (tid < QN) {
-        sm.qn_h[tid] = nh;
-        sm.qn_w[tid] = nw;
+        sm.qlo_h[tid] = lo_h;
+        sm.qlo_w[tid] = lo_w;
         sm.qf_h[tid] = fh;
         sm.qf_w[tid] = fw;
-        sm.fo_h[(dt + g.wt) * QN + tid] = fh;
-        sm.fo_w[(dt + g.wt) * QN + tid] = fw;
       }
       // union bounds: wave reductions, then one LDS atomic per wave
       if (tid < ((QN + 63) & ~63)) {
-        int a0 = inside ? nh : INT_MAX, a1 = inside ? nh : INT_MIN;
-        int a2 = inside ? nw : INT_MAX, a3 = inside ? nw : INT_MIN;
+        int a0 = inside ? lo_h : INT_MAX, a1 = inside ? hi_h : INT_MIN;
+        int a2 = inside ? lo_w : INT_MAX, a3 = inside ? hi_w : INT_MIN;
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) {
           a0 = min(a0, __shfl_xor(a0, off));
@@ -341,8 +345,8 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
     // (uniform values: kept in scalar registers)
     const int u0 = __builtin_amdgcn_readfirstlane(sm.uni[0]), u1 = __builtin_amdgcn_readfirstlane(sm.uni[1]);
     const int u2 = __builtin_amdgcn_readfirstlane(sm.uni[2]), u3 = __builtin_amdgcn_readfirstlane(sm.uni[3]);
-    const int dmin_h = u0 - r, UH = u1 - u0 + ws + 1;
-    const int dmin_w = u2 - r, UW = u3 - u2 + ws + 1;
+    const int dmin_h = u0, UH = u1 - u0 + 1;
+    const int dmin_w = u2, UW = u3 - u2 + 1;
     const int nblk = (UW + S - 1) / S;
     // survivors of the top-k filter, stored over the K staging area once the
     // frame's correlations are done: score and window cell (dh*ws + dw)
@@ -472,13 +476,13 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
 #pragma unroll
             for (int jw = 0; jw < TQW; ++jw) {
               const int j = jh * TQW + jw;
-              const int u = d_h - (sm.qn_h[j] - r);
-              const int vbase = dmin_w + blk * S - (sm.qn_w[j] - r);
-              if (u >= 0 && u <= ws) {
+              const int u = d_h - sm.qlo_h[j];
+              const int vbase = dmin_w + blk * S - sm.qlo_w[j];
+              if (u >= 0 && u < WP) {
 #pragma unroll
                 for (int i = 0; i < S; ++i) {
                   const int v = vbase + i;
-                  if (v >= 0 && v <= ws) {
+                  if (v >= 0 && v < WP) {
                     float* cell = &sm.bw[j * WIN + u * WP + v];
                     *cell = pp == 0 ? acc[jw][i] : *cell + acc[jw][i];
                   }
@@ -495,18 +499,25 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
         const int h = y0 + j / TQW, w = x0 + j % TQW;
         if (h >= g.H || w >= g.W) continue;
         const float fh = sm.qf_h[j], fw = sm.qf_w[j];
-        const float ah = fh - (float)sm.qn_h[j];
-        const float aw = fw - (float)sm.qn_w[j];
-        const float* r0p = &sm.bw[j * WIN + dh * WP];
+        const int lo_w = sm.qlo_w[j];
+        // the cell's bilinear taps: integer shift floor(disp) and fraction
+        const float disp_h = cand_disp(fh, g.s1, dh, r);
+        const bool okh = centre_ok(h, disp_h, g.H);
+        const float fl_h = floorf(disp_h);
+        const float ah = disp_h - fl_h;
+        const float* r0p = &sm.bw[j * WIN + (okh ? (int)fl_h - sm.qlo_h[j] : 0) * WP];
         const float* r1p = r0p + WP;
-        const bool okh = centre_ok(h, cand_disp(fh, 1.f, dh, r), g.H);
         const float ts = sm.gthr_s[j];
         const int ti = sm.gthr_id[j];
         const int idb = ((dt + g.wt) * ws + dh) * ws;
         for (int dw = 0; dw < ws; ++dw) {
-          const float top = (1.f - aw) * r0p[dw] + aw * r0p[dw + 1];
-          const float bot = (1.f - aw) * r1p[dw] + aw * r1p[dw + 1];
-          const bool ok = okh && centre_ok(w, cand_disp(fw, 1.f, dw, r), g.W);
+          const float disp_w = cand_disp(fw, g.s1, dw, r);
+          const bool ok = okh && centre_ok(w, disp_w, g.W);
+          const float fl_w = floorf(disp_w);
+          const float aw = disp_w - fl_w;
+          const int col = ok ? (int)fl_w - lo_w : 0;  // table reads only matter for valid cells
+          const float top = (1.f - aw) * r0p[col] + aw * r0p[col + 1];
+          const float bot = (1.f - aw) * r1p[col] + aw * r1p[col + 1];
           const float dv = (1.f - ah) * top + ah * bot;
           const float d = ok && dv == dv ? dv : -INFINITY;  // NaN scores as invalid
           if (ranks_before(d, idb + dw, ts, ti)) {
@@ -524,13 +535,13 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
         const int h = y0 + j / TQW, w = x0 + j % TQW;
         if (h >= g.H || w >= g.W) continue;
         const float fh = sm.qf_h[j], fw = sm.qf_w[j];
-        const float disp_h = cand_disp(fh, 1.f, dh, r);
+        const float disp_h = cand_disp(fh, g.s1, dh, r);
         const bool okh = centre_ok(h, disp_h, g.H);
         const float ts = sm.gthr_s[j];
         const int ti = sm.gthr_id[j];
         const int idb = ((dt + g.wt) * ws + dh) * ws;
         for (int dw = 0; dw < ws; ++dw) {
-          const float disp_w = cand_disp(fw, 1.f, dw, r);
+          const float disp_w = cand_disp(fw, g.s1, dw, r);
           float d = -INFINITY;
           if (okh && centre_ok(w, disp_w, g.W)) d = score_candidate(q, k, g, b, hd, t, h, w, t2, disp_h, disp_w);
           if (ranks_before(d, idb + dw, ts, ti)) {
@@ -616,29 +627,24 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
           const int dw = cid % ws, dh = (cid / ws) % ws, dt = cid / (ws * ws) - g.wt;
           float fh = 0.f, fw = 0.f;
           if (dt != 0) {
-            if (t + dt >= 0 && t + dt < g.T) {  // searched: offsets kept in LDS
-              fh = sm.fo_h[(dt + g.wt) * QN + j];
-              fw = sm.fo_w[(dt + g.wt) * QN + j];
-            } else {
-              long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dt, g.wt)) * 2;
-              fh = flows[base * g.HW + pix];
-              fw = flows[(base + 1) * g.HW + pix];
-            }
+            const long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dt, g.wt)) * 2;
+            fh = flows[base * g.HW + pix];
+            fw = flows[(base + 1) * g.HW + pix];
           }
           drow[i] = lst.s[e];
           irow[3 * i + 0] = (float)(t + dt);
-          irow[3 * i + 1] = cand_disp(fh, 1.f, dh, r);
-          irow[3 * i + 2] = cand_disp(fw, 1.f, dw, r);
+          irow[3 * i + 1] = cand_disp(fh, g.s1, dh, r);
+          irow[3 * i + 2] = cand_disp(fw, g.s1, dw, r);
         }
       }
     }
   }
 }
 
-// The tiled kernel handles: inner product, S_Q = S_K = 1, P <= 7, Ws <= 9, k <= 16.
+// The tiled kernel handles: inner product, S_Q = 1, S_K <= 1, P <= 7, Ws <= 9, k <= 16.
 bool tile_supported(const Geo& g) {
-  return g.dist == SNLS_DIST_PROD && g.s0 == 1 && g.s1 == 1.0f && g.ps <= 7 && g.ws <= tile::WSMAX &&
-         g.k >= 1 && g.k <= tile::KLIST && 2 * g.wt + 1 <= tile::MAXSLOT && (long long)g.Ch * g.HW * 4 < (1LL << 31);
+  return g.dist == SNLS_DIST_PROD && g.s0 == 1 && g.s1 > 0.f && g.s1 <= 1.0f && g.ps <= 7 && g.ws <= tile::WSMAX &&
+         g.k >= 1 && g.k <= tile::KLIST && (long long)g.Ch * g.HW * 4 < (1LL << 31);
 }
 
 snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,

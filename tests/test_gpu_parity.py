@@ -146,13 +146,13 @@ def _swap_mask(p, swaps):
 
 
 # ------------------------------------------------------ tiled kernel --
-# Cases inside the tiled kernel's domain (inner product, S_Q = S_K = 1,
-# P <= 7, Ws <= 9, k <= 16, 2wt+1 <= 7): every patch size, ragged tiles and
-# channel chunks, narrow shift unions (few tasks: channel-split groups),
-# wide ones (several rounds) and unions too wide for the LDS layout (the
-# per-candidate fallback).
+# Cases inside the tiled kernel's domain (inner product, S_Q = 1, S_K <= 1,
+# P <= 7, Ws <= 9, k <= 16): every patch size, key strides 1, 3/4, 1/2 and
+# 1/4, ragged tiles and channel chunks, narrow shift unions (few tasks:
+# channel-split groups), wide ones (several rounds) and unions too wide for
+# the LDS layout (the per-candidate fallback).
 
-def _tile_cases(n=18, seed=31):
+def _tile_cases(n=28, seed=31):
     r = np.random.default_rng(seed)
     cases = []
     for i in range(n):
@@ -161,7 +161,8 @@ def _tile_cases(n=18, seed=31):
         p = small_params(B=int(r.choice([1, 2])), T=int(r.choice([1, 2, 3, 5])), HD=HD,
                          C=HD * int(r.choice([1, 3, 4, 6, 9])), H=int(r.choice([5, 17, 23, 31])),
                          W=int(r.choice([6, 16, 19, 41])), ws=int(r.choice([1, 2, 4, 5, 7, 8, 9])),
-                         wt=int(r.choice([0, 1, 2, 3])), ps=ps, stride0=1, stride1=1.0, dist_type=0)
+                         wt=int(r.choice([0, 1, 2, 3, 4])), ps=ps, stride0=1,
+                         stride1=float([1.0, 0.5, 0.75, 1.0, 0.25][i % 5 if i < 20 else (i + 1) % 5]), dist_type=0)
         nc = (2 * p["wt"] + 1) * p["ws"] ** 2
         p["k"] = int(min(nc, r.choice([1, 5, 10, 12, 13, 16])))
         kind = ["frac", "smooth", "int", "wide", "far"][i % 5]
@@ -170,7 +171,7 @@ def _tile_cases(n=18, seed=31):
 
 
 TILE_CASES = _tile_cases()
-TILE_IDS = ["t%d-ws%d-wt%d-ps%d-k%d-%s" % (i, p["ws"], p["wt"], p["ps"], p["k"], kd)
+TILE_IDS = ["t%d-ws%d-wt%d-ps%d-sk%g-k%d-%s" % (i, p["ws"], p["wt"], p["ps"], p["stride1"], p["k"], kd)
             for i, (p, kd) in enumerate(TILE_CASES)]
 
 
