@@ -45,12 +45,12 @@ constexpr int TQW = 8;                  // tile width (queries)
 constexpr int HROWS = 16;               // halo rows = lanes per group
 constexpr int NGROUP = 64;              // groups per workgroup
 constexpr int NTHREADS = HROWS * NGROUP;
-static_assert(NTHREADS / 64 == HROWS, "q staging maps one halo row to each wave");
 constexpr int S = 6;                    // shift columns per task
 constexpr int CC = 4;                   // channels per staging chunk (double-buffered)
 constexpr int KR = 36;                  // K rows in LDS
 constexpr int KP = 45;                  // K row pitch (odd: spreads the 16 rows of a group over the banks)
 constexpr int QP = 21;                  // q row pitch (odd)
+constexpr int NIT = 2;                  // staging items (4 columns of one row) per thread and chunk
 constexpr int MAXBLK = 5;               // shift-column blocks: union width <= 30
 constexpr int WSMAX = 9;
 constexpr int WP = WSMAX + 2;           // window-table pitch (shifts floor(disp_0) .. floor(disp_last) + 1)
@@ -58,12 +58,9 @@ constexpr int WIN = WP * WP;
 constexpr int WSQ = WSMAX * WSMAX;      // candidates per query and frame
 constexpr int KLIST = 16;               // largest top-k capacity
 
-// Each direct-to-LDS load fills a whole 64-word block, so the staging
-// buffers are padded to a multiple of 64 words (the padding reads as 0).
+// Staging buffers (double-buffered chunks of CC channels).
 constexpr int KST_F = (CC * KR * KP + 63) / 64 * 64;     // 6528 floats
 constexpr int QST_F = (CC * HROWS * QP + 63) / 64 * 64;  // 1344
-// all direct-to-LDS targets (placed first in LDS) stay below 64 KB
-static_assert((2 * KST_F + 2 * QST_F) * 4 <= 65536, "staging buffers must sit in the first 64 KB of LDS");
 
 
 template <int PS, int KL>
@@ -174,6 +171,10 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
   constexpr int TQH = HROWS - PS + 1;
   constexpr int HW = TQW + PS - 1;
   constexpr int LO = -(PS / 2);
+  constexpr int QC4 = (HW + 3) / 4;  // 4-column items per q row
+  constexpr int NQIT = CC * HROWS * QC4;  // q items per chunk (a multiple of 64)
+  static_assert(NQIT % 64 == 0 && NQIT <= NTHREADS, "q items fill whole waves of item slot 1");
+  static_assert(CC * KR * ((KP + 3) / 4) <= 2 * NTHREADS - NQIT, "every K item has a slot");
   constexpr int QN = Smem<PS, KL>::QN;
   constexpr int NPART = Smem<PS, KL>::NPART;
   __shared__ Smem<PS, KL> sm;
@@ -250,14 +251,8 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
   };
   if (tid < QN) sm.nsurv[tid] = 0;
 
-  // Direct-to-LDS staging: one 64-lane buffer load fills one LDS row of a
-  // chunk (lane = column; lanes past the row width are masked off), so the
-  // row part of the address is wave-uniform and a lane only keeps its column.
-  // Positions outside the frame use an out-of-range offset, read as 0.
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-  constexpr unsigned OOB = 0x80000000u;
-  const bool q_col_in = lane < HW && X0 + lane >= 0 && X0 + lane < g.W;
-  const unsigned q_lane_off = q_col_in ? (unsigned)(X0 + lane) * 4u : OOB;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  constexpr unsigned OOB = 0x80000000u;  // buffer offset past any extent: reads 0
   const int HWi = (int)g.HW;
   const __amdgpu_buffer_rsrc_t q_rs =
       __builtin_amdgcn_make_buffer_rsrc((void*)qb, (short)0, (int)(g.Ch * g.HW * 4), 0x00020000);
@@ -376,65 +371,89 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
         const int d_h = dh_lo + d_row;
         const int krow = lane16 + d_row;
 
-        // K staging: this lane's column of the round's region; the lane part
-        // of every row's offset (out of range for columns outside the frame)
-        const int k_gx = X0 + dmin_w + lane;
-        const unsigned k_lane_off = (k_gx >= 0 && k_gx < g.W) ? (unsigned)k_gx * 4u : OOB;
-        const bool k_lane_on = lane < kcols;
-
         float acc[HW][S];
 #pragma unroll
         for (int x = 0; x < HW; ++x)
 #pragma unroll
           for (int i = 0; i < S; ++i) acc[x][i] = 0.f;
 
-        // issue the asynchronous loads of chunk c0 into buffer bsel: K rows
-        // (c, row) and q rows (c, row) are spread over the 16 waves.  The row
-        // part of an offset is wave-uniform (scalar offset, computed on the
-        // scalar unit); a lane adds its column (vector offset).  Offsets stay
-        // below 2^31: the tiled kernel requires Ch*H*W*4 < 2^31.
-        auto issue = [&](int c0, int bsel) {
-          const int nk = CC * krows;
-          int c = 0, row = wave;  // (channel, row) of K row rr = wave + 16*i, kept incrementally
-          while (row >= krows) {
-            row -= krows;
-            ++c;
-          }
-          for (int rr = wave; rr < nk; rr += 16) {
-            const int gy = Y0 + dh_lo + row;
-            const bool rin = c0 + c < g.Ch && gy >= 0 && gy < g.H;
-            const int soff = rin ? ((c0 + c) * HWi + gy * g.W) * 4 : 0;
-            const unsigned voff = rin ? k_lane_off : OOB;
-            if (k_lane_on)
-              __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                  k_rs, (__attribute__((address_space(3))) void*)&sm.kst[bsel][(c * KR + row) * KP], 4, voff, soff, 0,
-                  0);
-            row += 16;
-            while (row >= krows) {
-              row -= krows;
-              ++c;
-            }
-          }
-          // q: HROWS == 16 rows per channel, so wave w loads row w of every channel
+        // Staging through registers: a chunk (CC channels) of the round's K
+        // region and of the q halo is cut into items of 4 consecutive
+        // columns of one row; each thread owns up to NIT items, loads them
+        // with one 16-byte buffer load each (the start column is clamped into
+        // the frame, so no access leaves the row; values are realigned and
+        // columns outside the frame zeroed in registers) and writes them to
+        // LDS.  Rows outside the frame and channels past the head read 0
+        // through an out-of-range offset.  Offsets stay below 2^31: the tiled
+        // kernel requires Ch*H*W*4 < 2^31.
+        const int ncol4 = (kcols + 3) >> 2;
+        const int nkit = CC * krows * ncol4;  // K items (at most 2*NTHREADS - NQIT)
+        // Item slot 0 of every thread is K item tid; slot 1 is q item tid for
+        // the first NQIT threads (a whole number of waves, so the buffer a
+        // wave reads is wave-uniform) and K item NTHREADS + tid - NQIT after.
+        unsigned it_voff[NIT];  // byte offset of the item at channel 0 (OOB: nothing to read)
+        int it_pack[NIT];       // LDS index | (shift + 3) << 13 | column mask << 16 | channel << 20 | on << 24
+        const bool q_slot = wave < NQIT / 64;  // slot 1 holds a q item
 #pragma unroll
-          for (int cq = 0; cq < CC; ++cq) {
-            const int gy = Y0 + wave;
-            const bool rin = c0 + cq < g.Ch && gy >= 0 && gy < g.H;
-            const int soff = rin ? ((c0 + cq) * HWi + gy * g.W) * 4 : 0;
-            const unsigned voff = rin ? q_lane_off : OOB;
-            if (lane < HW)
-              __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                  q_rs, (__attribute__((address_space(3))) void*)&sm.qst[bsel][(cq * HROWS + wave) * QP], 4, voff, soff,
-                  0, 0);
+        for (int n = 0; n < NIT; ++n) {
+          const bool isq = n == 1 && q_slot;
+          const int ee = n == 0 ? tid : (isq ? tid : NTHREADS + tid - NQIT);
+          it_voff[n] = OOB;
+          it_pack[n] = 0;
+          if (isq || ee < nkit) {
+            const int nc4 = isq ? QC4 : ncol4, nrow = isq ? HROWS : krows;
+            const int c = ee / (nrow * nc4), rem = ee - c * (nrow * nc4);
+            const int row = rem / nc4, c4 = rem - row * nc4;
+            const int gy = Y0 + (isq ? 0 : dh_lo) + row;
+            const int gx = (isq ? X0 : X0 + dmin_w) + 4 * c4;
+            const int gxl = min(max(gx, 0), g.W - 4);
+            int mask = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) mask |= (gx + j >= 0 && gx + j < g.W) ? (1 << j) : 0;
+            if (gy >= 0 && gy < g.H && mask) it_voff[n] = (unsigned)((gy * g.W + gxl) * 4);
+            const int ldsi = isq ? (c * HROWS + row) * QP + 4 * c4 : (c * KR + row) * KP + 4 * c4;
+            it_pack[n] = ldsi | ((gx - gxl + 3) << 13) | (mask << 16) | (c << 20) | (1 << 24);
+          }
+        }
+        typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+        u32x4 stg[NIT];
+        auto load_items = [&](int c0) {
+#pragma unroll
+          for (int n = 0; n < NIT; ++n) {
+            const int c = (it_pack[n] >> 20) & 7;
+            const unsigned off = (it_voff[n] != OOB && c0 + c < g.Ch) ? it_voff[n] + (unsigned)((c0 + c) * HWi * 4) : OOB;
+            stg[n] = __builtin_amdgcn_raw_buffer_load_b128((n == 1 && q_slot) ? q_rs : k_rs, off, 0, 0);
+          }
+        };
+        auto store_items = [&](int bsel) {
+#pragma unroll
+          for (int n = 0; n < NIT; ++n) {
+            const int pk = it_pack[n];
+            if (pk & (1 << 24)) {
+              const int sh = ((pk >> 13) & 7) - 3, mask = (pk >> 16) & 15;
+              const float v0 = __uint_as_float(stg[n].x), v1 = __uint_as_float(stg[n].y);
+              const float v2 = __uint_as_float(stg[n].z), v3 = __uint_as_float(stg[n].w);
+              float o[4];
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                const int src = j + sh;  // in 0..3 for every column inside the frame
+                const float val = src <= 0 ? v0 : (src == 1 ? v1 : (src == 2 ? v2 : v3));
+                o[j] = (mask >> j) & 1 ? val : 0.f;
+              }
+              float* dst = (n == 1 && q_slot) ? &sm.qst[bsel][pk & 8191] : &sm.kst[bsel][pk & 8191];
+#pragma unroll
+              for (int j = 0; j < 4; ++j) dst[j] = o[j];
+            }
           }
         };
         __syncthreads();  // buffers of the previous round / frame are free
-        issue(0, 0);
+        load_items(0);
+        store_items(0);
         int bsel = 0;
         for (int c0 = 0; c0 < g.Ch; c0 += CC, bsel ^= 1) {
-          __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of chunk c0 have landed in LDS
-          __syncthreads();                // ... and everyone's; buffer bsel^1 is no longer read
-          if (c0 + CC < g.Ch) issue(c0 + CC, bsel ^ 1);
+          __syncthreads();  // chunk c0 is in buffer bsel; buffer bsel^1 is no longer read
+          const bool more = c0 + CC < g.Ch;
+          if (more) load_items(c0 + CC);  // in flight during this chunk's products
           if (active) {
 #pragma unroll 1
             for (int c = part; c < CC; c += csplit) {
@@ -455,6 +474,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
               }
             }
           }
+          if (more) store_items(bsel ^ 1);
         }
 
         // horizontal box over the patch width, in place (registers)
@@ -644,6 +664,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
 // The tiled kernel handles: inner product, S_Q = 1, S_K <= 1, P <= 7, Ws <= 9, k <= 16.
 bool tile_supported(const Geo& g) {
   return g.dist == SNLS_DIST_PROD && g.s0 == 1 && g.s1 > 0.f && g.s1 <= 1.0f && g.ps <= 7 && g.ws <= tile::WSMAX &&
+         g.W >= 4 &&
          g.k >= 1 && g.k <= tile::KLIST && (long long)g.Ch * g.HW * 4 < (1LL << 31);
 }
 
