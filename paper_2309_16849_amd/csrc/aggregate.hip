@@ -277,6 +277,246 @@ __global__ void __launch_bounds__(256) aggregate_merged_kernel(const float* __re
   }
 }
 
+// Tiled gather for the query stride S_Q = 1 (every pixel is a query).
+//
+// With S_Q = 1 the contribution of neighbour l of query i to the output
+// pixel y = i + p lands at y + disp_l, i.e. at the offset disp_l from y,
+// whatever the patch offset p.  So the (slot, offset) bin of a (query,
+// neighbour, tap) triple is the same for every pixel the query covers, and
+// it is computed once per tile instead of once per covered pixel:
+//  * phase 1 (all threads): for the tile's covering queries, softmax over
+//    the row, then per neighbour the fixed-point tap weights and the bin of
+//    its first tap in an 8 x 8 box of offsets per frame slot, centred on the
+//    mean offset of the tile's neighbours in that slot (a neighbour whose
+//    taps leave the box, or whose frame is outside the window, is marked
+//    for the direct path);
+//  * phase 2 (one wave per output row, pixel after pixel): the P*P*k
+//    records of the pixel's covering queries are added into the wave's bins
+//    (integer atomics: the sums do not depend on the order), then each
+//    non-empty bin is one position whose channel vector is read once from
+//    the channels-last copy of V (lane = channel), in bin order.
+namespace aggt {
+constexpr int TY = 4, TX = 16;       // output tile; wave w owns tile row w
+constexpr int WAVES = TY;
+constexpr int NSLOT = 7;             // frames per window: 2*wt + 1 <= 7
+constexpr int BOX = 8;               // offsets per axis and slot
+constexpr int SB = BOX * BOX;        // bins per slot (one per lane)
+constexpr int MAXREC = 2304;         // (covering query, neighbour) records per tile
+constexpr int MAXQ = 512;            // covering queries per tile
+constexpr float QSCALE = 16777216.f; // fixed point 2^24
+}  // namespace aggt
+
+__global__ void __launch_bounds__(256) aggregate_tile_kernel(const float* __restrict__ vcl,
+                                                             const float* __restrict__ dists,
+                                                             const float* __restrict__ inds, Geo g, float scale,
+                                                             int tiles_x, int tiles_y, float* __restrict__ out) {
+  using namespace aggt;
+  __shared__ int4 rtap[MAXREC];     // fixed-point tap weights (0,0) (0,1) (1,0) (1,1)
+  __shared__ int rcode[MAXREC];     // bin of tap (0,0); -1 nothing; -2 direct path
+  __shared__ float qm[MAXQ], qinv[MAXQ];  // softmax max and 1/sum per covering query
+  __shared__ int sstat[3 * NSLOT];  // per slot: sum of row offsets, of column offsets, count
+  __shared__ int sbase[2 * NSLOT];  // per slot: box origin (row, column offset)
+  __shared__ int bins[WAVES][NSLOT * SB];
+  __shared__ float obuf[WAVES][64][TX + 1];
+
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  // XCD-aware order: each XCD takes a contiguous run of tiles (neighbouring
+  // tiles read overlapping V regions, which then stay in that XCD's L2).
+  const long long nwg = (long long)gridDim.x;
+  const long long xcd = blockIdx.x % 8, xq = nwg / 8, xrem = nwg % 8;
+  const long long wg = xcd * xq + (xcd < xrem ? xcd : xrem) + blockIdx.x / 8;
+  const long long tiles_img = (long long)tiles_x * tiles_y;
+  const int img = (int)(wg / tiles_img);
+  const int trem = (int)(wg % tiles_img);
+  const int ty = trem / tiles_x, tx = trem % tiles_x;
+  const int t = img % g.T, hd = (img / g.T) % g.HD, b = img / (g.T * g.HD);
+  const int y0 = ty * TY, x0 = tx * TX;
+  const int P = g.ps, K = g.k, nslot = 2 * g.wt + 1;
+  const int QY = TY + P - 1, QX = TX + P - 1, NQ = QY * QX, NR = NQ * K;
+  const int hq0 = y0 - g.lo - P + 1, wq0 = x0 - g.lo - P + 1;  // first covering query
+  const float sscale = (g.dist == SNLS_DIST_PROD ? 1.f : -1.f) * scale;
+  const long long rowb = (((long long)b * g.HD + hd) * g.T + t) * g.nH;
+
+  for (int i = tid; i < WAVES * NSLOT * SB; i += 256) (&bins[0][0])[i] = 0;
+  if (tid < 3 * NSLOT) sstat[tid] = 0;
+
+  // ---- phase 1a: softmax statistics of the covering queries ----
+  for (int j = tid; j < NQ; j += 256) {
+    const int h = hq0 + j / QX, w = wq0 + j % QX;
+    float m = -INFINITY, z = 0.f;
+    if (h >= 0 && h < g.H && w >= 0 && w < g.W) {
+      const float* d = dists + ((rowb + h) * g.nW + w) * K;
+      for (int l = 0; l < K; ++l)
+        if (isfinite(d[l])) m = fmaxf(m, sscale * d[l]);
+      for (int l = 0; l < K; ++l)
+        if (isfinite(d[l])) z += expf(sscale * d[l] - m);
+    }
+    qm[j] = m;
+    qinv[j] = z > 0.f ? 1.f / z : 0.f;
+  }
+  __syncthreads();
+
+  // A neighbour's weight (0: contributes nothing) and its position; the
+  // same tests as the softmax of the other aggregation kernels.
+  auto neighbour = [&](int e, float& wl, int& t2, int& nh, int& nw, float& ah, float& aw) {
+    const int j = e / K, l = e - (e / K) * K;
+    const int h = hq0 + j / QX, w = wq0 + j % QX;
+    wl = 0.f;
+    if (qinv[j] == 0.f) return;  // query outside the frame, or no finite score
+    const long long row = (rowb + h) * g.nW + w;
+    const float d = dists[row * K + l];
+    const float* ind = inds + (row * K + l) * 3;
+    const float tf = ind[0], dh = ind[1], dw = ind[2];
+    const bool ok = isfinite(d) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < 1.0e6f &&
+                    fabsf(dw) < 1.0e6f;
+    if (!ok) return;
+    wl = expf(sscale * d - qm[j]) * qinv[j];
+    t2 = (int)tf;
+    const float fh = floorf(dh), fw = floorf(dw);
+    nh = (int)fh;
+    nw = (int)fw;
+    ah = dh - fh;
+    aw = dw - fw;
+  };
+
+  // ---- phase 1b: mean offset per frame slot (centres the bin boxes) ----
+  for (int e = tid; e < NR; e += 256) {
+    float wl, ah, aw;
+    int t2, nh, nw;
+    neighbour(e, wl, t2, nh, nw, ah, aw);
+    const int slot = t2 - t + g.wt;
+    if (wl != 0.f && slot >= 0 && slot < nslot) {
+      atomicAdd(&sstat[slot], min(max(nh, -4096), 4096));
+      atomicAdd(&sstat[NSLOT + slot], min(max(nw, -4096), 4096));
+      atomicAdd(&sstat[2 * NSLOT + slot], 1);
+    }
+  }
+  __syncthreads();
+  if (tid < NSLOT) {
+    const int c = sstat[2 * NSLOT + tid];
+    sbase[tid] = c ? (int)floorf((float)sstat[tid] / (float)c + 0.5f) - (BOX / 2 - 1) : 0;
+    sbase[NSLOT + tid] = c ? (int)floorf((float)sstat[NSLOT + tid] / (float)c + 0.5f) - (BOX / 2 - 1) : 0;
+  }
+  __syncthreads();
+
+  // ---- phase 1c: records ----
+  for (int e = tid; e < NR; e += 256) {
+    float wl, ah, aw;
+    int t2, nh, nw;
+    neighbour(e, wl, t2, nh, nw, ah, aw);
+    int code = -1;
+    int4 tp = make_int4(0, 0, 0, 0);
+    if (wl != 0.f) {
+      const int slot = t2 - t + g.wt;
+      const int rh = slot >= 0 && slot < nslot ? nh - sbase[slot] : -1;
+      const int rw = slot >= 0 && slot < nslot ? nw - sbase[NSLOT + slot] : -1;
+      code = (rh >= 0 && rh < BOX - 1 && rw >= 0 && rw < BOX - 1) ? slot * SB + rh * BOX + rw : -2;
+      tp.x = __float2int_rn(wl * (1.f - ah) * (1.f - aw) * QSCALE);
+      tp.y = __float2int_rn(wl * (1.f - ah) * aw * QSCALE);
+      tp.z = __float2int_rn(wl * ah * (1.f - aw) * QSCALE);
+      tp.w = __float2int_rn(wl * ah * aw * QSCALE);
+    }
+    rcode[e] = code;
+    rtap[e] = tp;
+  }
+  __syncthreads();
+
+  // ---- phase 2: output row wv, pixel after pixel ----
+  const int y = y0 + wv;
+  const int PPK = P * P * K;
+  const float inv_k = 1.f / (float)K, inv_p = 1.f / (float)P;
+  const float* vb = vcl + (long long)b * g.T * g.HW * g.C + (long long)hd * g.Ch;
+  const int cov_y = cover_count_1d(y, 1, g.nH, g.lo, P);
+  unsigned slots = 0;  // slots with entries in the tile (wave-uniform)
+  for (int s = 0; s < nslot; ++s)
+    if (sstat[2 * NSLOT + s] != 0) slots |= 1u << s;
+  int* const wbins = bins[wv];
+  for (int px = 0; px < TX; ++px) {
+    const int x = x0 + px;
+    if (y >= g.H || x >= g.W) break;  // wave-uniform
+    float acc = 0.f;
+    for (int e0 = 0; e0 < PPK; e0 += 64) {
+      const int e = e0 + lane;
+      // covering query (qy, qx) of the pixel's P x P patch positions, neighbour l
+      const int jq = (int)(((float)e + 0.5f) * inv_k);
+      const int l = e - jq * K;
+      const int qy = (int)(((float)jq + 0.5f) * inv_p);
+      const int qx = jq - qy * P;
+      const int ri = ((wv + qy) * QX + px + qx) * K + l;
+      int code = -1;
+      if (e < PPK) code = rcode[ri];
+      if (code >= 0) {
+        const int4 tp = rtap[ri];
+        if (tp.x) atomicAdd(&wbins[code], tp.x);
+        if (tp.y) atomicAdd(&wbins[code + 1], tp.y);
+        if (tp.z) atomicAdd(&wbins[code + BOX], tp.z);
+        if (tp.w) atomicAdd(&wbins[code + BOX + 1], tp.w);
+      }
+      // neighbours outside the bin boxes: the whole wave reads their taps directly
+      unsigned long long om = __ballot(code == -2);
+      while (om) {
+        const int src = __ffsll((long long)om) - 1;
+        om &= om - 1;
+        const int e_ = __builtin_amdgcn_readlane(ri, src);
+        float wl, ah, aw;
+        int t2, nh, nw;
+        neighbour(e_, wl, t2, nh, nw, ah, aw);
+        const float* vf = vb + (long long)t2 * g.HW * g.C;
+#pragma unroll
+        for (int eh = 0; eh < 2; ++eh)
+#pragma unroll
+          for (int ew = 0; ew < 2; ++ew) {
+            const int Y = y + nh + eh, X = x + nw + ew;
+            const float tw = wl * (eh ? ah : 1.f - ah) * (ew ? aw : 1.f - aw);
+            if (Y >= 0 && Y < g.H && X >= 0 && X < g.W && tw != 0.f && lane < g.Ch)
+              acc = fmaf(tw, vf[((long long)Y * g.W + X) * g.C + lane], acc);
+          }
+      }
+    }
+    wave_lds_sync();
+    // non-empty bins in bin order: one channel-vector read per position
+    for (int s = 0; s < nslot; ++s) {
+      if (!(slots & (1u << s))) continue;
+      const int v = wbins[s * SB + lane];
+      if (v != 0) wbins[s * SB + lane] = 0;
+      const int Y = y + sbase[s] + (lane >> 3), X = x + sbase[NSLOT + s] + (lane & 7);
+      const bool nz = v != 0 && Y >= 0 && Y < g.H && X >= 0 && X < g.W;
+      const int off = ((t + s - g.wt) * (int)g.HW + Y * g.W + X) * g.C;
+      const float wgt = (float)v * (1.f / QSCALE);
+      unsigned long long m = __ballot(nz);
+      // up to 8 positions per pass, their loads in flight together
+      while (m) {
+        const int s0 = __ffsll((long long)m) - 1;
+        m &= m - 1;
+        const int s1 = m ? __ffsll((long long)m) - 1 : s0;
+        const bool two = m != 0;
+        if (two) m &= m - 1;
+        const float w0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wgt), s0));
+        const int o0 = __builtin_amdgcn_readlane(off, s0);
+        const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wgt), s1));
+        const int o1 = __builtin_amdgcn_readlane(off, s1);
+        if (lane < g.Ch) {
+          const float a0 = vb[o0 + lane], a1 = vb[o1 + lane];
+          acc = fmaf(w0, a0, acc);
+          if (two) acc = fmaf(w1, a1, acc);
+        }
+      }
+    }
+    wave_lds_sync();
+    const int cnt = cov_y * cover_count_1d(x, 1, g.nW, g.lo, P);
+    obuf[wv][lane][px] = cnt > 0 ? acc * (1.f / (float)cnt) : 0.f;
+  }
+  // write the row: TX consecutive pixels per channel
+  if (y < g.H) {
+    const int nx = min(TX, g.W - x0);
+    float* ob = out + (((long long)b * g.T + t) * g.C + (long long)hd * g.Ch) * g.HW + (long long)y * g.W + x0;
+    for (int e = lane; e < g.Ch * TX; e += 64) {
+      const int c = e / TX, px = e % TX;
+      if (px < nx) ob[(long long)c * g.HW + px] = obuf[wv][c][px];
+    }
+  }
+}
+
 // Plain per-tap gather for configurations beyond the merged kernel's limits
 // (more than 7 frames per window or more than 256 channels per head).
 constexpr int kAggChunk = 16;
@@ -352,12 +592,24 @@ snls_status launch_aggregate(const float* v, const float* dists, const float* in
   float* wts = static_cast<float*>(ws);
   size_t woff = ((size_t)g.rows * g.k * sizeof(float) + 255) & ~(size_t)255;
   float* vcl = reinterpret_cast<float*>(static_cast<char*>(ws) + woff);
-  hipLaunchKernelGGL(softmax_weights_kernel, dim3((unsigned)((g.rows + 255) / 256)), dim3(256), 0, s, dists, inds, g,
-                     scale, wts);
   const int nslot = 2 * g.wt + 1;
   // merged kernel limits: frames per window, channels per head, 32-bit
   // offsets inside one batch entry, per-bin weight sums below 2^31 in 2^-24
   // fixed point (at most P^2 <= 121 covering patches)
+  const long long nq_tile = (long long)(aggt::TY + g.ps - 1) * (aggt::TX + g.ps - 1);
+  if (g.s0 == 1 && nslot <= aggt::NSLOT && g.Ch <= 64 && (long long)g.T * g.HW * g.C < (1LL << 31) &&
+      g.ps <= 11 && nq_tile <= aggt::MAXQ && nq_tile * g.k <= aggt::MAXREC) {
+    dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
+    hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
+    const int tiles_x = (g.W + aggt::TX - 1) / aggt::TX, tiles_y = (g.H + aggt::TY - 1) / aggt::TY;
+    const long long nwg = (long long)tiles_x * tiles_y * g.B * g.T * g.HD;
+    if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL(aggregate_tile_kernel, dim3((unsigned)nwg), dim3(256), 0, s, vcl, dists, inds, g, scale,
+                       tiles_x, tiles_y, out);
+    return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+  }
+  hipLaunchKernelGGL(softmax_weights_kernel, dim3((unsigned)((g.rows + 255) / 256)), dim3(256), 0, s, dists, inds, g,
+                     scale, wts);
   if (nslot <= agg::NSLOT && g.Ch <= 256 && (long long)g.T * g.HW * g.C < (1LL << 31) && g.ps <= 11) {
     dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
     hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);

@@ -135,6 +135,65 @@ def test_aggregate(dev, case):
     assert_close(out_h[~mask], ref2[~mask], "aggregate (end to end)", scale=rms_finite(ref2))
 
 
+# ------------------------------------------------ tiled aggregation --
+# Query stride 1 with up to 7 frames and 64 channels per head goes through
+# the tiled gather: neighbours of smooth motion land in the per-slot bin
+# boxes; scattered neighbours, frames outside the window and odd caller-given
+# positions take its direct path.
+
+def _motion_inputs(p, seed, amp=4.0):
+    from workloads import make_motion_video
+    r = np.random.default_rng(seed)
+    fr, fl = make_motion_video(r, p["T"], p["C"], p["H"], p["W"], p["wt"], amp)
+    return fr[None].copy(), fl[None].copy()
+
+
+@pytest.mark.parametrize("ps,k,C,HD,scale", [(7, 10, 64, 1, 1.0), (3, 10, 64, 1, 1.0), (5, 16, 32, 2, 0.3),
+                                              (7, 4, 48, 1, 0.05), (1, 12, 64, 1, 1.0)])
+def test_aggregate_tiled_motion(dev, ps, k, C, HD, scale):
+    p = small_params(T=5, C=C, HD=HD, H=37, W=53, ws=9, wt=2, ps=ps, k=k)
+    x, flows = _motion_inputs(p, 9100 + ps + k)
+    v = np.random.default_rng(9200 + ps).standard_normal(x.shape, dtype=np.float32)
+    xd = _d(x, dev)
+    gd, gi = B.snls_search(xd, xd, _d(flows, dev), p)
+    out = B.snls_aggregate(_d(v, dev), gd, gi, p, scale)
+    torch.cuda.synchronize()
+    ref = oracle.aggregate(v, _h(gd), _h(gi), p, scale)
+    assert_close(_h(out), ref, "tiled aggregate (motion neighbours)")
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_aggregate_tiled_odd_neighbours(dev, seed):
+    """Caller-given neighbours: frames outside the window or the clip,
+    non-integer frames, huge and non-finite displacements, non-finite scores,
+    neighbours far from the others (direct path) and integer positions."""
+    p = small_params(T=4, C=64, H=21, W=35, ws=5, wt=1, ps=5, k=6)
+    r = np.random.default_rng(9300 + seed)
+    v = r.standard_normal((1, 4, 64, 21, 35), dtype=np.float32)
+    nH, nW = oracle.grid(p)
+    shp = (1, 1, 4, nH, nW, 6)
+    d = r.standard_normal(shp).astype(np.float32)
+    t_q = np.arange(4)[None, None, :, None, None, None]
+    ind = np.zeros(shp + (3,), np.float32)
+    ind[..., 0] = np.clip(t_q + r.integers(-1, 2, shp), 0, 3)
+    ind[..., 1] = r.uniform(-2, 2, shp).astype(np.float32)
+    ind[..., 2] = r.uniform(-2, 2, shp).astype(np.float32)
+    m = r.random(shp)
+    ind[..., 0] = np.where(m < 0.05, t_q + 2 * (t_q < 2) - (t_q >= 2) * 2, ind[..., 0])  # outside the window
+    ind[..., 1] = np.where((m > 0.05) & (m < 0.1), r.uniform(-30, 30, shp), ind[..., 1])  # far: direct path
+    ind[..., 2] = np.where((m > 0.1) & (m < 0.15), np.round(ind[..., 2]), ind[..., 2])  # integer columns
+    ind[..., 0] = np.where((m > 0.15) & (m < 0.17), 1.5, ind[..., 0])  # not an integer frame
+    ind[..., 0] = np.where((m > 0.17) & (m < 0.19), 7.0, ind[..., 0])  # outside the clip
+    ind[..., 1] = np.where((m > 0.19) & (m < 0.21), 3.0e6, ind[..., 1])  # absurd displacement
+    ind[..., 2] = np.where((m > 0.21) & (m < 0.22), np.nan, ind[..., 2])
+    d = np.where((m > 0.22) & (m < 0.24), -np.inf, d).astype(np.float32)
+    d[0, 0, 1, 3, 4, :] = -np.inf  # a row with no finite score
+    out = B.snls_aggregate(_d(v, dev), _d(d, dev), _d(ind, dev), p, 0.7)
+    torch.cuda.synchronize()
+    ref = oracle.aggregate(v, d, ind, p, 0.7)
+    assert_close(_h(out), ref, "tiled aggregate (odd neighbours)")
+
+
 def _swap_mask(p, swaps):
     """Output pixels covered by a query patch whose top-k had a near-tie swap."""
     mask = np.zeros((p["B"], p["T"], p["C"], p["H"], p["W"]), bool)
