@@ -231,11 +231,12 @@ def main():
     inds = torch.empty(shp + (3,), device=dev)
     out = torch.empty(B.video_shape(p), device=dev)
     ws = B.workspace_for(B.SNLS_OP_AGGREGATE, p, dev)
+    sws = B.workspace_for(B.SNLS_OP_SEARCH, p, dev)
 
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        B.snls_search(x, x, fl, p, dists, inds)
+        B.snls_search(x, x, fl, p, dists, inds, sws)
         if ev is not None:
             ev[1].record()
         B.snls_aggregate(x, dists, inds, p, scale, out, ws)

@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define SNLS_ABI_VERSION 1
+#define SNLS_ABI_VERSION 2
 
 typedef enum {
   SNLS_OK = 0,
@@ -108,11 +108,17 @@ typedef struct {
  *                            inds  (B, HD, T, nH, nW, k, 3)
  *   p->k == 0 every candidate in id order (invalid ones at -inf / +inf):
  *             dists (B, HD, T, nH, nW, (2wt+1)*ws*ws), inds (..., 3)
+ *   workspace device scratch of at least snls_workspace_size(SNLS_OP_SEARCH, p)
+ *             bytes, 256-byte aligned; may be NULL when that size is 0.  The
+ *             top-k path for the inner product with stride0 = 1, stride1 <= 1,
+ *             ps <= 7 and ws <= 9 scores every candidate into it (4 bytes per
+ *             query row and candidate) before selecting; its contents are not
+ *             needed between calls
  * Errors: SNLS_ERR_INVALID_ARG for shapes/parameters out of range or NULL
- * buffers; SNLS_ERR_UNSUPPORTED for k > SNLS_MAX_K; SNLS_ERR_HIP on a launch
- * failure. */
+ * buffers; SNLS_ERR_UNSUPPORTED for k > SNLS_MAX_K; SNLS_ERR_WORKSPACE for a
+ * missing, short or misaligned workspace; SNLS_ERR_HIP on a launch failure. */
 snls_status snls_search(const float* q, const float* k, const float* flows, const snls_params* p, float* dists,
-                        float* inds, void* stream);
+                        float* inds, void* workspace, size_t workspace_bytes, void* stream);
 
 /* snls_topk -- top-L of precomputed scores (Sec. 3.2).
  *   dists_all  device, rows x n_cand scores; column j is candidate id j
@@ -171,7 +177,7 @@ snls_status snls_backward(const float* q, const float* k, const float* v, const 
 #define SNLS_OP_BACKWARD 2
 
 /* Device workspace in bytes that operation op needs for parameters p
- * (0 for search; (size_t)-1 for invalid arguments). */
+ * (0 when none is needed; (size_t)-1 for invalid arguments). */
 size_t snls_workspace_size(int op, const snls_params* p);
 
 /* Static, NUL-terminated description of a status code. */

@@ -25,6 +25,9 @@ snls_status device_ready() {
 
 size_t backward_ws_bytes(const Geo& g) { return (size_t)g.rows * (size_t)g.k * sizeof(float); }
 
+// Only the tiled top-k path needs scratch: the scores of every candidate.
+size_t search_ws_bytes(const Geo& g) { return g.k >= 1 && tile_supported(g) ? tile_ws_bytes(g) : 0; }
+
 }  // namespace
 
 extern "C" {
@@ -44,21 +47,24 @@ const char* snls_status_string(snls_status s) {
 
 size_t snls_workspace_size(int op, const snls_params* p) {
   Geo g;
-  if (op == SNLS_OP_SEARCH) return check_params(p, false, &g) == SNLS_OK ? 0 : (size_t)-1;
+  if (op == SNLS_OP_SEARCH) return check_params(p, false, &g) == SNLS_OK ? search_ws_bytes(g) : (size_t)-1;
   if (op == SNLS_OP_AGGREGATE) return check_params(p, true, &g) == SNLS_OK ? aggregate_ws_bytes(g) : (size_t)-1;
   if (op == SNLS_OP_BACKWARD) return check_params(p, true, &g) == SNLS_OK ? backward_ws_bytes(g) : (size_t)-1;
   return (size_t)-1;
 }
 
 snls_status snls_search(const float* q, const float* k, const float* flows, const snls_params* p, float* dists,
-                        float* inds, void* stream) {
+                        float* inds, void* workspace, size_t workspace_bytes, void* stream) {
   Geo g;
   snls_status st = check_params(p, false, &g);
   if (st != SNLS_OK) return st;
   if (!q || !k || !dists || !inds || (g.wt > 0 && !flows)) return SNLS_ERR_INVALID_ARG;
+  const size_t need = search_ws_bytes(g);
+  if (need > 0 && (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)))
+    return SNLS_ERR_WORKSPACE;
   if ((st = device_ready()) != SNLS_OK) return st;
   if (g.k == 0) return launch_search_full(q, k, flows, g, dists, inds, as_stream(stream));
-  return launch_search_topk(q, k, flows, g, dists, inds, as_stream(stream));
+  return launch_search_topk(q, k, flows, g, dists, inds, workspace, as_stream(stream));
 }
 
 snls_status snls_topk(const float* dists_all, const float* inds_all, int64_t rows, int32_t n_cand, int32_t k,

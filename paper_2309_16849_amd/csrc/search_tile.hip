@@ -31,10 +31,15 @@
 //    writes B for its tile row into the per-query window table Bw (every
 //    (query, cell) entry is written by exactly one lane: deterministic);
 //  * the 4-tap combination (positions and weights from disp_d exactly as
-//    the output reports them), the exact validity test and the top-k
-//    update then run per query.
+//    the output reports them) and the exact validity test give the score of
+//    every window cell, which is written to the caller's workspace
+//    (rows x candidates, candidate id order).
 // A frame whose union of shifts is too wide for the LDS layout is scored
 // directly instead (per candidate, canonical positions).
+//
+// A second kernel then streams each query row's scores once and keeps its
+// top k (Sec. 3.2 top-L over the whole space-time window), so the
+// correlation kernel carries no per-query selection state.
 #include "snls_internal.h"
 
 namespace snls {
@@ -56,33 +61,40 @@ constexpr int WSMAX = 9;
 constexpr int WP = WSMAX + 2;           // window-table pitch (shifts floor(disp_0) .. floor(disp_last) + 1)
 constexpr int WIN = WP * WP;
 constexpr int WSQ = WSMAX * WSMAX;      // candidates per query and frame
-constexpr int KLIST = 16;               // largest top-k capacity
 
 // Staging buffers (double-buffered chunks of CC channels).
 constexpr int KST_F = (CC * KR * KP + 63) / 64 * 64;     // 6528 floats
 constexpr int QST_F = (CC * HROWS * QP + 63) / 64 * 64;  // 1344
 
 
-template <int PS, int KL>
+template <int PS>
 struct Smem {
   static constexpr int QN = (HROWS - PS + 1) * TQW;  // queries per tile
-  static constexpr int NPART = QN <= 80 ? 4 : 2;     // partial top-k lists per query
-  static_assert(QN * WSQ * 5 <= 2 * KST_F * 4, "survivor lists must fit in the K staging buffers");
-  static_assert(QN * NPART <= 1024, "one thread per partial list");
-  float kst[2][KST_F];  // K union region chunks (double buffer); reused for the top-k survivors
+  static_assert(QN * WSQ <= 2 * KST_F, "a frame's scores fit in the K staging buffers");
+  float kst[2][KST_F];  // K union region chunks (double buffer); reused for the frame's scores
   float qst[2][QST_F];  // q halo chunks
-  float bw[QN * WIN];  // per-query window of box sums
-  float lst_s[QN * NPART * KL];  // partial lists (query-major), TopList slot layout
-  int lst_id[QN * NPART * KL];
-  float gthr_s[QN];  // k-th best so far over all partial lists of a query
-  int gthr_id[QN];
-  int nsurv[QN];
+  float bw[QN * WIN];   // per-query window of box sums
   int qlo_h[QN], qlo_w[QN];  // smallest integer shift of the query's window (table origin)
   float qf_h[QN], qf_w[QN];  // the offset itself
   int uni[4];                // min N_h, max N_h, min N_w, max N_w
 };
 
 }  // namespace tile
+
+// Window cell offsets (d_h - r, d_w - r) of a 9 x 9 window by distance from
+// the centre (then row, then column): the first k inside the window seed the
+// threshold of the query frame.
+__constant__ signed char kSpiral[81][2] = {
+    {0, 0}, {-1, 0}, {0, -1}, {0, 1}, {1, 0}, {-1, -1}, {-1, 1}, {1, -1}, {1, 1},
+    {-2, 0}, {0, -2}, {0, 2}, {2, 0}, {-2, -1}, {-2, 1}, {-1, -2}, {-1, 2}, {1, -2},
+    {1, 2}, {2, -1}, {2, 1}, {-2, -2}, {-2, 2}, {2, -2}, {2, 2}, {-3, 0}, {0, -3},
+    {0, 3}, {3, 0}, {-3, -1}, {-3, 1}, {-1, -3}, {-1, 3}, {1, -3}, {1, 3}, {3, -1},
+    {3, 1}, {-3, -2}, {-3, 2}, {-2, -3}, {-2, 3}, {2, -3}, {2, 3}, {3, -2}, {3, 2},
+    {-4, 0}, {0, -4}, {0, 4}, {4, 0}, {-4, -1}, {-4, 1}, {-1, -4}, {-1, 4}, {1, -4},
+    {1, 4}, {4, -1}, {4, 1}, {-3, -3}, {-3, 3}, {3, -3}, {3, 3}, {-4, -2}, {-4, 2},
+    {-2, -4}, {-2, 4}, {2, -4}, {2, 4}, {4, -2}, {4, 2}, {-4, -3}, {-4, 3}, {-3, -4},
+    {-3, 4}, {3, -4}, {3, 4}, {4, -3}, {4, 3}, {-4, -4}, {-4, 4}, {4, -4}, {4, 4},
+};
 
 // Value of lane (i + N) of the same 16-lane row (DPP row_shl:N); lanes whose
 // source lies past the end of the row read 0.
@@ -160,13 +172,12 @@ SNLS_DEV void box_cols(float (&a)[L][S]) {
   }
 }
 
-template <int PS, int KL>
-__global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float* __restrict__ q,
-                                                                      const float* __restrict__ k,
-                                                                      const float* __restrict__ flows, Geo g,
-                                                                      int tiles_x, int tiles_y,
-                                                                      float* __restrict__ dists,
-                                                                      float* __restrict__ inds) {
+template <int PS>
+__global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(const float* __restrict__ q,
+                                                                             const float* __restrict__ k,
+                                                                             const float* __restrict__ flows, Geo g,
+                                                                             int tiles_x, int tiles_y,
+                                                                             float* __restrict__ scores, int pitch) {
   using namespace tile;
   constexpr int TQH = HROWS - PS + 1;
   constexpr int HW = TQW + PS - 1;
@@ -175,9 +186,8 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
   constexpr int NQIT = CC * HROWS * QC4;  // q items per chunk (a multiple of 64)
   static_assert(NQIT % 64 == 0 && NQIT <= NTHREADS, "q items fill whole waves of item slot 1");
   static_assert(CC * KR * ((KP + 3) / 4) <= 2 * NTHREADS - NQIT, "every K item has a slot");
-  constexpr int QN = Smem<PS, KL>::QN;
-  constexpr int NPART = Smem<PS, KL>::NPART;
-  __shared__ Smem<PS, KL> sm;
+  constexpr int QN = Smem<PS>::QN;
+  __shared__ Smem<PS> sm;
 
   const int tid = threadIdx.x;
   const int lane16 = tid & 15;
@@ -203,54 +213,6 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
 
   const float* qb = q + (((long long)b * g.T + t) * g.C + (long long)hd * g.Ch) * g.HW;
 
-  for (int i = tid; i < QN * NPART * KL; i += NTHREADS) {
-    const bool sentinel = i % KL < KL - g.k;  // see TopList
-    sm.lst_s[i] = sentinel ? INFINITY : -INFINITY;
-    sm.lst_id[i] = sentinel ? -1 : 0x7fffffff;
-  }
-  if (tid < QN) {
-    sm.gthr_s[tid] = -INFINITY;
-    sm.gthr_id[tid] = 0x7fffffff;
-  }
-
-  // The k best entries of the union of query j's sorted partial lists, best
-  // first: emit(i, score, id) for i = 0 .. k-1 (a k-way merge).
-  auto merge_parts = [&](int j, auto&& emit) {
-    const int first = KL - g.k;
-    float hs[NPART];
-    int hid[NPART], hp[NPART];
-#pragma unroll
-    for (int pp = 0; pp < NPART; ++pp) {
-      hp[pp] = first;
-      hs[pp] = sm.lst_s[(j * NPART + pp) * KL + first];
-      hid[pp] = sm.lst_id[(j * NPART + pp) * KL + first];
-    }
-    for (int i = 0; i < g.k; ++i) {
-      float bs = hs[0];
-      int bi = hid[0], bp = 0, np = hp[0] + 1;
-#pragma unroll
-      for (int pp = 1; pp < NPART; ++pp)
-        if (ranks_before(hs[pp], hid[pp], bs, bi)) {
-          bs = hs[pp];
-          bi = hid[pp];
-          bp = pp;
-          np = hp[pp] + 1;
-        }
-      emit(i, bs, bi);
-      const int o = (j * NPART + bp) * KL + min(np, KL - 1);
-      const float ns = np < KL ? sm.lst_s[o] : -INFINITY;
-      const int nid = np < KL ? sm.lst_id[o] : 0x7fffffff;
-#pragma unroll
-      for (int pp = 0; pp < NPART; ++pp)
-        if (pp == bp) {
-          hp[pp] = np;
-          hs[pp] = ns;
-          hid[pp] = nid;
-        }
-    }
-  };
-  if (tid < QN) sm.nsurv[tid] = 0;
-
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   constexpr unsigned OOB = 0x80000000u;  // buffer offset past any extent: reads 0
   const int HWi = (int)g.HW;
@@ -272,11 +234,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
   float fh_next = 0.f, fw_next = 0.f;
   bool first = true;
 
-  // Frames are searched nearest first (dt = 0, -1, +1, -2, +2, ...): the
-  // query frame's own matches raise the top-k thresholds early, so fewer
-  // candidates of the later frames survive the filter.  Candidate ids do
-  // not depend on this order, and neither does the result.
-  auto frame_dt = [](int s) { return (s & 1) ? -((s + 1) >> 1) : (s >> 1); };
+  auto frame_dt = [&](int s) { return s - g.wt; };
   for (int si = 0; si <= 2 * g.wt; ++si) {
     const int dt = frame_dt(si);
     const int t2 = t + dt;
@@ -343,10 +301,9 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
     const int dmin_h = u0, UH = u1 - u0 + 1;
     const int dmin_w = u2, UW = u3 - u2 + 1;
     const int nblk = (UW + S - 1) / S;
-    // survivors of the top-k filter, stored over the K staging area once the
-    // frame's correlations are done: score and window cell (dh*ws + dw)
-    float* const surv_s = sm.kst[0];
-    unsigned char* const surv_c = reinterpret_cast<unsigned char*>(sm.kst[0] + QN * WSQ);
+    // the frame's scores, staged over the K staging area once its
+    // correlations are done: query j, window cell dh*ws + dw
+    float* const fsc = &sm.kst[0][0];  // spans both staging buffers
 
     if (nblk <= MAXBLK) {
       // A wave's 4 groups take 4 consecutive shift rows of one column block:
@@ -513,39 +470,29 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
         }
       }
       __syncthreads();
-      // ---- 4-tap combination, exact validity, threshold filter ----
+      // score of window cell (dh, dw) of query j from its box-sum table:
+      // bilinear taps at floor(disp), fraction disp - floor(disp)
+      auto cell_score = [&](int j, int h, int w, int dh, int dw) -> float {
+        const float disp_h = cand_disp(sm.qf_h[j], g.s1, dh, r);
+        const float disp_w = cand_disp(sm.qf_w[j], g.s1, dw, r);
+        const bool ok = centre_ok(h, disp_h, g.H) && centre_ok(w, disp_w, g.W);
+        const float fl_h = floorf(disp_h), fl_w = floorf(disp_w);
+        const float ah = disp_h - fl_h, aw = disp_w - fl_w;
+        // table reads only matter for valid cells
+        const float* r0p = &sm.bw[j * WIN + (ok ? (int)fl_h - sm.qlo_h[j] : 0) * WP];
+        const float* r1p = r0p + WP;
+        const int col = ok ? (int)fl_w - sm.qlo_w[j] : 0;
+        const float top = (1.f - aw) * r0p[col] + aw * r0p[col + 1];
+        const float bot = (1.f - aw) * r1p[col] + aw * r1p[col + 1];
+        const float dv = (1.f - ah) * top + ah * bot;
+        return ok && dv == dv ? dv : -INFINITY;  // NaN scores as invalid
+      };
+      // ---- 4-tap combination and exact validity ----
       for (int e = tid; e < QN * ws; e += NTHREADS) {
         const int j = e / ws, dh = e % ws;
         const int h = y0 + j / TQW, w = x0 + j % TQW;
         if (h >= g.H || w >= g.W) continue;
-        const float fh = sm.qf_h[j], fw = sm.qf_w[j];
-        const int lo_w = sm.qlo_w[j];
-        // the cell's bilinear taps: integer shift floor(disp) and fraction
-        const float disp_h = cand_disp(fh, g.s1, dh, r);
-        const bool okh = centre_ok(h, disp_h, g.H);
-        const float fl_h = floorf(disp_h);
-        const float ah = disp_h - fl_h;
-        const float* r0p = &sm.bw[j * WIN + (okh ? (int)fl_h - sm.qlo_h[j] : 0) * WP];
-        const float* r1p = r0p + WP;
-        const float ts = sm.gthr_s[j];
-        const int ti = sm.gthr_id[j];
-        const int idb = ((dt + g.wt) * ws + dh) * ws;
-        for (int dw = 0; dw < ws; ++dw) {
-          const float disp_w = cand_disp(fw, g.s1, dw, r);
-          const bool ok = okh && centre_ok(w, disp_w, g.W);
-          const float fl_w = floorf(disp_w);
-          const float aw = disp_w - fl_w;
-          const int col = ok ? (int)fl_w - lo_w : 0;  // table reads only matter for valid cells
-          const float top = (1.f - aw) * r0p[col] + aw * r0p[col + 1];
-          const float bot = (1.f - aw) * r1p[col] + aw * r1p[col + 1];
-          const float dv = (1.f - ah) * top + ah * bot;
-          const float d = ok && dv == dv ? dv : -INFINITY;  // NaN scores as invalid
-          if (ranks_before(d, idb + dw, ts, ti)) {
-            const int sl = atomicAdd(&sm.nsurv[j], 1);
-            surv_s[j * WSQ + sl] = d;
-            surv_c[j * WSQ + sl] = (unsigned char)(dh * ws + dw);
-          }
-        }
+        for (int dw = 0; dw < ws; ++dw) fsc[j * WSQ + dh * ws + dw] = cell_score(j, h, w, dh, dw);
       }
     } else {
       // Union too wide for the LDS layout: score this frame directly.
@@ -557,119 +504,157 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_kernel(const float
         const float fh = sm.qf_h[j], fw = sm.qf_w[j];
         const float disp_h = cand_disp(fh, g.s1, dh, r);
         const bool okh = centre_ok(h, disp_h, g.H);
-        const float ts = sm.gthr_s[j];
-        const int ti = sm.gthr_id[j];
-        const int idb = ((dt + g.wt) * ws + dh) * ws;
         for (int dw = 0; dw < ws; ++dw) {
           const float disp_w = cand_disp(fw, g.s1, dw, r);
           float d = -INFINITY;
           if (okh && centre_ok(w, disp_w, g.W)) d = score_candidate(q, k, g, b, hd, t, h, w, t2, disp_h, disp_w);
-          if (ranks_before(d, idb + dw, ts, ti)) {
-            const int sl = atomicAdd(&sm.nsurv[j], 1);
-            surv_s[j * WSQ + sl] = d;
-            surv_c[j * WSQ + sl] = (unsigned char)(dh * ws + dw);
-          }
+          fsc[j * WSQ + dh * ws + dw] = d;
         }
       }
     }
     __syncthreads();
-    // ---- top-k update: NPART threads per query, survivor c goes to part c % NPART ----
-    if (tid < QN * NPART) {
-      const int j = tid / NPART, pp = tid % NPART;
-      const int ns = sm.nsurv[j];
-      if (ns > pp) {
-        TopList<KL> lst;
-        const int lo = tid * KL;
-#pragma unroll
-        for (int i = 0; i < KL; ++i) {
-          lst.s[i] = sm.lst_s[lo + i];
-          lst.id[i] = sm.lst_id[lo + i];
-        }
-        const int idf = (dt + g.wt) * ws * ws;
-        for (int c = pp; c < ns; c += NPART) lst.push(surv_s[j * WSQ + c], idf + surv_c[j * WSQ + c]);
-#pragma unroll
-        for (int i = 0; i < KL; ++i) {
-          sm.lst_s[lo + i] = lst.s[i];
-          sm.lst_id[lo + i] = lst.id[i];
-        }
-      }
-    }
-    __syncthreads();
-    if (tid < QN) {
-      // exact k-th best so far: the next frames keep only candidates that
-      // rank before it (a candidate that does not cannot enter the top k)
-      sm.nsurv[tid] = 0;
-      float ks = -INFINITY;
-      int kid = 0x7fffffff;
-      merge_parts(tid, [&](int, float sc, int id) {
-        ks = sc;
-        kid = id;
-      });
-      sm.gthr_s[tid] = ks;
-      sm.gthr_id[tid] = kid;
-    }
-  }
-
-  // ---- output: complete short lists with the frames outside the clip ----
-  if (tid < QN) {
-    const int j = tid;
-    const int h = y0 + j / TQW, w = x0 + j % TQW;
-    if (h < g.H && w < g.W) {
-      // merge the sorted partial lists into one list (TopList slot layout)
-      TopList<KL> lst;
-      lst.init(g.k);
-      const int first = KL - g.k;
-      merge_parts(j, [&](int i, float sc, int id) {
-#pragma unroll
-        for (int e = 0; e < KL; ++e)
-          if (e == first + i) {
-            lst.s[e] = sc;
-            lst.id[e] = id;
-          }
-      });
-      if (lst.thr_s() == -INFINITY) {
-        for (int dt = -g.wt; dt <= g.wt; ++dt) {
-          if (t + dt >= 0 && t + dt < g.T) continue;
-          for (int c = 0; c < ws * ws; ++c) lst.push(-INFINITY, (dt + g.wt) * ws * ws + c);
-        }
-      }
-      const long long row = ((((long long)b * g.HD + hd) * g.T + t) * g.nH + h) * g.nW + w;
-      float* drow = dists + row * g.k;
-      float* irow = inds + row * g.k * 3;
-      const long long pix = (long long)h * g.W + w;
-#pragma unroll
-      for (int e = 0; e < KL; ++e) {
-        if (e >= first) {
-          const int i = e - first;
-          // every candidate of the window was ranked, so the k best are real
-          // candidates; the clamp only keeps a placeholder id in bounds
-          const int cid = min(lst.id[e], g.ncand - 1);
-          const int dw = cid % ws, dh = (cid / ws) % ws, dt = cid / (ws * ws) - g.wt;
-          float fh = 0.f, fw = 0.f;
-          if (dt != 0) {
-            const long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dt, g.wt)) * 2;
-            fh = flows[base * g.HW + pix];
-            fw = flows[(base + 1) * g.HW + pix];
-          }
-          drow[i] = lst.s[e];
-          irow[3 * i + 0] = (float)(t + dt);
-          irow[3 * i + 1] = cand_disp(fh, g.s1, dh, r);
-          irow[3 * i + 2] = cand_disp(fw, g.s1, dw, r);
-        }
+    // ---- the frame's scores to the workspace: 81 consecutive floats per query row ----
+    {
+      const int ncell = ws * ws;
+      const long long rowb = (((long long)b * g.HD + hd) * g.T + t) * g.nH;
+      const int cbase = (dt + g.wt) * ncell;
+      for (int e = tid; e < QN * ncell; e += NTHREADS) {
+        const int j = e / ncell, c = e - (e / ncell) * ncell;
+        const int h = y0 + j / TQW, w = x0 + j % TQW;
+        if (h < g.H && w < g.W) scores[((rowb + h) * g.nW + w) * pitch + cbase + c] = fsc[j * WSQ + c];
       }
     }
   }
 }
 
-// The tiled kernel handles: inner product, S_Q = 1, S_K <= 1, P <= 7, Ws <= 9, k <= 16.
+// ---- top-k of the scored rows ----
+//
+// One thread per query row, reading its row of scores 32 at a time with
+// 16-byte loads (rows are padded to a multiple of 4 candidates).  A thread
+// first takes as threshold the worst of the k query-frame cells nearest the
+// window centre (a lower bound of its k-th best: the k best of any k
+// candidates rank no higher than the k best of all), so only candidates that
+// rank before the threshold reach its register top-k list.  Candidates of
+// frames outside the clip score as invalid (-inf), in id order.
+namespace tk {
+constexpr int ROWS = 256;  // query rows per workgroup (one per thread)
+constexpr int CK = 32;     // candidates per pass
+constexpr int CP = CK + 4; // private LDS row of a thread (16-byte aligned, spreads the banks)
+}  // namespace tk
+
+template <int KMAX>
+__global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __restrict__ scores, int pitch,
+                                                             const float* __restrict__ flows, Geo g,
+                                                             float* __restrict__ dists, float* __restrict__ inds) {
+  using namespace tk;
+  __shared__ float4 pass_buf[ROWS * CP / 4];  // a thread's current 32 scores, read back by index
+  const int tid = threadIdx.x;
+  const long long row = (long long)blockIdx.x * ROWS + tid;
+  if (row >= g.rows) return;
+  const int ncell = g.ws * g.ws;
+  // query of this row (query stride 1: nH = H, nW = W)
+  const int w = (int)(row % g.nW);
+  const int h = (int)((row / g.nW) % g.nH);
+  const int t = (int)((row / ((long long)g.nW * g.nH)) % g.T);
+  const int b = (int)(row / ((long long)g.nW * g.nH * g.T * g.HD));
+  const float* srow = scores + row * pitch;
+  // candidate ids of the frames inside the clip
+  const int lo = (max(0, t - g.wt) - t + g.wt) * ncell, hi = (min(g.T - 1, t + g.wt) - t + g.wt + 1) * ncell;
+  float ts = -INFINITY;  // threshold entry: candidates ranking after it are skipped
+  int ti = 0x7fffffff;
+  if (g.k <= ncell) {
+    ts = INFINITY;
+    ti = -1;
+    for (int i = 0, n = 0; n < g.k && i < 81; ++i) {
+      const int dh = g.r + kSpiral[i][0], dw = g.r + kSpiral[i][1];
+      if (dh < 0 || dh >= g.ws || dw < 0 || dw >= g.ws) continue;
+      ++n;
+      const int id = (g.wt * g.ws + dh) * g.ws + dw;  // query frame: always inside the clip
+      const float d = srow[id];
+      if (ranks_before(ts, ti, d, id)) {
+        ts = d;
+        ti = id;
+      }
+    }
+  }
+  TopList<KMAX> lst;
+  lst.init(g.k);
+  float4* const mine = &pass_buf[tid * (CP / 4)];
+  for (int c0 = 0; c0 < g.ncand; c0 += CK) {
+    float4 v[CK / 4];
+#pragma unroll
+    for (int i = 0; i < CK / 4; ++i) {
+      const int c = c0 + 4 * i;
+      v[i] = c + 4 > lo && c < hi ? *reinterpret_cast<const float4*>(srow + c)
+                                  : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+    }
+    // the tighter of the seed threshold and the list's k-th entry
+    if (ranks_before(lst.thr_s(), lst.thr_id(), ts, ti)) {
+      ts = lst.thr_s();
+      ti = lst.thr_id();
+    }
+    unsigned mask = 0;
+#pragma unroll
+    for (int i = 0; i < CK / 4; ++i) {
+      const float e[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = c0 + 4 * i + u;
+        const float sc = c >= lo && c < hi ? e[u] : -INFINITY;
+        if (c < g.ncand && (ranks_before(sc, c, ts, ti) || c == ti)) mask |= 1u << (4 * i + u);
+      }
+    }
+    if (mask) {
+#pragma unroll
+      for (int i = 0; i < CK / 4; ++i) mine[i] = v[i];
+      while (mask) {
+        const int j = __ffs(mask) - 1;
+        mask &= mask - 1;
+        const int c = c0 + j;
+        const float sc = c >= lo && c < hi ? reinterpret_cast<const float*>(mine)[j] : -INFINITY;
+        lst.push(sc, c);
+      }
+    }
+  }
+  float* drow = dists + row * g.k;
+  float* irow = inds + row * g.k * 3;
+  const long long pix = (long long)h * g.W + w;
+  const int first = KMAX - g.k;  // slot of the best entry
+#pragma unroll
+  for (int e = 0; e < KMAX; ++e) {
+    if (e >= first) {
+      const int i = e - first;
+      // every candidate was ranked, so the k best are real candidates; the
+      // clamp only keeps a placeholder id in bounds
+      const int cid = min(lst.id[e], g.ncand - 1);
+      const int dw = cid % g.ws, dh = (cid / g.ws) % g.ws, dt = cid / ncell - g.wt;
+      float fh = 0.f, fw = 0.f;
+      if (dt != 0) {
+        const long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dt, g.wt)) * 2;
+        fh = flows[base * g.HW + pix];
+        fw = flows[(base + 1) * g.HW + pix];
+      }
+      drow[i] = lst.s[e];
+      irow[3 * i + 0] = (float)(t + dt);
+      irow[3 * i + 1] = cand_disp(fh, g.s1, dh, g.r);
+      irow[3 * i + 2] = cand_disp(fw, g.s1, dw, g.r);
+    }
+  }
+}
+
+// The tiled path handles: inner product, S_Q = 1, S_K <= 1, P <= 7, Ws <= 9.
 bool tile_supported(const Geo& g) {
   return g.dist == SNLS_DIST_PROD && g.s0 == 1 && g.s1 > 0.f && g.s1 <= 1.0f && g.ps <= 7 && g.ws <= tile::WSMAX &&
-         g.W >= 4 &&
-         g.k >= 1 && g.k <= tile::KLIST && (long long)g.Ch * g.HW * 4 < (1LL << 31);
+         g.W >= 4 && g.k >= 1 && (long long)g.Ch * g.HW * 4 < (1LL << 31);
 }
 
+// Workspace rows hold the scores of one query row, padded to a multiple of
+// 4 candidates (16-byte aligned rows).
+static int tile_ws_pitch(const Geo& g) { return (g.ncand + 3) & ~3; }
+size_t tile_ws_bytes(const Geo& g) { return (size_t)g.rows * (size_t)tile_ws_pitch(g) * sizeof(float); }
+
 snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
-                               float* inds, hipStream_t s) {
+                               float* inds, float* scores, hipStream_t s) {
   const int tqh = tile::HROWS - g.ps + 1;
   const int tiles_x = (g.W + tile::TQW - 1) / tile::TQW;
   const int tiles_y = (g.H + tqh - 1) / tqh;
@@ -677,16 +662,11 @@ snls_status launch_search_tile(const float* q, const float* k, const float* flow
   if (nwg == 0) return SNLS_OK;
   if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
   dim3 grid((unsigned)nwg), block(tile::NTHREADS);
-  const bool small_k = g.k <= 12;
   switch (g.ps) {
-#define SNLS_TILE_CASE(P)                                                                                     \
-  case P:                                                                                                     \
-    if (small_k)                                                                                              \
-      hipLaunchKernelGGL((search_tile_kernel<P, 12>), grid, block, 0, s, q, k, flows, g, tiles_x, tiles_y,     \
-                         dists, inds);                                                                        \
-    else                                                                                                      \
-      hipLaunchKernelGGL((search_tile_kernel<P, 16>), grid, block, 0, s, q, k, flows, g, tiles_x, tiles_y,     \
-                         dists, inds);                                                                        \
+#define SNLS_TILE_CASE(P)                                                                                       \
+  case P:                                                                                                       \
+    hipLaunchKernelGGL((search_tile_scores_kernel<P>), grid, block, 0, s, q, k, flows, g, tiles_x, tiles_y,    \
+                       scores, tile_ws_pitch(g));                                                               \
     break;
     SNLS_TILE_CASE(1)
     SNLS_TILE_CASE(2)
@@ -699,6 +679,23 @@ snls_status launch_search_tile(const float* q, const float* k, const float* flow
     default:
       return SNLS_ERR_UNSUPPORTED;
   }
+  const unsigned tblocks = (unsigned)((g.rows + tk::ROWS - 1) / tk::ROWS);
+  const int pitch = tile_ws_pitch(g);
+  if (g.k <= 12)
+    hipLaunchKernelGGL(tile_topk_kernel<12>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, pitch, flows, g, dists,
+                       inds);
+  else if (g.k <= 16)
+    hipLaunchKernelGGL(tile_topk_kernel<16>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, pitch, flows, g, dists,
+                       inds);
+  else if (g.k <= 32)
+    hipLaunchKernelGGL(tile_topk_kernel<32>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, pitch, flows, g, dists,
+                       inds);
+  else if (g.k <= 64)
+    hipLaunchKernelGGL(tile_topk_kernel<64>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, pitch, flows, g, dists,
+                       inds);
+  else
+    hipLaunchKernelGGL(tile_topk_kernel<128>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, pitch, flows, g, dists,
+                       inds);
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
 }
 

@@ -38,18 +38,22 @@ snls_status check_topk_args(int64_t rows, int32_t n_cand, int32_t k, int32_t dis
 // channels-last copy of V, 256-byte aligned.
 size_t aggregate_ws_bytes(const Geo& g);
 
+// The tiled search path (inner product, S_Q = 1, S_K <= 1, P <= 7, Ws <= 9)
+// and its workspace: the score of every candidate (rows x candidates fp32).
+bool tile_supported(const Geo& g);
+size_t tile_ws_bytes(const Geo& g);
+
 #ifdef __HIPCC__
 
 // Launchers (one per kernel family); all return SNLS_OK or SNLS_ERR_HIP.
 snls_status launch_search_full(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, hipStream_t s);
 snls_status launch_search_topk(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
-                               float* inds, hipStream_t s);
+                               float* inds, void* ws, hipStream_t s);
 snls_status launch_search_topk_direct(const float* q, const float* k, const float* flows, const Geo& g,
                                       float* dists, float* inds, hipStream_t s);
 snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
-                               float* inds, hipStream_t s);
-bool tile_supported(const Geo& g);
+                               float* inds, float* scores, hipStream_t s);
 snls_status launch_topk(const float* dall, const float* iall, int64_t rows, int ncand, int k, int dist,
                         float* dists, float* inds, hipStream_t s);
 snls_status launch_aggregate(const float* v, const float* dists, const float* inds, const Geo& g, float scale,

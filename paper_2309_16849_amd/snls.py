@@ -53,7 +53,7 @@ def load_library():
         lib = ctypes.CDLL(LIB_PATH)
         P, F32, I32, I64, SZ = ctypes.c_void_p, ctypes.c_float, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
         PP = ctypes.POINTER(SnlsParams)
-        lib.snls_search.argtypes = [P, P, P, PP, P, P, P]
+        lib.snls_search.argtypes = [P, P, P, PP, P, P, P, SZ, P]
         lib.snls_topk.argtypes = [P, P, I64, I32, I32, I32, P, P, P]
         lib.snls_aggregate.argtypes = [P, P, P, PP, F32, P, P, SZ, P]
         lib.snls_backward.argtypes = [P] * 8 + [PP, F32, P, P, P, P, P, SZ, P]
@@ -134,8 +134,9 @@ def out_shape(p: dict):
     return (p["B"], p["HD"], p["T"], nH, nW, kk)
 
 
-def snls_search(q, k, flows, p: dict, dists=None, inds=None, stream=None):
-    """Shifted non-local search; returns (dists, inds) (see include/snls.h)."""
+def snls_search(q, k, flows, p: dict, dists=None, inds=None, workspace=None, stream=None):
+    """Shifted non-local search; returns (dists, inds) (see include/snls.h).
+    The workspace is allocated here when not given (its size may be 0)."""
     lib = load_library()
     _dev(q, "q", video_shape(p))
     _dev(k, "k", video_shape(p))
@@ -148,9 +149,11 @@ def snls_search(q, k, flows, p: dict, dists=None, inds=None, stream=None):
         inds = torch.empty(shp + (3,), device=q.device, dtype=torch.float32)
     _dev(dists, "dists", shp)
     _dev(inds, "inds", shp + (3,))
+    if workspace is None:
+        workspace = workspace_for(SNLS_OP_SEARCH, p, q.device)
     prm = params_from_dict(p)
     _check(lib.snls_search(_ptr(q), _ptr(k), _ptr(flows), ctypes.byref(prm), _ptr(dists), _ptr(inds),
-                           _stream(stream)), "snls_search")
+                           _ptr(workspace), workspace.numel() * 4, _stream(stream)), "snls_search")
     return dists, inds
 
 

@@ -13,6 +13,7 @@ from paper_2309_16849_amd import snls as B
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "snls.h")
 FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
+BIG = 1 << 40  # workspace size argument large enough for any case below
 
 
 def _declared_functions():
@@ -40,7 +41,7 @@ def test_exports_every_declared_function(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert B.snls_abi_version() == 1
+    assert B.snls_abi_version() == 2
     assert B.snls_status_string(0) == "ok"
     for s in range(1, 5):
         assert B.snls_status_string(s) not in ("ok", "unknown status")
@@ -58,27 +59,27 @@ BAD_PARAMS = [
 @pytest.mark.parametrize("kw", BAD_PARAMS, ids=[str(k) for k in BAD_PARAMS])
 def test_search_rejects_bad_params(lib, kw):
     prm = _params(**kw)
-    st = lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, None)
+    st = lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, FAKE, BIG, None)
     assert st == B.SNLS_ERR_INVALID_ARG
 
 
 def test_search_rejects_bad_struct_size_and_nulls(lib):
     prm = _params()
     prm.struct_size = 12
-    assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, FAKE, BIG, None) == B.SNLS_ERR_INVALID_ARG
     prm = _params()
-    assert lib.snls_search(FAKE, FAKE, FAKE, None, FAKE, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_search(FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, BIG, None) == B.SNLS_ERR_INVALID_ARG
     for i in range(5):
         args = [FAKE] * 5
         args[i] = None
         q, k, fl, d, ind = args
-        assert lib.snls_search(q, k, fl, ctypes.byref(prm), d, ind, None) == B.SNLS_ERR_INVALID_ARG
+        assert lib.snls_search(q, k, fl, ctypes.byref(prm), d, ind, FAKE, BIG, None) == B.SNLS_ERR_INVALID_ARG
     # flows may be NULL when wt == 0: the call then passes validation (checked below without a device)
 
 
 def test_k_limits(lib):
     prm = _params(ws=15, wt=1, k=B.SNLS_MAX_K + 1)
-    assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, None) == B.SNLS_ERR_UNSUPPORTED
+    assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, FAKE, BIG, None) == B.SNLS_ERR_UNSUPPORTED
     assert lib.snls_topk(FAKE, FAKE, 10, 500, B.SNLS_MAX_K + 1, 0, FAKE, FAKE, None) == B.SNLS_ERR_UNSUPPORTED
     for rows, nc, k, dt in ((-1, 10, 2, 0), (5, 0, 1, 0), (5, 10, 0, 0), (5, 10, 11, 0), (5, 10, 2, 3)):
         assert lib.snls_topk(FAKE, FAKE, rows, nc, k, dt, FAKE, FAKE, None) == B.SNLS_ERR_INVALID_ARG
@@ -109,16 +110,32 @@ def test_aggregate_and_backward_validation(lib):
     assert st == B.SNLS_ERR_WORKSPACE  # not 256-byte aligned
     st = lib.snls_backward(*args, ctypes.byref(prm), 1.0, FAKE, FAKE, FAKE, None, FAKE, need, None)
     assert st == B.SNLS_ERR_INVALID_ARG  # grad_flows required when wt > 0
-    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(prm)) == 0
     assert lib.snls_workspace_size(7, ctypes.byref(prm)) == ctypes.c_size_t(-1).value
     bad = _params(ws=0)
     assert lib.snls_workspace_size(B.SNLS_OP_BACKWARD, ctypes.byref(bad)) == ctypes.c_size_t(-1).value
 
 
+def test_search_workspace(lib):
+    """The tiled top-k path (inner product, stride0 = 1, stride1 <= 1, ps <= 7,
+    ws <= 9) scores every candidate into the workspace; other paths need none."""
+    prm = _params()
+    rows, ncand = 1 * 2 * 3 * 16 * 17, 3 * 3 * 3
+    need = lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(prm))
+    assert need == rows * ((ncand + 3) // 4 * 4) * 4  # rows padded to a multiple of 4 candidates
+    for kw in (dict(k=0), dict(dist_type=1), dict(stride0=2), dict(stride1=1.5), dict(ps=9), dict(ws=11, k=4)):
+        assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(**kw))) == 0, kw
+    assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, None, BIG, None) == B.SNLS_ERR_WORKSPACE
+    assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, FAKE, need - 1,
+                           None) == B.SNLS_ERR_WORKSPACE
+    assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, ctypes.c_void_p(0x1104), need,
+                           None) == B.SNLS_ERR_WORKSPACE  # not 256-byte aligned
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=0))) == ctypes.c_size_t(-1).value
+
+
 @pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device error path")
 def test_valid_call_without_device_reports_hip_error(lib):
     prm = _params(wt=0)
-    assert lib.snls_search(FAKE, FAKE, None, ctypes.byref(prm), FAKE, FAKE, None) == B.SNLS_ERR_HIP
+    assert lib.snls_search(FAKE, FAKE, None, ctypes.byref(prm), FAKE, FAKE, FAKE, BIG, None) == B.SNLS_ERR_HIP
 
 
 def test_binding_refuses_cpu_tensors():
