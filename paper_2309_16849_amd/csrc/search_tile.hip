@@ -70,8 +70,7 @@ constexpr int QST_F = (CC * HROWS * QP + 63) / 64 * 64;  // 1344
 template <int PS>
 struct Smem {
   static constexpr int QN = (HROWS - PS + 1) * TQW;  // queries per tile
-  static_assert(QN * WSQ <= 2 * KST_F, "a frame's scores fit in the K staging buffers");
-  float kst[2][KST_F];  // K union region chunks (double buffer); reused for the frame's scores
+  float kst[2][KST_F];  // K union region chunks (double buffer)
   float qst[2][QST_F];  // q halo chunks
   float bw[QN * WIN];   // per-query window of box sums
   int qlo_h[QN], qlo_w[QN];  // smallest integer shift of the query's window (table origin)
@@ -237,6 +236,8 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
   auto frame_dt = [&](int s) { return s - g.wt; };
   for (int si = 0; si <= 2 * g.wt; ++si) {
     const int dt = frame_dt(si);
+    const long long rowb = (((long long)b * g.HD + hd) * g.T + t) * g.nH;
+    const int cbase = (dt + g.wt) * ws * ws;
     const int t2 = t + dt;
     if (t2 < 0 || t2 >= g.T) continue;
     const float* kb = k + (((long long)b * g.T + t2) * g.C + (long long)hd * g.Ch) * g.HW;
@@ -301,9 +302,6 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
     const int dmin_h = u0, UH = u1 - u0 + 1;
     const int dmin_w = u2, UW = u3 - u2 + 1;
     const int nblk = (UW + S - 1) / S;
-    // the frame's scores, staged over the K staging area once its
-    // correlations are done: query j, window cell dh*ws + dw
-    float* const fsc = &sm.kst[0][0];  // spans both staging buffers
 
     if (nblk <= MAXBLK) {
       // A wave's 4 groups take 4 consecutive shift rows of one column block:
@@ -492,7 +490,8 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
         const int j = e / ws, dh = e % ws;
         const int h = y0 + j / TQW, w = x0 + j % TQW;
         if (h >= g.H || w >= g.W) continue;
-        for (int dw = 0; dw < ws; ++dw) fsc[j * WSQ + dh * ws + dw] = cell_score(j, h, w, dh, dw);
+        float* srow = scores + ((rowb + h) * g.nW + w) * pitch + cbase + dh * ws;
+        for (int dw = 0; dw < ws; ++dw) srow[dw] = cell_score(j, h, w, dh, dw);
       }
     } else {
       // Union too wide for the LDS layout: score this frame directly.
@@ -508,22 +507,11 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
           const float disp_w = cand_disp(fw, g.s1, dw, r);
           float d = -INFINITY;
           if (okh && centre_ok(w, disp_w, g.W)) d = score_candidate(q, k, g, b, hd, t, h, w, t2, disp_h, disp_w);
-          fsc[j * WSQ + dh * ws + dw] = d;
+          scores[((rowb + h) * g.nW + w) * pitch + cbase + dh * ws + dw] = d;
         }
       }
     }
     __syncthreads();
-    // ---- the frame's scores to the workspace: 81 consecutive floats per query row ----
-    {
-      const int ncell = ws * ws;
-      const long long rowb = (((long long)b * g.HD + hd) * g.T + t) * g.nH;
-      const int cbase = (dt + g.wt) * ncell;
-      for (int e = tid; e < QN * ncell; e += NTHREADS) {
-        const int j = e / ncell, c = e - (e / ncell) * ncell;
-        const int h = y0 + j / TQW, w = x0 + j % TQW;
-        if (h < g.H && w < g.W) scores[((rowb + h) * g.nW + w) * pitch + cbase + c] = fsc[j * WSQ + c];
-      }
-    }
   }
 }
 
