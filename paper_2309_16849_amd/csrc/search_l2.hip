@@ -1,0 +1,205 @@
+// search_l2.hip -- norm terms of the squared L2 distance for the tiled
+// search (Sec. 3.2 patch similarity, L2 form).
+//
+// For a candidate at displacement disp of query (b, t, h, w) the squared L2
+// distance over the query's in-frame patch pixels p and the head's channels is
+//     d = sum_p |q(h+p)|^2 - 2 sum_p <q(h+p), k~(h+p+disp)> + sum_p |k~(h+p+disp)|^2 .
+// The middle term is the inner-product score the tiled kernel computes; this
+// file computes the two norm terms:
+//   Qn(query)       = sum over in-frame patch pixels of |q|^2;
+//   G(query, cell)  = sum over in-frame patch pixels p of |k~(h+p+disp_cell)|^2.
+// With key stride S_K = 1 every cell of a query's window in one frame has the
+// same bilinear fraction a = F - floor(F), so |k~|^2 is evaluated once per
+// position of the (ws + P - 1)^2 region the window's patches cover, and G is
+// a box sum of those values over the patch rows and columns that lie inside
+// the frame.  (Per-cell fractions of fl32(F + d - r) can differ from a by
+// rounding in the last bit; the effect on G is far below the fp32 score
+// tolerance, and the positions reported come from the exact per-cell values.)
+#include "snls_internal.h"
+
+namespace snls {
+
+namespace l2n {
+constexpr int TY = 4, TX = 8;        // query tile
+constexpr int NQ = TY * TX;          // queries per workgroup
+constexpr int TPQ = 8;               // threads per query
+constexpr int NT = NQ * TPQ;         // 256
+constexpr int EG = 16;               // per-query grid of positions (ws + P - 1 <= 15, one spare)
+constexpr int PPT = EG * EG / TPQ;   // positions per thread
+constexpr int CC = 8;                // channels per staging chunk
+constexpr int RH = 32, RW = 40;      // union region of the tile (rows, columns), +1 tap included
+constexpr int RP = RW + 1;           // region row pitch (odd)
+constexpr int WSMAX = 9;             // window side
+constexpr int GRIDS = NQ * EG * EG;  // per-query |k~|^2 grids
+constexpr int VSUM = NQ * WSMAX * EG;  // per-query column sums
+constexpr int REGF = CC * RH * RP > GRIDS + VSUM ? CC * RH * RP : GRIDS + VSUM;
+}  // namespace l2n
+
+// One workgroup = a TY x TX tile of queries of one (b, head, t) and one
+// frame step dt (grid z = dt + wt).
+__global__ void __launch_bounds__(l2n::NT) l2_norms_kernel(const float* __restrict__ q, const float* __restrict__ k,
+                                                          const float* __restrict__ flows, Geo g, int tiles_x,
+                                                          float* __restrict__ G, int pitch,
+                                                          float* __restrict__ Qn) {
+  using namespace l2n;
+  __shared__ float reg[REGF];  // K region chunk; then the per-query |k~|^2 grids and column sums
+  __shared__ int ubox[4];              // union: min row, max row, min col, max col (region origins)
+  __shared__ int qoy[NQ], qox[NQ];     // query's grid origin inside the region
+  __shared__ float qpart[NT];
+
+  const int tid = threadIdx.x, jq = tid / TPQ, sub = tid % TPQ;
+  const int dt = (int)blockIdx.z - g.wt;
+  const int img = (int)blockIdx.y;  // (b, hd, t)
+  const int t = img % g.T, hd = (img / g.T) % g.HD, b = img / (g.T * g.HD);
+  const int t2 = t + dt;
+  if (t2 < 0 || t2 >= g.T) return;  // whole workgroup
+  const int ty = (int)blockIdx.x / tiles_x, tx = (int)blockIdx.x % tiles_x;
+  const int h = ty * TY + jq / TX, w = tx * TX + jq % TX;
+  const bool inside = h < g.H && w < g.W;
+  const int E = g.ws + g.ps - 1;  // grid side used (<= 15)
+
+  // offset of the query's window and the integer origin of its grid
+  float fh = 0.f, fw = 0.f;
+  if (dt != 0 && inside) {
+    const long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dt, g.wt)) * 2;
+    const long long pix = (long long)h * g.W + w;
+    fh = flows[base * g.HW + pix];
+    fw = flows[(base + 1) * g.HW + pix];
+  }
+  // non-finite or absurd offsets: their candidates are invalid (the inner
+  // product pass scores them so); any G value does
+  const float fh_u = fabsf(fh) < 1.0e6f ? fh : 0.f, fw_u = fabsf(fw) < 1.0e6f ? fw : 0.f;
+  const float flh = floorf(fh_u), flw = floorf(fw_u);
+  const int oy = h + g.lo + (int)flh - g.r, ox = w + g.lo + (int)flw - g.r;  // key coords of grid (0, 0)
+  if (tid < 4) ubox[tid] = (tid & 1) ? INT_MIN : INT_MAX;
+  __syncthreads();
+  if (sub == 0 && inside) {
+    atomicMin(&ubox[0], oy);
+    atomicMax(&ubox[1], oy);
+    atomicMin(&ubox[2], ox);
+    atomicMax(&ubox[3], ox);
+  }
+  __syncthreads();
+  const int ry0 = ubox[0], rx0 = ubox[2];
+  const int rh = ubox[1] - ry0 + E + 1, rw = ubox[3] - rx0 + E + 1;  // region extent (taps included)
+  const bool staged = ubox[1] >= ubox[0] && rh <= RH && rw <= RW;  // else read K from global memory
+  if (sub == 0) {
+    qoy[jq] = oy - ry0;
+    qox[jq] = ox - rx0;
+  }
+  const float ah = fh_u - flh, aw = fw_u - flw;
+
+  const float* kb = k + (((long long)b * g.T + t2) * g.C + (long long)hd * g.Ch) * g.HW;
+  float acc[PPT];
+#pragma unroll
+  for (int i = 0; i < PPT; ++i) acc[i] = 0.f;
+
+  // key value at (y, x) of channel plane c: 0 outside the frame
+  auto kval = [&](int c, int y, int x) -> float {
+    return (y >= 0 && y < g.H && x >= 0 && x < g.W) ? kb[(long long)c * g.HW + (long long)y * g.W + x] : 0.f;
+  };
+  for (int c0 = 0; c0 < g.Ch; c0 += CC) {
+    const int nc = min(CC, g.Ch - c0);
+    if (staged) {
+      __syncthreads();  // previous chunk fully read
+      for (int e = tid; e < nc * rh * rw; e += NT) {
+        const int c = e / (rh * rw), rem = e - c * (rh * rw);
+        const int yy = rem / rw, xx = rem - yy * rw;
+        reg[(c * RH + yy) * RP + xx] = kval(c0 + c, ry0 + yy, rx0 + xx);
+      }
+      __syncthreads();
+    }
+    if (inside) {
+      for (int c = 0; c < nc; ++c) {
+#pragma unroll
+        for (int i = 0; i < PPT; ++i) {
+          const int z = sub + TPQ * i, zy = z / EG, zx = z % EG;
+          if (zy < E && zx < E) {
+            float v00, v01, v10, v11;
+            if (staged) {
+              const float* rp = &reg[(c * RH + qoy[jq] + zy) * RP + qox[jq] + zx];
+              v00 = rp[0];
+              v01 = rp[1];
+              v10 = rp[RP];
+              v11 = rp[RP + 1];
+            } else {
+              const int y = oy + zy, x = ox + zx;
+              v00 = kval(c0 + c, y, x);
+              v01 = kval(c0 + c, y, x + 1);
+              v10 = kval(c0 + c, y + 1, x);
+              v11 = kval(c0 + c, y + 1, x + 1);
+            }
+            const float top = (1.f - aw) * v00 + aw * v01;
+            const float bot = (1.f - aw) * v10 + aw * v11;
+            const float kv = (1.f - ah) * top + ah * bot;
+            acc[i] = fmaf(kv, kv, acc[i]);
+          }
+        }
+      }
+    }
+  }
+  // the query's grid of |k~|^2 into LDS (over the region buffer)
+  __syncthreads();
+  float* gq = &reg[jq * EG * EG];
+#pragma unroll
+  for (int i = 0; i < PPT; ++i) gq[sub + TPQ * i] = acc[i];  // zero for queries outside the frame
+  __syncthreads();
+  // patch rows and columns whose query pixel is inside the frame
+  const int ip0 = max(0, -h - g.lo), ip1 = min(g.ps - 1, g.H - 1 - h - g.lo);
+  const int jp0 = max(0, -w - g.lo), jp1 = min(g.ps - 1, g.W - 1 - w - g.lo);
+  // column sums over the valid patch rows, for window row dh and grid column x
+  float* vs = &reg[GRIDS + jq * WSMAX * EG];
+  if (inside) {
+    for (int e = sub; e < g.ws * E; e += TPQ) {
+      const int dh = e / E, x = e % E;
+      float sacc = 0.f;
+      for (int ip = ip0; ip <= ip1; ++ip) sacc += gq[(ip + dh) * EG + x];
+      vs[dh * EG + x] = sacc;
+    }
+  }
+  __syncthreads();
+  if (!inside) return;  // no barrier follows
+  const long long row = ((((long long)b * g.HD + hd) * g.T + t) * g.nH + h) * g.nW + w;
+  float* grow = G + row * pitch + (dt + g.wt) * g.ws * g.ws;
+  for (int e = sub; e < g.ws * g.ws; e += TPQ) {
+    const int dh = e / g.ws, dw = e % g.ws;
+    float sacc = 0.f;
+    for (int jp = jp0; jp <= jp1; ++jp) sacc += vs[dh * EG + jp + dw];
+    grow[e] = sacc;
+  }
+  if (dt == 0) {
+    // |q|^2 over the in-frame patch pixels (once per query: the query frame's workgroup)
+    const float* qb = q + (((long long)b * g.T + t) * g.C + (long long)hd * g.Ch) * g.HW;
+    float sq = 0.f;
+    const int pw_n = jp1 - jp0 + 1, npix = (ip1 - ip0 + 1) * pw_n;
+    for (int e = sub; e < npix * g.Ch; e += TPQ) {
+      const int c = e / npix, pp = e % npix;
+      const int y = h + g.lo + ip0 + pp / pw_n, x = w + g.lo + jp0 + pp % pw_n;
+      const float qv = qb[(long long)c * g.HW + (long long)y * g.W + x];
+      sq = fmaf(qv, qv, sq);
+    }
+    qpart[tid] = sq;
+    // the query's TPQ threads are lanes of one wave: order its LDS accesses
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (sub == 0) {
+      float tot = 0.f;
+      for (int i = 0; i < TPQ; ++i) tot += qpart[tid + i];
+      Qn[row] = tot;
+    }
+  }
+}
+
+snls_status launch_l2_norms(const float* q, const float* k, const float* flows, const Geo& g, float* G, int pitch,
+                            float* Qn, hipStream_t s) {
+  const int tiles_x = (g.W + l2n::TX - 1) / l2n::TX, tiles_y = (g.H + l2n::TY - 1) / l2n::TY;
+  const long long ntile = (long long)tiles_x * tiles_y;
+  if (ntile == 0 || g.rows == 0) return SNLS_OK;
+  if (ntile > 0x7fffffffLL || (long long)g.B * g.HD * g.T > 65535 || 2 * g.wt + 1 > 65535) return SNLS_ERR_UNSUPPORTED;
+  dim3 grid((unsigned)ntile, (unsigned)(g.B * g.HD * g.T), (unsigned)(2 * g.wt + 1));
+  hipLaunchKernelGGL(l2_norms_kernel, grid, dim3(l2n::NT), 0, s, q, k, flows, g, tiles_x, G, pitch, Qn);
+  return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+}
+
+}  // namespace snls

@@ -531,7 +531,9 @@ constexpr int CP = CK + 4; // private LDS row of a thread (16-byte aligned, spre
 }  // namespace tk
 
 template <int KMAX>
-__global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __restrict__ scores, int pitch,
+__global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __restrict__ scores,
+                                                             const float* __restrict__ gnorm,
+                                                             const float* __restrict__ qnorm, int pitch,
                                                              const float* __restrict__ flows, Geo g,
                                                              float* __restrict__ dists, float* __restrict__ inds) {
   using namespace tk;
@@ -546,6 +548,16 @@ __global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __rest
   const int t = (int)((row / ((long long)g.nW * g.nH)) % g.T);
   const int b = (int)(row / ((long long)g.nW * g.nH * g.T * g.HD));
   const float* srow = scores + row * pitch;
+  // ranking score of a candidate: the inner product, or minus the squared L2
+  // distance |q|^2 - 2 <q, k~> + |k~|^2 from the norm terms (invalid: -inf)
+  const bool l2 = g.dist == SNLS_DIST_L2;
+  const float qn = l2 ? qnorm[row] : 0.f;
+  const float* grow = l2 ? gnorm + row * pitch : nullptr;
+  auto rank_score = [&](float ip, float gn) -> float {
+    if (!l2) return ip;
+    const float dd = qn - 2.f * ip + gn;
+    return ip > -INFINITY && dd == dd ? -dd : -INFINITY;
+  };
   // candidate ids of the frames inside the clip
   const int lo = (max(0, t - g.wt) - t + g.wt) * ncell, hi = (min(g.T - 1, t + g.wt) - t + g.wt + 1) * ncell;
   float ts = -INFINITY;  // threshold entry: candidates ranking after it are skipped
@@ -558,7 +570,7 @@ __global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __rest
       if (dh < 0 || dh >= g.ws || dw < 0 || dw >= g.ws) continue;
       ++n;
       const int id = (g.wt * g.ws + dh) * g.ws + dw;  // query frame: always inside the clip
-      const float d = srow[id];
+      const float d = rank_score(srow[id], l2 ? grow[id] : 0.f);
       if (ranks_before(ts, ti, d, id)) {
         ts = d;
         ti = id;
@@ -575,6 +587,17 @@ __global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __rest
       const int c = c0 + 4 * i;
       v[i] = c + 4 > lo && c < hi ? *reinterpret_cast<const float4*>(srow + c)
                                   : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+    }
+    if (l2) {
+#pragma unroll
+      for (int i = 0; i < CK / 4; ++i) {
+        const int c = c0 + 4 * i;
+        if (c + 4 > lo && c < hi) {
+          const float4 gn = *reinterpret_cast<const float4*>(grow + c);
+          v[i] = make_float4(rank_score(v[i].x, gn.x), rank_score(v[i].y, gn.y), rank_score(v[i].z, gn.z),
+                             rank_score(v[i].w, gn.w));
+        }
+      }
     }
     // the tighter of the seed threshold and the list's k-th entry
     if (ranks_before(lst.thr_s(), lst.thr_id(), ts, ti)) {
@@ -622,7 +645,7 @@ __global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __rest
         fh = flows[base * g.HW + pix];
         fw = flows[(base + 1) * g.HW + pix];
       }
-      drow[i] = lst.s[e];
+      drow[i] = from_score(lst.s[e], g.dist);
       irow[3 * i + 0] = (float)(t + dt);
       irow[3 * i + 1] = cand_disp(fh, g.s1, dh, g.r);
       irow[3 * i + 2] = cand_disp(fw, g.s1, dw, g.r);
@@ -630,16 +653,25 @@ __global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __rest
   }
 }
 
-// The tiled path handles: inner product, S_Q = 1, S_K <= 1, P <= 7, Ws <= 9.
+// The tiled path handles S_Q = 1, P <= 7, Ws <= 9 with the inner product
+// (S_K <= 1) or the squared L2 distance (S_K = 1).
 bool tile_supported(const Geo& g) {
-  return g.dist == SNLS_DIST_PROD && g.s0 == 1 && g.s1 > 0.f && g.s1 <= 1.0f && g.ps <= 7 && g.ws <= tile::WSMAX &&
-         g.W >= 4 && g.k >= 1 && (long long)g.Ch * g.HW * 4 < (1LL << 31);
+  const bool dist_ok = g.dist == SNLS_DIST_PROD ? g.s1 > 0.f && g.s1 <= 1.0f : g.s1 == 1.0f;
+  return dist_ok && g.s0 == 1 && g.ps <= 7 && g.ws <= tile::WSMAX && g.W >= 4 && g.k >= 1 &&
+         (long long)g.Ch * g.HW * 4 < (1LL << 31);
 }
 
 // Workspace rows hold the scores of one query row, padded to a multiple of
 // 4 candidates (16-byte aligned rows).
 static int tile_ws_pitch(const Geo& g) { return (g.ncand + 3) & ~3; }
-size_t tile_ws_bytes(const Geo& g) { return (size_t)g.rows * (size_t)tile_ws_pitch(g) * sizeof(float); }
+static size_t tile_plane_bytes(const Geo& g) {
+  return ((size_t)g.rows * (size_t)tile_ws_pitch(g) * sizeof(float) + 255) & ~(size_t)255;
+}
+size_t tile_ws_bytes(const Geo& g) {
+  size_t b = tile_plane_bytes(g);                             // inner-product scores
+  if (g.dist == SNLS_DIST_L2) b += tile_plane_bytes(g) + (size_t)g.rows * sizeof(float);  // key and query norms
+  return b;
+}
 
 snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, float* scores, hipStream_t s) {
@@ -667,23 +699,31 @@ snls_status launch_search_tile(const float* q, const float* k, const float* flow
     default:
       return SNLS_ERR_UNSUPPORTED;
   }
-  const unsigned tblocks = (unsigned)((g.rows + tk::ROWS - 1) / tk::ROWS);
   const int pitch = tile_ws_pitch(g);
+  float* gnorm = nullptr;
+  float* qnorm = nullptr;
+  if (g.dist == SNLS_DIST_L2) {
+    gnorm = reinterpret_cast<float*>(reinterpret_cast<char*>(scores) + tile_plane_bytes(g));
+    qnorm = reinterpret_cast<float*>(reinterpret_cast<char*>(gnorm) + tile_plane_bytes(g));
+    const snls_status st = launch_l2_norms(q, k, flows, g, gnorm, pitch, qnorm, s);
+    if (st != SNLS_OK) return st;
+  }
+  const unsigned tblocks = (unsigned)((g.rows + tk::ROWS - 1) / tk::ROWS);
   if (g.k <= 12)
-    hipLaunchKernelGGL(tile_topk_kernel<12>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, pitch, flows, g, dists,
-                       inds);
+    hipLaunchKernelGGL(tile_topk_kernel<12>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
+                       g, dists, inds);
   else if (g.k <= 16)
-    hipLaunchKernelGGL(tile_topk_kernel<16>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, pitch, flows, g, dists,
-                       inds);
+    hipLaunchKernelGGL(tile_topk_kernel<16>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
+                       g, dists, inds);
   else if (g.k <= 32)
-    hipLaunchKernelGGL(tile_topk_kernel<32>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, pitch, flows, g, dists,
-                       inds);
+    hipLaunchKernelGGL(tile_topk_kernel<32>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
+                       g, dists, inds);
   else if (g.k <= 64)
-    hipLaunchKernelGGL(tile_topk_kernel<64>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, pitch, flows, g, dists,
-                       inds);
+    hipLaunchKernelGGL(tile_topk_kernel<64>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
+                       g, dists, inds);
   else
-    hipLaunchKernelGGL(tile_topk_kernel<128>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, pitch, flows, g, dists,
-                       inds);
+    hipLaunchKernelGGL(tile_topk_kernel<128>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
+                       g, dists, inds);
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
 }
 

@@ -38,8 +38,10 @@ snls_status check_topk_args(int64_t rows, int32_t n_cand, int32_t k, int32_t dis
 // channels-last copy of V, 256-byte aligned.
 size_t aggregate_ws_bytes(const Geo& g);
 
-// The tiled search path (inner product, S_Q = 1, S_K <= 1, P <= 7, Ws <= 9)
-// and its workspace: the score of every candidate (rows x candidates fp32).
+// The tiled search path (S_Q = 1, P <= 7, Ws <= 9; inner product with
+// S_K <= 1, squared L2 with S_K = 1) and its workspace: the inner-product
+// score of every candidate (rows x candidates fp32), plus for L2 the key-norm
+// term of every candidate and the query-norm term of every row.
 bool tile_supported(const Geo& g);
 size_t tile_ws_bytes(const Geo& g);
 
@@ -54,6 +56,8 @@ snls_status launch_search_topk_direct(const float* q, const float* k, const floa
                                       float* dists, float* inds, hipStream_t s);
 snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, float* scores, hipStream_t s);
+snls_status launch_l2_norms(const float* q, const float* k, const float* flows, const Geo& g, float* G, int pitch,
+                            float* Qn, hipStream_t s);
 snls_status launch_topk(const float* dall, const float* iall, int64_t rows, int ncand, int k, int dist,
                         float* dists, float* inds, hipStream_t s);
 snls_status launch_aggregate(const float* v, const float* dists, const float* inds, const Geo& g, float scale,

@@ -116,14 +116,19 @@ def test_aggregate_and_backward_validation(lib):
 
 
 def test_search_workspace(lib):
-    """The tiled top-k path (inner product, stride0 = 1, stride1 <= 1, ps <= 7,
-    ws <= 9) scores every candidate into the workspace; other paths need none."""
+    """The tiled top-k path (stride0 = 1, ps <= 7, ws <= 9; inner product with
+    stride1 <= 1, squared L2 with stride1 = 1) scores every candidate into the
+    workspace; other paths need none."""
     prm = _params()
     rows, ncand = 1 * 2 * 3 * 16 * 17, 3 * 3 * 3
     need = lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(prm))
     assert need == rows * ((ncand + 3) // 4 * 4) * 4  # rows padded to a multiple of 4 candidates
-    for kw in (dict(k=0), dict(dist_type=1), dict(stride0=2), dict(stride1=1.5), dict(ps=9), dict(ws=11, k=4)):
+    for kw in (dict(k=0), dict(dist_type=1, stride1=0.5), dict(stride0=2), dict(stride1=1.5), dict(ps=9),
+               dict(ws=11, k=4)):
         assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(**kw))) == 0, kw
+    # squared L2 (key stride 1): the scores, the key-norm terms and the query-norm terms
+    plane = (rows * 28 * 4 + 255) // 256 * 256
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(dist_type=1))) == 2 * plane + rows * 4
     assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, None, BIG, None) == B.SNLS_ERR_WORKSPACE
     assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, FAKE, need - 1,
                            None) == B.SNLS_ERR_WORKSPACE

@@ -262,6 +262,38 @@ def test_tiled_search_topk(dev, case):
     compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
 
 
+# Squared L2 through the tiled path (key stride 1): inner products from the
+# tiled kernel, key and query norm terms from their own kernel; border queries
+# (clipped patches), wide unions (norms read straight from memory) and every
+# patch size.
+L2_TILE_CASES = [
+    (small_params(T=3, C=8, H=23, W=31, ws=9, wt=1, ps=7, k=10, dist_type=1), "frac"),
+    (small_params(T=5, C=32, H=37, W=53, ws=9, wt=2, ps=7, k=10, dist_type=1), "smooth"),
+    (small_params(T=2, C=5, H=17, W=19, ws=5, wt=1, ps=3, k=7, dist_type=1), "int"),
+    (small_params(T=3, C=12, HD=2, H=20, W=41, ws=7, wt=1, ps=5, k=16, dist_type=1), "wide"),
+    (small_params(T=2, C=4, H=13, W=16, ws=3, wt=1, ps=1, k=4, dist_type=1), "far"),
+    (small_params(T=4, C=9, H=9, W=8, ws=8, wt=2, ps=6, k=13, dist_type=1), "frac"),
+    (small_params(B=2, T=1, C=16, H=21, W=22, ws=9, wt=0, ps=4, k=12, dist_type=1), "frac"),
+    (small_params(T=3, C=70, H=19, W=26, ws=9, wt=1, ps=2, k=10, dist_type=1), "smooth"),
+]
+
+
+@pytest.mark.parametrize("case", range(len(L2_TILE_CASES)),
+                         ids=["l%d-ws%d-ps%d-%s" % (i, p["ws"], p["ps"], kd) for i, (p, kd) in enumerate(L2_TILE_CASES)])
+def test_tiled_search_l2(dev, case):
+    p, kind = L2_TILE_CASES[case]
+    r = np.random.default_rng(8500 + case)
+    shp = (p["B"], p["T"], p["C"], p["H"], p["W"])
+    q = r.standard_normal(shp, dtype=np.float32)
+    k = (q + 0.3 * r.standard_normal(shp, dtype=np.float32)).astype(np.float32) if case % 2 else \
+        r.standard_normal(shp, dtype=np.float32)
+    flows = _tile_flows(p, kind, r)
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    torch.cuda.synchronize()
+    res = oracle.search(q, k, flows, p)
+    compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
+
+
 # --------------------------------------------------- non-finite inputs --
 
 @pytest.mark.parametrize("dist_type,ps,ws", [(0, 3, 5), (0, 7, 9), (1, 3, 5), (0, 4, 8)])
