@@ -25,8 +25,10 @@ snls_status device_ready() {
 
 size_t backward_ws_bytes(const Geo& g) { return (size_t)g.rows * (size_t)g.k * sizeof(float); }
 
-// Only the tiled top-k path needs scratch: the scores of every candidate.
-size_t search_ws_bytes(const Geo& g) { return g.k >= 1 && tile_supported(g) ? tile_ws_bytes(g) : 0; }
+// Only the scored top-k paths need scratch: the scores of every candidate.
+size_t search_ws_bytes(const Geo& g) {
+  return g.k >= 1 && (tile_supported(g) || p1_supported(g)) ? tile_ws_bytes(g) : 0;
+}
 
 }  // namespace
 

@@ -152,6 +152,7 @@ snls_status launch_search_topk_direct(const float* q, const float* k, const floa
 snls_status launch_search_topk(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, void* ws, hipStream_t s) {
   if (tile_supported(g)) return launch_search_tile(q, k, flows, g, dists, inds, static_cast<float*>(ws), s);
+  if (p1_supported(g)) return launch_search_p1(q, k, flows, g, dists, inds, static_cast<float*>(ws), s);
   return launch_search_topk_direct(q, k, flows, g, dists, inds, s);
 }
 

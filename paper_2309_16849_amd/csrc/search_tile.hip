@@ -542,9 +542,9 @@ __global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __rest
   const long long row = (long long)blockIdx.x * ROWS + tid;
   if (row >= g.rows) return;
   const int ncell = g.ws * g.ws;
-  // query of this row (query stride 1: nH = H, nW = W)
-  const int w = (int)(row % g.nW);
-  const int h = (int)((row / g.nW) % g.nH);
+  // query of this row
+  const int w = (int)(row % g.nW) * g.s0;
+  const int h = (int)((row / g.nW) % g.nH) * g.s0;
   const int t = (int)((row / ((long long)g.nW * g.nH)) % g.T);
   const int b = (int)(row / ((long long)g.nW * g.nH * g.T * g.HD));
   const float* srow = scores + row * pitch;
@@ -673,6 +673,36 @@ size_t tile_ws_bytes(const Geo& g) {
   return b;
 }
 
+// Top-k of the scored rows (any scores kernel of the tiled family).
+static snls_status launch_tile_topk(const float* scores, const float* gnorm, const float* qnorm, int pitch,
+                                    const float* flows, const Geo& g, float* dists, float* inds, hipStream_t s) {
+  const unsigned tblocks = (unsigned)((g.rows + tk::ROWS - 1) / tk::ROWS);
+  if (g.k <= 12)
+    hipLaunchKernelGGL(tile_topk_kernel<12>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
+                       g, dists, inds);
+  else if (g.k <= 16)
+    hipLaunchKernelGGL(tile_topk_kernel<16>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
+                       g, dists, inds);
+  else if (g.k <= 32)
+    hipLaunchKernelGGL(tile_topk_kernel<32>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
+                       g, dists, inds);
+  else if (g.k <= 64)
+    hipLaunchKernelGGL(tile_topk_kernel<64>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
+                       g, dists, inds);
+  else
+    hipLaunchKernelGGL(tile_topk_kernel<128>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
+                       g, dists, inds);
+  return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+}
+
+snls_status launch_search_p1(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
+                             float* inds, float* scores, hipStream_t s) {
+  const int pitch = tile_ws_pitch(g);
+  const snls_status st = launch_search_p1_scores(q, k, flows, g, scores, pitch, s);
+  if (st != SNLS_OK) return st;
+  return launch_tile_topk(scores, nullptr, nullptr, pitch, flows, g, dists, inds, s);
+}
+
 snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, float* scores, hipStream_t s) {
   const int tqh = tile::HROWS - g.ps + 1;
@@ -708,23 +738,7 @@ snls_status launch_search_tile(const float* q, const float* k, const float* flow
     const snls_status st = launch_l2_norms(q, k, flows, g, gnorm, pitch, qnorm, s);
     if (st != SNLS_OK) return st;
   }
-  const unsigned tblocks = (unsigned)((g.rows + tk::ROWS - 1) / tk::ROWS);
-  if (g.k <= 12)
-    hipLaunchKernelGGL(tile_topk_kernel<12>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
-                       g, dists, inds);
-  else if (g.k <= 16)
-    hipLaunchKernelGGL(tile_topk_kernel<16>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
-                       g, dists, inds);
-  else if (g.k <= 32)
-    hipLaunchKernelGGL(tile_topk_kernel<32>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
-                       g, dists, inds);
-  else if (g.k <= 64)
-    hipLaunchKernelGGL(tile_topk_kernel<64>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
-                       g, dists, inds);
-  else
-    hipLaunchKernelGGL(tile_topk_kernel<128>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,
-                       g, dists, inds);
-  return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+  return launch_tile_topk(scores, gnorm, qnorm, pitch, flows, g, dists, inds, s);
 }
 
 }  // namespace snls

@@ -44,6 +44,9 @@ size_t aggregate_ws_bytes(const Geo& g);
 // term of every candidate and the query-norm term of every row.
 bool tile_supported(const Geo& g);
 size_t tile_ws_bytes(const Geo& g);
+// Single-pixel patches (P = 1), any S_Q, S_K = 1, inner product, Ws <= 15:
+// same workspace layout (scores of every candidate).
+bool p1_supported(const Geo& g);
 
 #ifdef __HIPCC__
 
@@ -56,6 +59,10 @@ snls_status launch_search_topk_direct(const float* q, const float* k, const floa
                                       float* dists, float* inds, hipStream_t s);
 snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, float* scores, hipStream_t s);
+snls_status launch_search_p1(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
+                             float* inds, float* scores, hipStream_t s);
+snls_status launch_search_p1_scores(const float* q, const float* k, const float* flows, const Geo& g, float* scores,
+                                    int pitch, hipStream_t s);
 snls_status launch_l2_norms(const float* q, const float* k, const float* flows, const Geo& g, float* G, int pitch,
                             float* Qn, hipStream_t s);
 snls_status launch_topk(const float* dall, const float* iall, int64_t rows, int ncand, int k, int dist,

@@ -126,6 +126,11 @@ def test_search_workspace(lib):
     for kw in (dict(k=0), dict(dist_type=1, stride1=0.5), dict(stride0=2), dict(stride1=1.5), dict(ps=9),
                dict(ws=11, k=4)):
         assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(**kw))) == 0, kw
+    # single-pixel patches at query stride 2: the scores of every candidate
+    p1 = _params(ps=1, stride0=2, ws=15, k=30)
+    rows1 = 1 * 2 * 3 * 8 * 9
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(p1)) == rows1 * 676 * 4  # 675 padded to 676
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, stride0=2, ws=17, k=30))) == 0
     # squared L2 (key stride 1): the scores, the key-norm terms and the query-norm terms
     plane = (rows * 28 * 4 + 255) // 256 * 256
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(dist_type=1))) == 2 * plane + rows * 4

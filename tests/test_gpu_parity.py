@@ -294,6 +294,36 @@ def test_tiled_search_l2(dev, case):
     compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
 
 
+# Single-pixel patches at any query stride (the multi-head workload's path):
+# windows up to 15, k up to 30, several heads, ragged query grids.
+P1_CASES = [
+    (small_params(T=4, C=64, HD=4, H=40, W=37, ws=15, wt=1, ps=1, stride0=2, k=30), "smooth"),
+    (small_params(T=3, C=8, HD=2, H=31, W=26, ws=15, wt=1, ps=1, stride0=3, k=20), "frac"),
+    (small_params(B=2, T=2, C=5, H=19, W=23, ws=9, wt=1, ps=1, stride0=2, k=12), "int"),
+    (small_params(T=3, C=16, HD=1, H=22, W=30, ws=7, wt=1, ps=1, stride0=2, k=9), "wide"),
+    (small_params(T=2, C=4, H=17, W=18, ws=5, wt=1, ps=1, stride0=2, k=6), "far"),
+    (small_params(T=5, C=33, HD=1, H=25, W=21, ws=14, wt=2, ps=1, stride0=4, k=17), "frac"),
+]
+
+
+@pytest.mark.parametrize("case", range(len(P1_CASES)),
+                         ids=["p%d-ws%d-s%d-%s" % (i, p["ws"], p["stride0"], kd) for i, (p, kd) in enumerate(P1_CASES)])
+def test_p1_search(dev, case):
+    p, kind = P1_CASES[case]
+    r = np.random.default_rng(8700 + case)
+    shp = (p["B"], p["T"], p["C"], p["H"], p["W"])
+    q = r.standard_normal(shp, dtype=np.float32)
+    k = r.standard_normal(shp, dtype=np.float32)
+    flows = _tile_flows(p, kind, r)
+    v = r.standard_normal(shp, dtype=np.float32)
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    out = B.snls_aggregate(_d(v, dev), gd, gi, p, 0.5)
+    torch.cuda.synchronize()
+    res = oracle.search(q, k, flows, p)
+    compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
+    assert_close(_h(out), oracle.aggregate(v, _h(gd), _h(gi), p, 0.5), "aggregate (P = 1)")
+
+
 # --------------------------------------------------- non-finite inputs --
 
 @pytest.mark.parametrize("dist_type,ps,ws", [(0, 3, 5), (0, 7, 9), (1, 3, 5), (0, 4, 8)])
