@@ -21,6 +21,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 WORKLOAD = 2
 PEAK_FP32_VALU = 157.3e12  # MI355X fp32 vector peak (packed FMA), FLOP/s
+PEAK_FP32_VALU_UNPACKED = 78.6e12  # 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz, unpacked FMA
 PEAK_HBM = 8.0e12          # MI355X HBM3E, B/s
 
 
@@ -56,9 +57,10 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
-    """HBM bytes per search launch from the committed rocprofv3 counter
-    summary, or None when missing or taken on different kernel sources."""
+def measured_counters():
+    """Counter record of one snls_search call (HBM bytes, fp32 FMA
+    instructions) from the committed rocprofv3 summary, or None when missing
+    or taken on different kernel sources."""
     path = os.path.join(ROOT, "profiles", "search_denoise480x854_traffic.json")
     if not os.path.exists(path):
         return None
@@ -66,11 +68,12 @@ def measured_traffic():
         rec = json.load(f)
     if rec.get("kernel_source_hash") != kernel_source_hash():
         return None
-    return rec.get("bytes_per_launch")
+    return rec
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "search_denoise480x854_traffic.json")
-SEARCH_KERNEL = "search_tile_kernel"
+# the two kernels of one snls_search call on this workload: scores, then top-k
+SEARCH_KERNELS = ("search_tile_scores_kernel", "tile_topk_kernel")
 COPY_KERNEL_HINT = "mulfunctor"  # torch.mul(src, 1, out=dst): one read and one write per element
 
 
@@ -123,26 +126,31 @@ def summarize_profiles(outdir, copy_mib):
     for kn in sorted(counters):
         for cn in sorted(counters[kn]):
             lines.append("| %s | %s | %.6g |" % (kn.split("(")[0].replace("void ", "")[:60], cn, counters[kn][cn]))
-    search = [kn for kn in counters if SEARCH_KERNEL in kn]
+    search = [kn for kn in counters if any(sk in kn for sk in SEARCH_KERNELS)]
     copy = [kn for kn in counters if COPY_KERNEL_HINT in kn.lower() and "FETCH_SIZE" in counters[kn]]
     rec = None
-    if search and copy:
-        s, cpy = counters[search[0]], counters[copy[0]]
+    if search and copy and all("FETCH_SIZE" in counters[kn] and "WRITE_SIZE" in counters[kn] for kn in search):
+        cpy = counters[copy[0]]
         exp_kib = copy_mib * 1024.0
         f_fetch = exp_kib / cpy["FETCH_SIZE"]
         f_write = exp_kib / cpy["WRITE_SIZE"]
-        fetch_b = s["FETCH_SIZE"] * f_fetch * 1024.0
-        write_b = s["WRITE_SIZE"] * f_write * 1024.0
-        rec = {"kernel": search[0], "kernel_source_hash": kernel_source_hash(), "copy_kernel": copy[0],
+        fetch_kib = sum(counters[kn]["FETCH_SIZE"] for kn in search)
+        write_kib = sum(counters[kn]["WRITE_SIZE"] for kn in search)
+        fetch_b = fetch_kib * f_fetch * 1024.0
+        write_b = write_kib * f_write * 1024.0
+        fma = sum(counters[kn].get("SQ_INSTS_VALU_FMA_F32", 0.0) for kn in search)
+        rec = {"kernels": search, "kernel_source_hash": kernel_source_hash(), "copy_kernel": copy[0],
                "copy_mib": copy_mib, "copy_fetch_kib": cpy["FETCH_SIZE"], "copy_write_kib": cpy["WRITE_SIZE"],
-               "fetch_scale": f_fetch, "write_scale": f_write, "search_fetch_kib": s["FETCH_SIZE"],
-               "search_write_kib": s["WRITE_SIZE"], "fetch_bytes_per_launch": fetch_b,
-               "write_bytes_per_launch": write_b, "bytes_per_launch": fetch_b + write_b}
+               "fetch_scale": f_fetch, "write_scale": f_write, "search_fetch_kib": fetch_kib,
+               "search_write_kib": write_kib, "fetch_bytes_per_launch": fetch_b,
+               "write_bytes_per_launch": write_b, "bytes_per_launch": fetch_b + write_b,
+               "fma_f32_wave_insts_per_launch": fma}
         with open(TRAFFIC_FILE, "w") as f:
             json.dump(rec, f, indent=1)
-        lines += ["", "HBM traffic of one search launch: FETCH %.1f MB + WRITE %.1f MB = %.1f MB "
+        lines += ["", "HBM traffic of one snls_search call (%s): FETCH %.1f MB + WRITE %.1f MB = %.1f MB "
                   "(counter KiB x %.3f / %.3f, from a %d MiB copy)." % (
-                      fetch_b / 1e6, write_b / 1e6, (fetch_b + write_b) / 1e6, f_fetch, f_write, copy_mib)]
+                      " + ".join(k.split("(")[0].replace("void ", "") for k in search), fetch_b / 1e6,
+                      write_b / 1e6, (fetch_b + write_b) / 1e6, f_fetch, f_write, copy_mib)]
     md = os.path.join(ROOT, "profiles", "search_denoise480x854_rocprofv3.md")
     with open(md, "w") as f:
         f.write("\n".join(lines) + "\n")
@@ -268,7 +276,17 @@ def main():
     ms = elapsed / args.steps * 1e3
     value = w["queries"] * args.steps / elapsed
     achieved = w["f_search"] / t_search
-    traffic = measured_traffic()
+    rec = measured_counters()
+    traffic = rec["bytes_per_launch"] if rec else None
+    # fp32 multiply-adds the search kernels issue (rocprofv3 counter, 64 lanes
+    # per wave instruction), against the unpacked fp32 VALU peak this build
+    # can reach (packed fp32 instructions are disabled)
+    issued = None
+    if rec and rec.get("fma_f32_wave_insts_per_launch"):
+        fl = rec["fma_f32_wave_insts_per_launch"] * 64 * 2
+        issued = {"fma_flop_per_launch": fl, "tflops": fl / t_search / 1e12,
+                  "peak_unpacked": PEAK_FP32_VALU_UNPACKED / 1e12,
+                  "frac_unpacked": fl / t_search / PEAK_FP32_VALU_UNPACKED}
     line = {
         "metric": "queries/s (search+top-k+aggregate) and % fp32 VALU/HBM roofline, config 2",
         "value": value, "unit": "queries/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -278,9 +296,9 @@ def main():
                    "HD": p["HD"], "ws": p["ws"], "wt": p["wt"], "ps": p["ps"], "stride0": p["stride0"],
                    "stride1": p["stride1"], "k": p["k"], "dist": "inner_product", "softmax_scale": scale,
                    "parallelism": "single_gpu"},
-        "roofline": {"bound": "alu", "kernel": "snls_search (fused search+top-k)", "achieved": achieved / 1e12,
+        "roofline": {"bound": "alu", "kernel": "snls_search (scores + top-k kernels)", "achieved": achieved / 1e12,
                      "peak": PEAK_FP32_VALU / 1e12, "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_VALU,
-                     "traffic": traffic},
+                     "traffic": traffic, "issued": issued},
         "candidates_per_s": w["candidates"] * args.steps / elapsed,
         "step_alg_tflops": (w["f_search"] + w["f_agg"]) / (elapsed / args.steps) / 1e12,
         "step_frac_fp32_valu": (w["f_search"] + w["f_agg"]) / (elapsed / args.steps) / PEAK_FP32_VALU,
