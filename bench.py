@@ -19,7 +19,6 @@ import time
 import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-WORKLOAD = 2
 PEAK_FP32_VALU = 157.3e12  # MI355X fp32 vector peak (packed FMA), FLOP/s
 PEAK_FP32_VALU_UNPACKED = 78.6e12  # 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz, unpacked FMA
 PEAK_HBM = 8.0e12          # MI355X HBM3E, B/s
@@ -207,6 +206,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default="denoise480x854",
+                    help="workload name (default: the 480x854 denoising workload; paper320_s1, paper320_s2 and "
+                         "paper152_mem are the paper's own benchmark shapes)")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run one plain device copy of this size (calibrates the HBM byte counters)")
@@ -226,11 +228,11 @@ def main():
     import torch
     sys.path.insert(0, ROOT)
     from paper_2309_16849_amd import snls as B
-    from workloads import make_config
+    from workloads import config_index, make_config
 
     B.load_library()
     dev = torch.device("cuda:0")
-    c = make_config(WORKLOAD)
+    c = make_config(config_index(args.workload))
     p, scale = c["params"], c["scale"]
     x = torch.from_numpy(c["q"]).to(dev)
     fl = torch.from_numpy(c["flows"]).to(dev)
@@ -259,6 +261,11 @@ def main():
         torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
         del src, dst
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats(dev)
+    step()
+    torch.cuda.synchronize()
+    peak_mem = torch.cuda.max_memory_allocated(dev)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -294,7 +301,7 @@ def main():
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": c["name"], "B": p["B"], "T": p["T"], "C": p["C"], "H": p["H"], "W": p["W"],
                    "HD": p["HD"], "ws": p["ws"], "wt": p["wt"], "ps": p["ps"], "stride0": p["stride0"],
-                   "stride1": p["stride1"], "k": p["k"], "dist": "inner_product", "softmax_scale": scale,
+                   "stride1": p["stride1"], "k": p["k"], "dist": "inner_product" if p["dist_type"] == 0 else "squared_l2", "softmax_scale": scale,
                    "parallelism": "single_gpu"},
         "roofline": {"bound": "alu", "kernel": "snls_search (scores + top-k kernels)", "achieved": achieved / 1e12,
                      "peak": PEAK_FP32_VALU / 1e12, "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_VALU,
@@ -304,9 +311,10 @@ def main():
         "step_frac_fp32_valu": (w["f_search"] + w["f_agg"]) / (elapsed / args.steps) / PEAK_FP32_VALU,
         "step_frac_hbm": w["bytes_total"] / (elapsed / args.steps) / PEAK_HBM,
         "search_ms": t_search * 1e3, "aggregate_ms": t_agg * 1e3,
+        "peak_mem_gb": peak_mem / 1e9, "search_workspace_gb": sws.numel() * 4 / 1e9,
         "aggregate_alg_tflops": w["f_agg"] / t_agg / 1e12,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.workload == "denoise480x854":
         line["cpu_baseline"] = cpu_baseline(c, args.cpu_budget)
     print(json.dumps(line), flush=True)
 

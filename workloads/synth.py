@@ -40,7 +40,30 @@ CONFIGS = [
          k=30, dist_type=0, scale=1.0, video="motion", amp=8.0, backward=False),
     dict(name="train256", B=1, T=5, C=64, H=256, W=256, HD=1, ws=9, wt=2, ps=3, stride0=1, stride1=1.0, k=10,
          dist_type=0, scale=1.0, video="motion", amp=8.0, backward=True),
+    # The paper's own benchmark shapes (Sec. 4.4): runtime on 5 frames of
+    # 320 x 320 with 32 features, ws = 9, ps = 1, query stride 1 or 2; peak
+    # memory on 5 frames of 152 x 152 with 192 features, ps = 7, ws = 3.  The
+    # temporal window and k are not stated there: the whole clip (wt = 2) and
+    # k = 10 are used.
+    dict(name="paper320_s1", B=1, T=5, C=32, H=320, W=320, HD=1, ws=9, wt=2, ps=1, stride0=1, stride1=1.0, k=10,
+         dist_type=0, scale=1.0, video="motion", amp=8.0, backward=False),
+    dict(name="paper320_s2", B=1, T=5, C=32, H=320, W=320, HD=1, ws=9, wt=2, ps=1, stride0=2, stride1=1.0, k=10,
+         dist_type=0, scale=1.0, video="motion", amp=8.0, backward=False),
+    dict(name="paper152_mem", B=1, T=5, C=192, H=152, W=152, HD=1, ws=3, wt=2, ps=7, stride0=1, stride1=1.0,
+         k=10, dist_type=0, scale=1.0, video="motion", amp=8.0, backward=False),
 ]
+
+# The five workloads every parity test covers; the paper's benchmark shapes
+# follow them.
+N_MAIN_CONFIGS = 5
+
+
+def config_index(name: str) -> int:
+    """Index of the workload called name."""
+    for i, c in enumerate(CONFIGS):
+        if c["name"] == name:
+            return i
+    raise KeyError(name)
 
 PARAM_KEYS = ("B", "T", "C", "H", "W", "HD", "ws", "wt", "ps", "stride0", "stride1", "k", "dist_type")
 
