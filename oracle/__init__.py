@@ -58,8 +58,12 @@ def _load():
         lib.oracle_search_fixed.argtypes = [P, P, P, P, P, P, P]
         lib.oracle_backward.argtypes = [P] * 9 + [ctypes.c_double, P, P, P, P]
         lib.oracle_bilinear_image.argtypes = [P, ctypes.c_int, ctypes.c_int, P, P, i64, P]
+        ci = ctypes.c_int
+        lib.oracle_chain_flows.argtypes = [P, P, ci, ci, ci, ci, ci, P]
+        lib.oracle_aggregate_stacked.argtypes = [P, P, P, P, ctypes.c_double, P]
         for f in ("oracle_search", "oracle_topk", "oracle_aggregate", "oracle_aggregate_at",
-                  "oracle_search_fixed", "oracle_backward", "oracle_bilinear_image"):
+                  "oracle_search_fixed", "oracle_backward", "oracle_bilinear_image", "oracle_chain_flows",
+                  "oracle_aggregate_stacked"):
             getattr(lib, f).restype = None
         _lib = lib
     return _lib
@@ -198,4 +202,24 @@ def bilinear_image(img, ys, xs):
     y, x = _f64(ys).ravel(), _f64(xs).ravel()
     out = np.empty(len(y), np.float64)
     lib.oracle_bilinear_image(_ptr(im), im.shape[0], im.shape[1], _ptr(y), _ptr(x), len(y), _ptr(out))
+    return out
+
+
+def chain_flows(fflow, bflow, wt: int):
+    """Offsets to frames t-wt..t+wt composed from one-step flows (B,T,2,H,W); returns (B,T,2wt,2,H,W)."""
+    lib = _load()
+    ff, bf = _f64(fflow), _f64(bflow)
+    B, T, _, H, W = ff.shape
+    out = np.empty((B, T, 2 * wt, 2, H, W), np.float64)
+    lib.oracle_chain_flows(_ptr(ff), _ptr(bf), B, T, H, W, int(wt), _ptr(out))
+    return out
+
+
+def aggregate_stacked(v, dists, inds, p: dict, scale: float = 1.0):
+    """The aggregation with the k neighbours kept apart: (B, HD, k, T, C/HD, H, W), float64."""
+    lib = _load()
+    vv, dd, ii = _f64(v), _f64(dists), _f64(inds)
+    out = np.empty((p["B"], p["HD"], p["k"], p["T"], p["C"] // p["HD"], p["H"], p["W"]), np.float64)
+    prm = _params(p)
+    lib.oracle_aggregate_stacked(_ptr(vv), _ptr(dd), _ptr(ii), ctypes.byref(prm), float(scale), _ptr(out))
     return out

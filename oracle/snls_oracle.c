@@ -517,3 +517,111 @@ void oracle_bilinear_image(const double* img, int H, int W, const double* ys, co
   p.B = 1; p.T = 1; p.C = 1; p.H = H; p.W = W; p.HD = 1;
   for (int64_t i = 0; i < n; i++) out[i] = bilinear(img, &p, 0, 0, 0, ys[i], xs[i]);
 }
+
+/* ---- front-end of the paper's example interface (Appendix "Pytorch
+ * Example"): the search there takes one forward flow (t -> t+1) and one
+ * backward flow (t -> t-1) per frame while its window spans wt > 1 frames
+ * each way.  How the one-step flows are combined is not described; the
+ * reading taken here composes them along the motion path:
+ *   F_{+1}(x) = f_t(x),  F_{+s}(x) = F_{+(s-1)}(x) + f_{t+s-1}(x + F_{+(s-1)}(x)),
+ * and mirrored with the backward flows for negative steps.  A one-step flow
+ * is read bilinearly at a fractional position clamped into the frame (the
+ * field continues at its border).  Steps whose frame lies outside the clip
+ * are left at 0 (such frames are never searched).
+ * fflow, bflow: (B, T, 2, H, W); flows: (B, T, 2*wt, 2, H, W), slot order as
+ * in the search (dt = -wt..-1, +1..+wt), component 0 = row offset. */
+static double clamped_bilinear(const double* f, int H, int W, double y, double x) {
+  double yc = y < 0.0 ? 0.0 : (y > H - 1 ? (double)(H - 1) : y);
+  double xc = x < 0.0 ? 0.0 : (x > W - 1 ? (double)(W - 1) : x);
+  int y0 = (int)floor(yc), x0 = (int)floor(xc);
+  double ay = yc - y0, ax = xc - x0;
+  int y1 = y0 + 1 < H ? y0 + 1 : H - 1, x1 = x0 + 1 < W ? x0 + 1 : W - 1;
+  return (1.0 - ay) * ((1.0 - ax) * f[(int64_t)y0 * W + x0] + ax * f[(int64_t)y0 * W + x1]) +
+         ay * ((1.0 - ax) * f[(int64_t)y1 * W + x0] + ax * f[(int64_t)y1 * W + x1]);
+}
+
+void oracle_chain_flows(const double* fflow, const double* bflow, int B, int T, int H, int W, int wt,
+                        double* flows) {
+  int64_t HW = (int64_t)H * W;
+  memset(flows, 0, sizeof(double) * (size_t)B * T * 2 * wt * 2 * HW);
+  for (int b = 0; b < B; b++)
+    for (int t = 0; t < T; t++)
+      for (int dir = -1; dir <= 1; dir += 2) {
+        const double* one = dir > 0 ? fflow : bflow;
+        for (int y = 0; y < H; y++)
+          for (int x = 0; x < W; x++) {
+            double fh = 0.0, fw = 0.0;
+            for (int s = 1; s <= wt; s++) {
+              int t1 = t + dir * (s - 1), t2 = t + dir * s;
+              if (t2 < 0 || t2 >= T) break;
+              const double* fh1 = one + (((int64_t)b * T + t1) * 2 + 0) * HW;
+              const double* fw1 = one + (((int64_t)b * T + t1) * 2 + 1) * HW;
+              double py = y + fh, px = x + fw;
+              double dh = clamped_bilinear(fh1, H, W, py, px), dw = clamped_bilinear(fw1, H, W, py, px);
+              fh += dh;
+              fw += dw;
+              int slot = dir < 0 ? -s + wt : s + wt - 1;
+              flows[((((int64_t)b * T + t) * 2 * wt + slot) * 2 + 0) * HW + (int64_t)y * W + x] = fh;
+              flows[((((int64_t)b * T + t) * 2 * wt + slot) * 2 + 1) * HW + (int64_t)y * W + x] = fw;
+            }
+          }
+      }
+}
+
+/* The aggregation that keeps the k neighbours apart (Sec. 3.2 aggregation;
+ * the example's NonLocalGather returns (B,HD,K,T,F',H,W) and reduces over K
+ * afterwards): stacked[b,hd,l,t,c,y,x] = (1/count(y,x)) * sum over the query
+ * patches covering (y,x) of w_l * v~_l, with the softmax weights, bilinear
+ * reads and count of oracle_aggregate.  Summed over l it is that
+ * aggregation. */
+void oracle_aggregate_stacked(const double* v, const double* dists, const double* inds, const oracle_params* p,
+                              double scale, double* stacked) {
+  int nH = grid_h(p), nW = grid_w(p), Ch = p->C / p->HD, lo = patch_lo(p), kk = p->k;
+  int64_t HW = (int64_t)p->H * p->W;
+  int64_t nst = (int64_t)p->B * p->HD * kk * p->T * Ch * HW;
+  double* cnt = (double*)calloc((size_t)p->B * p->T * HW, sizeof(double));
+  double* wts = (double*)malloc(sizeof(double) * (size_t)kk);
+  memset(stacked, 0, sizeof(double) * (size_t)nst);
+  for (int b = 0; b < p->B; b++)
+    for (int t = 0; t < p->T; t++)
+      for (int mh = 0; mh < nH; mh++)
+        for (int mw = 0; mw < nW; mw++) {
+          int h = mh * p->stride0, w = mw * p->stride0;
+          for (int ph = lo; ph < lo + p->ps; ph++)
+            for (int pw = lo; pw < lo + p->ps; pw++) {
+              int y = h + ph, x = w + pw;
+              if (y < 0 || y >= p->H || x < 0 || x >= p->W) continue;
+              cnt[((int64_t)b * p->T + t) * HW + (int64_t)y * p->W + x] += 1.0;
+            }
+          for (int hd = 0; hd < p->HD; hd++) {
+            int64_t row = ((((int64_t)b * p->HD + hd) * p->T + t) * nH + mh) * nW + mw;
+            softmax_row(dists + row * kk, kk, p->dist_type, scale, wts);
+            for (int l = 0; l < kk; l++) {
+              if (wts[l] == 0.0) continue;
+              const double* ind = inds + 3 * (row * kk + l);
+              int tk = neighbour_frame(p, ind[0]);
+              if (tk < 0) continue;
+              for (int ph = lo; ph < lo + p->ps; ph++)
+                for (int pw = lo; pw < lo + p->ps; pw++) {
+                  int y = h + ph, x = w + pw;
+                  if (y < 0 || y >= p->H || x < 0 || x >= p->W) continue;
+                  for (int c = 0; c < Ch; c++) {
+                    int64_t o = (((((int64_t)b * p->HD + hd) * kk + l) * p->T + t) * Ch + c) * HW +
+                                (int64_t)y * p->W + x;
+                    stacked[o] += wts[l] * bilinear(v, p, b, tk, hd * Ch + c, (double)y + ind[1], (double)x + ind[2]);
+                  }
+                }
+            }
+          }
+        }
+  for (int64_t o = 0; o < nst; o++) {
+    int64_t pix = o % HW;
+    int64_t r = o / HW / Ch;
+    int t = (int)(r % p->T);
+    int b = (int)(r / p->T / kk / p->HD);
+    double n = cnt[((int64_t)b * p->T + t) * HW + pix];
+    stacked[o] = n > 0.0 ? stacked[o] / n : 0.0;
+  }
+  free(wts);
+  free(cnt);
+}

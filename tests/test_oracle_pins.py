@@ -558,3 +558,127 @@ def test_nan_similarity_scores_as_invalid():
         assert changed.any()
         assert np.all(d1[changed] == (-np.inf if dist == 0 else np.inf))
         assert np.all(np.isfinite(d0[changed]))
+
+
+# ------------------------------------------- flow chaining (front-end) --
+
+def _one_step_flows(r, B, T, H, W, kind):
+    shp = (B, T, 2, H, W)
+    if kind == "int":
+        return r.integers(-2, 3, shp).astype(np.float64), r.integers(-2, 3, shp).astype(np.float64)
+    return r.uniform(-3, 3, shp), r.uniform(-3, 3, shp)
+
+
+def test_chain_flows_one_step_is_the_input(oracle_lib):
+    """wt = 1: the +-1 slots are the forward and backward flows themselves;
+    steps whose frame is outside the clip stay 0."""
+    r = _rng(40)
+    ff, bf = _one_step_flows(r, 2, 4, 7, 9, "frac")
+    out = oracle.chain_flows(ff, bf, 1)
+    np.testing.assert_array_equal(out[:, 1:, 0], bf[:, 1:])
+    np.testing.assert_array_equal(out[:, :-1, 1], ff[:, :-1])
+    assert not out[:, 0, 0].any() and not out[:, -1, 1].any()
+
+
+def test_chain_flows_constant_motion_adds_up(oracle_lib):
+    """A uniform translation composes to s times the one-step offset."""
+    B, T, H, W, wt = 1, 6, 8, 10, 3
+    ff = np.broadcast_to(np.array([0.75, -1.25]).reshape(1, 1, 2, 1, 1), (B, T, 2, H, W)).copy()
+    bf = -ff
+    out = oracle.chain_flows(ff, bf, wt)
+    for t in range(T):
+        for s in range(1, wt + 1):
+            for sign, slot in ((1, wt + s - 1), (-1, wt - s)):
+                if 0 <= t + sign * s < T:
+                    np.testing.assert_array_equal(out[0, t, slot, 0], np.full((H, W), sign * s * 0.75))
+                    np.testing.assert_array_equal(out[0, t, slot, 1], np.full((H, W), -sign * s * 1.25))
+                else:
+                    assert not out[0, t, slot].any()
+
+
+def test_chain_flows_integer_composition_is_a_gather(oracle_lib):
+    """Integer one-step flows: F_{+2}(x) = f_t(x) + f_{t+1}(x + f_t(x)), read
+    by integer indexing (positions clamped into the frame)."""
+    r = _rng(41)
+    B, T, H, W = 1, 5, 9, 11
+    ff, bf = _one_step_flows(r, B, T, H, W, "int")
+    out = oracle.chain_flows(ff, bf, 2)
+    yy, xx = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    for t in range(T - 2):
+        f1 = ff[0, t]
+        py = np.clip(yy + f1[0], 0, H - 1).astype(int)
+        px = np.clip(xx + f1[1], 0, W - 1).astype(int)
+        ref = f1 + ff[0, t + 1][:, py, px]
+        np.testing.assert_array_equal(out[0, t, 3], ref)
+    for t in range(2, T):
+        b1 = bf[0, t]
+        py = np.clip(yy + b1[0], 0, H - 1).astype(int)
+        px = np.clip(xx + b1[1], 0, W - 1).astype(int)
+        ref = b1 + bf[0, t - 1][:, py, px]
+        np.testing.assert_array_equal(out[0, t, 0], ref)
+
+
+def test_chain_flows_fractional_composition_matches_grid_sample(oracle_lib):
+    """Fractional flows: the second step is a bilinear read of the next flow
+    field at the displaced position, clamped into the frame -- torch
+    grid_sample with align_corners=True and border padding (fp64)."""
+    r = _rng(42)
+    B, T, H, W = 1, 4, 8, 13
+    ff, bf = _one_step_flows(r, B, T, H, W, "frac")
+    out = oracle.chain_flows(ff, bf, 3)
+    yy, xx = np.meshgrid(np.arange(H, dtype=np.float64), np.arange(W, dtype=np.float64), indexing="ij")
+
+    def sample(field, py, px):  # field (2, H, W) at positions (H, W)
+        gx = 2 * px / (W - 1) - 1
+        gy = 2 * py / (H - 1) - 1
+        grid = torch.from_numpy(np.stack([gx, gy], -1)[None])
+        return F.grid_sample(torch.from_numpy(field[None]), grid, mode="bilinear", padding_mode="border",
+                             align_corners=True)[0].numpy()
+
+    acc = ff[0, 0].copy()
+    np.testing.assert_array_equal(out[0, 0, 3], acc)
+    for s in (2, 3):
+        acc = acc + sample(ff[0, s - 1], yy + acc[0], xx + acc[1])
+        np.testing.assert_allclose(out[0, 0, 3 + s - 1], acc, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------- aggregation, neighbours apart --
+
+@pytest.mark.parametrize("ps,stride0,HD", [(1, 1, 2), (3, 1, 1), (3, 2, 1)])
+def test_stacked_aggregation_keeps_neighbours_apart(oracle_lib, ps, stride0, HD):
+    """Integer offsets: slice l of the stacked aggregation is the fold of the
+    queries' w_l-weighted l-th neighbour patches divided by the cover count
+    (torch fold), per head."""
+    r = _rng(43 + ps + stride0)
+    Ch, H, W, T, kk = 2, 9, 8, 3, 4
+    C = Ch * HD
+    p = small_params(T=T, C=C, HD=HD, H=H, W=W, ps=ps, stride0=stride0, k=kk)
+    nH, nW = oracle.grid(p)
+    v = r.standard_normal((1, T, C, H, W))
+    dists = r.standard_normal((1, HD, T, nH, nW, kk))
+    inds = np.zeros((1, HD, T, nH, nW, kk, 3))
+    inds[..., 0] = r.integers(0, T, size=inds.shape[:-1])
+    inds[..., 1:] = r.integers(-2, 3, size=inds.shape[:-1] + (2,))
+    scale = 0.8
+    st = oracle.aggregate_stacked(v, dists, inds, p, scale)
+    assert st.shape == (1, HD, kk, T, Ch, H, W)
+    wts = np.exp(scale * dists - (scale * dists).max(-1, keepdims=True))
+    wts /= wts.sum(-1, keepdims=True)
+    m = ps + 4
+    pad = np.pad(v[0], ((0, 0), (0, 0), (m, m), (m, m)))
+    ones = F.fold(torch.ones(1, ps * ps, nH * nW, dtype=torch.float64), (H, W), ps, padding=ps // 2,
+                  stride=stride0)[0, 0]
+    for hd in range(HD):
+        for l in range(kk):
+            for t in range(T):
+                cols = np.zeros((Ch * ps * ps, nH * nW))
+                for mh in range(nH):
+                    for mw in range(nW):
+                        t2, dh, dw = inds[0, hd, t, mh, mw, l].astype(int)
+                        y0 = mh * stride0 + dh + m - ps // 2
+                        x0 = mw * stride0 + dw + m - ps // 2
+                        patch = pad[t2, hd * Ch:(hd + 1) * Ch, y0:y0 + ps, x0:x0 + ps].reshape(-1)
+                        cols[:, mh * nW + mw] = wts[0, hd, t, mh, mw, l] * patch
+                folded = F.fold(torch.from_numpy(cols)[None], (H, W), ps, padding=ps // 2, stride=stride0)[0]
+                ref = torch.where(ones > 0, folded / ones.clamp(min=1), torch.zeros_like(folded)).numpy()
+                np.testing.assert_allclose(st[0, hd, l, t], ref, rtol=0, atol=1e-12)
