@@ -12,7 +12,9 @@
  *   snls_aggregate  Sec. 3.2 "Aggregation", softmax-weighted sum of the
  *                   selected patches, normalised per pixel;
  *   snls_backward   Sec. 1 / 3.2, gradients of the differentiable search and
- *                   aggregation.
+ *                   aggregation;
+ *   snls_aggregate_stacked, snls_chain_flows  the code example's neighbour-
+ *                   stacked gather and its forward/backward flow interface.
  *
  * Conventions shared by every call
  * --------------------------------
@@ -172,9 +174,46 @@ snls_status snls_backward(const float* q, const float* k, const float* v, const 
                           float scale, float* grad_q, float* grad_k, float* grad_v, float* grad_flows,
                           void* workspace, size_t workspace_bytes, void* stream);
 
+/* snls_aggregate_stacked -- the aggregation with the k neighbours kept apart
+ * (Sec. 3.2 "Aggregation" as the paper's code example uses it: its gather
+ * returns (B, HD, K, T, F', H, W) and a convolution reduces over K
+ * afterwards).  Slice l holds, for each output pixel, the sum over the query
+ * patches covering it of w_l * v~(frame_l, ...) (the weights, reads and
+ * validity rules of snls_aggregate), divided by the number of covering
+ * patches; summed over l it is snls_aggregate's output.
+ *   v, dists, inds, p, scale  as in snls_aggregate
+ *   stacked    device out, (B, HD, k, T, C/HD, H, W), fully overwritten
+ *   workspace  device scratch of at least
+ *              snls_workspace_size(SNLS_OP_AGGREGATE_STACKED, p) bytes,
+ *              256-byte aligned (softmax weights)
+ * Errors: as snls_aggregate; SNLS_ERR_UNSUPPORTED for outputs beyond 2^40
+ * elements. */
+snls_status snls_aggregate_stacked(const float* v, const float* dists, const float* inds, const snls_params* p,
+                                   float scale, float* stacked, void* workspace, size_t workspace_bytes,
+                                   void* stream);
+
+/* snls_chain_flows -- window offsets from one-step flows, the front-end of
+ * the paper's code example, whose search takes a forward flow (t -> t+1) and
+ * a backward flow (t -> t-1) per frame while its window spans wt frames each
+ * way.  The offset to frame t+s (s = 1..wt) is composed along the motion
+ * path: F_1(x) = fflow_t(x), F_s(x) = F_{s-1}(x) + fflow_{t+s-1}(x + F_{s-1}(x)),
+ * with each one-step flow read bilinearly at the position clamped into the
+ * frame; the backward direction mirrors it with bflow.  Offsets to frames
+ * outside the clip are 0 (never searched).
+ *   fflow, bflow  device, (B, T, 2, H, W); component 0 = row offset
+ *   flows         device out, (B, T, 2*wt, 2, H, W) in the slot order of
+ *                 snls_search, fully overwritten; nothing is touched when
+ *                 wt == 0 (NULL pointers are then allowed)
+ * Errors: SNLS_ERR_INVALID_ARG for sizes < 1, wt < 0 or NULL buffers;
+ * SNLS_ERR_UNSUPPORTED for H*W > 2^30, wt > 63 or more than 2^40 output
+ * pixels; SNLS_ERR_HIP on a launch failure. */
+snls_status snls_chain_flows(const float* fflow, const float* bflow, int32_t B, int32_t T, int32_t H, int32_t W,
+                             int32_t wt, float* flows, void* stream);
+
 #define SNLS_OP_SEARCH 0
 #define SNLS_OP_AGGREGATE 1
 #define SNLS_OP_BACKWARD 2
+#define SNLS_OP_AGGREGATE_STACKED 3
 
 /* Device workspace in bytes that operation op needs for parameters p
  * (0 when none is needed; (size_t)-1 for invalid arguments). */

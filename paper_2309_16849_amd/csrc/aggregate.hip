@@ -580,6 +580,14 @@ __global__ void __launch_bounds__(256) aggregate_gather_kernel(const float* __re
     if (c < nc) ob[c * g.HW] = cnt > 0 ? acc[c] * inv : 0.f;
 }
 
+snls_status launch_softmax_weights(const float* dists, const float* inds, const Geo& g, float scale, float* wts,
+                                   hipStream_t s) {
+  if (g.rows == 0) return SNLS_OK;
+  hipLaunchKernelGGL(softmax_weights_kernel, dim3((unsigned)((g.rows + 255) / 256)), dim3(256), 0, s, dists, inds, g,
+                     scale, wts);
+  return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+}
+
 size_t aggregate_ws_bytes(const Geo& g) {
   size_t w = (size_t)g.rows * (size_t)g.k * sizeof(float);
   w = (w + 255) & ~(size_t)255;

@@ -52,6 +52,8 @@ size_t snls_workspace_size(int op, const snls_params* p) {
   if (op == SNLS_OP_SEARCH) return check_params(p, false, &g) == SNLS_OK ? search_ws_bytes(g) : (size_t)-1;
   if (op == SNLS_OP_AGGREGATE) return check_params(p, true, &g) == SNLS_OK ? aggregate_ws_bytes(g) : (size_t)-1;
   if (op == SNLS_OP_BACKWARD) return check_params(p, true, &g) == SNLS_OK ? backward_ws_bytes(g) : (size_t)-1;
+  if (op == SNLS_OP_AGGREGATE_STACKED)
+    return check_params(p, true, &g) == SNLS_OK ? aggregate_stacked_ws_bytes(g) : (size_t)-1;
   return (size_t)-1;
 }
 
@@ -88,6 +90,31 @@ snls_status snls_aggregate(const float* v, const float* dists, const float* inds
     return SNLS_ERR_WORKSPACE;
   if ((st = device_ready()) != SNLS_OK) return st;
   return launch_aggregate(v, dists, inds, g, scale, out, workspace, as_stream(stream));
+}
+
+snls_status snls_aggregate_stacked(const float* v, const float* dists, const float* inds, const snls_params* p,
+                                   float scale, float* stacked, void* workspace, size_t workspace_bytes,
+                                   void* stream) {
+  Geo g;
+  snls_status st = check_params(p, true, &g);
+  if (st != SNLS_OK) return st;
+  if (!v || !dists || !inds || !stacked || !std::isfinite(scale)) return SNLS_ERR_INVALID_ARG;
+  if ((long long)g.B * g.HD * g.k * g.T * ((g.Ch + 15) / 16) * g.HW > 0xffffffffLL * 256) return SNLS_ERR_UNSUPPORTED;
+  if (!workspace || workspace_bytes < aggregate_stacked_ws_bytes(g) || (reinterpret_cast<uintptr_t>(workspace) & 255))
+    return SNLS_ERR_WORKSPACE;
+  if ((st = device_ready()) != SNLS_OK) return st;
+  return launch_aggregate_stacked(v, dists, inds, g, scale, stacked, workspace, as_stream(stream));
+}
+
+snls_status snls_chain_flows(const float* fflow, const float* bflow, int32_t B, int32_t T, int32_t H, int32_t W,
+                             int32_t wt, float* flows, void* stream) {
+  if (B < 1 || T < 1 || H < 1 || W < 1 || wt < 0) return SNLS_ERR_INVALID_ARG;
+  if ((long long)H * W > (1LL << 30) || wt > 63) return SNLS_ERR_UNSUPPORTED;
+  if ((long long)B * T * 2 * H * W > 0xffffffffLL * 256) return SNLS_ERR_UNSUPPORTED;
+  if (wt > 0 && (!fflow || !bflow || !flows)) return SNLS_ERR_INVALID_ARG;
+  snls_status st;
+  if ((st = device_ready()) != SNLS_OK) return st;
+  return launch_chain_flows(fflow, bflow, B, T, H, W, wt, flows, as_stream(stream));
 }
 
 snls_status snls_backward(const float* q, const float* k, const float* v, const float* flows, const float* dists,

@@ -37,6 +37,8 @@ snls_status check_topk_args(int64_t rows, int32_t n_cand, int32_t k, int32_t dis
 // Device workspace of snls_aggregate: softmax weights (rows x k) then a
 // channels-last copy of V, 256-byte aligned.
 size_t aggregate_ws_bytes(const Geo& g);
+// Device workspace of snls_aggregate_stacked: softmax weights (rows x k).
+size_t aggregate_stacked_ws_bytes(const Geo& g);
 
 // The tiled search path (S_Q = 1, P <= 7, Ws <= 9; inner product with
 // S_K <= 1, squared L2 with S_K = 1) and its workspace: the inner-product
@@ -69,6 +71,12 @@ snls_status launch_topk(const float* dall, const float* iall, int64_t rows, int 
                         float* dists, float* inds, hipStream_t s);
 snls_status launch_aggregate(const float* v, const float* dists, const float* inds, const Geo& g, float scale,
                              float* out, void* ws, hipStream_t s);
+snls_status launch_softmax_weights(const float* dists, const float* inds, const Geo& g, float scale, float* wts,
+                                   hipStream_t s);
+snls_status launch_chain_flows(const float* fflow, const float* bflow, int B, int T, int H, int W, int wt,
+                               float* flows, hipStream_t s);
+snls_status launch_aggregate_stacked(const float* v, const float* dists, const float* inds, const Geo& g,
+                                     float scale, float* stacked, void* ws, hipStream_t s);
 snls_status launch_backward(const float* q, const float* k, const float* v, const float* dists, const float* inds,
                             const float* grad_out, const float* grad_dists, const Geo& g, float scale,
                             float* grad_q, float* grad_k, float* grad_v, float* grad_flows, float* Gws,

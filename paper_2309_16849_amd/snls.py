@@ -6,7 +6,8 @@ There is no CPU fallback -- if libsnls.so is missing or fails to load, every
 call raises.
 
 Functions carry the C names: snls_search, snls_topk, snls_aggregate,
-snls_backward, snls_workspace_size, snls_status_string, snls_abi_version.
+snls_backward, snls_aggregate_stacked, snls_chain_flows, snls_workspace_size,
+snls_status_string, snls_abi_version.
 Parameters are plain dicts with keys B, T, C, H, W, HD, ws, wt, ps, stride0,
 stride1, k, dist_type (see ``params_from_dict``).
 """
@@ -22,10 +23,10 @@ LIB_PATH = os.path.join(_HERE, "libsnls.so")
 
 SNLS_OK, SNLS_ERR_INVALID_ARG, SNLS_ERR_UNSUPPORTED, SNLS_ERR_HIP, SNLS_ERR_WORKSPACE = range(5)
 SNLS_DIST_PROD, SNLS_DIST_L2 = 0, 1
-SNLS_OP_SEARCH, SNLS_OP_AGGREGATE, SNLS_OP_BACKWARD = 0, 1, 2
+SNLS_OP_SEARCH, SNLS_OP_AGGREGATE, SNLS_OP_BACKWARD, SNLS_OP_AGGREGATE_STACKED = 0, 1, 2, 3
 SNLS_MAX_K = 128
 SYMBOLS = ("snls_search", "snls_topk", "snls_aggregate", "snls_backward", "snls_workspace_size",
-           "snls_status_string", "snls_abi_version")
+           "snls_status_string", "snls_abi_version", "snls_aggregate_stacked", "snls_chain_flows")
 
 
 class SnlsParams(ctypes.Structure):
@@ -57,12 +58,15 @@ def load_library():
         lib.snls_topk.argtypes = [P, P, I64, I32, I32, I32, P, P, P]
         lib.snls_aggregate.argtypes = [P, P, P, PP, F32, P, P, SZ, P]
         lib.snls_backward.argtypes = [P] * 8 + [PP, F32, P, P, P, P, P, SZ, P]
+        lib.snls_aggregate_stacked.argtypes = [P, P, P, PP, F32, P, P, SZ, P]
+        lib.snls_chain_flows.argtypes = [P, P, I32, I32, I32, I32, I32, P, P]
         lib.snls_workspace_size.argtypes = [ctypes.c_int, PP]
         lib.snls_workspace_size.restype = SZ
         lib.snls_status_string.argtypes = [ctypes.c_int]
         lib.snls_status_string.restype = ctypes.c_char_p
         lib.snls_abi_version.argtypes = []
-        for f in ("snls_search", "snls_topk", "snls_aggregate", "snls_backward", "snls_abi_version"):
+        for f in ("snls_search", "snls_topk", "snls_aggregate", "snls_backward", "snls_abi_version",
+                  "snls_aggregate_stacked", "snls_chain_flows"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -224,3 +228,39 @@ def snls_backward(q, k, v, flows, dists, inds, grad_out, p: dict, scale: float =
                              _ptr(grad_dists), ctypes.byref(prm), float(scale), _ptr(gq), _ptr(gk), _ptr(gv),
                              _ptr(gf), _ptr(workspace), workspace.numel() * 4, _stream(stream)), "snls_backward")
     return gq, gk, gv, gf
+
+
+def snls_aggregate_stacked(v, dists, inds, p: dict, scale: float = 1.0, stacked=None, workspace=None, stream=None):
+    """Aggregation with the k neighbours kept apart; returns (B, HD, k, T, C/HD, H, W)."""
+    lib = load_library()
+    _dev(v, "v", video_shape(p))
+    shp = out_shape(p)
+    _dev(dists, "dists", shp)
+    _dev(inds, "inds", shp + (3,))
+    st_shape = (p["B"], p["HD"], p["k"], p["T"], p["C"] // p["HD"], p["H"], p["W"])
+    if stacked is None:
+        stacked = torch.empty(st_shape, device=v.device, dtype=torch.float32)
+    _dev(stacked, "stacked", st_shape)
+    if workspace is None:
+        workspace = workspace_for(SNLS_OP_AGGREGATE_STACKED, p, v.device)
+    prm = params_from_dict(p)
+    _check(lib.snls_aggregate_stacked(_ptr(v), _ptr(dists), _ptr(inds), ctypes.byref(prm), float(scale),
+                                      _ptr(stacked), _ptr(workspace), workspace.numel() * 4, _stream(stream)),
+           "snls_aggregate_stacked")
+    return stacked
+
+
+def snls_chain_flows(fflow, bflow, wt: int, flows=None, stream=None):
+    """Window offsets (B, T, 2wt, 2, H, W) composed from one-step flows (B, T, 2, H, W)."""
+    lib = load_library()
+    _dev(fflow, "fflow")
+    B, T, two, H, W = fflow.shape
+    if two != 2:
+        raise ValueError("fflow must be (B, T, 2, H, W)")
+    _dev(bflow, "bflow", tuple(fflow.shape))
+    if flows is None:
+        flows = torch.empty((B, T, 2 * wt, 2, H, W), device=fflow.device, dtype=torch.float32)
+    _dev(flows, "flows", (B, T, 2 * wt, 2, H, W))
+    _check(lib.snls_chain_flows(_ptr(fflow), _ptr(bflow), B, T, H, W, int(wt), _ptr(flows), _stream(stream)),
+           "snls_chain_flows")
+    return flows

@@ -153,3 +153,19 @@ def test_binding_refuses_cpu_tensors():
     x = torch.zeros(1, 1, 2, 4, 4)
     with pytest.raises(ValueError):
         B.snls_search(x, x, None, p)
+
+
+def test_stacked_and_chain_validation(lib):
+    prm = _params()
+    need = lib.snls_workspace_size(B.SNLS_OP_AGGREGATE_STACKED, ctypes.byref(prm))
+    assert need == 1 * 2 * 3 * 16 * 17 * 4 * 4  # softmax weights, rows x k
+    assert lib.snls_aggregate_stacked(FAKE, FAKE, FAKE, ctypes.byref(_params(k=0)), 1.0, FAKE, FAKE, BIG,
+                                      None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_aggregate_stacked(FAKE, FAKE, None, ctypes.byref(prm), 1.0, FAKE, FAKE, BIG,
+                                      None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_aggregate_stacked(FAKE, FAKE, FAKE, ctypes.byref(prm), 1.0, FAKE, FAKE, need - 1,
+                                      None) == B.SNLS_ERR_WORKSPACE
+    for args in ((0, 3, 4, 4, 1), (1, 0, 4, 4, 1), (1, 3, 0, 4, 1), (1, 3, 4, 0, 1), (1, 3, 4, 4, -1)):
+        assert lib.snls_chain_flows(FAKE, FAKE, *args, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_chain_flows(FAKE, None, 1, 3, 4, 4, 2, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_chain_flows(FAKE, FAKE, 1, 3, 4, 4, 64, FAKE, None) == B.SNLS_ERR_UNSUPPORTED

@@ -324,6 +324,54 @@ def test_p1_search(dev, case):
     assert_close(_h(out), oracle.aggregate(v, _h(gd), _h(gi), p, 0.5), "aggregate (P = 1)")
 
 
+# ------------------------------------------- the example's interface --
+
+@pytest.mark.parametrize("nb,T,H,W,wt,kind", [(1, 5, 23, 31, 2, "frac"), (2, 4, 9, 14, 3, "frac"),
+                                              (1, 6, 16, 16, 2, "int"), (1, 3, 1, 7, 2, "frac"),
+                                              (1, 7, 12, 10, 4, "far")])
+def test_chain_flows(dev, nb, T, H, W, wt, kind):
+    """Flow chaining from one-step forward/backward flows against the oracle;
+    then a search on the chained offsets against the oracle's."""
+    r = np.random.default_rng(9400 + T + H)
+    shp = (nb, T, 2, H, W)
+    if kind == "int":
+        ff, bf = r.integers(-2, 3, shp).astype(np.float32), r.integers(-2, 3, shp).astype(np.float32)
+    elif kind == "far":  # large, smooth offsets: most reads clamp at the border (a rough field of this
+        # size would amplify rounding by its gradient at every step of the chain)
+        ff = (r.choice([-30.0, 30.0], (nb, T, 2, 1, 1)) + r.uniform(-0.5, 0.5, shp)).astype(np.float32)
+        bf = (r.choice([-30.0, 30.0], (nb, T, 2, 1, 1)) + r.uniform(-0.5, 0.5, shp)).astype(np.float32)
+    else:
+        ff, bf = r.uniform(-2.5, 2.5, shp).astype(np.float32), r.uniform(-2.5, 2.5, shp).astype(np.float32)
+    fl = B.snls_chain_flows(_d(ff, dev), _d(bf, dev), wt)
+    torch.cuda.synchronize()
+    ref = oracle.chain_flows(ff, bf, wt)
+    assert_close(_h(fl), ref, "chained flows")
+    p = small_params(B=nb, T=T, C=6, H=H, W=W, ws=5, wt=wt, ps=3, k=7)
+    q = r.standard_normal((nb, T, 6, H, W), dtype=np.float32)
+    gd, gi = B.snls_search(_d(q, dev), _d(q, dev), fl, p)
+    torch.cuda.synchronize()
+    res = oracle.search(q, q, _h(fl), p)
+    compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
+
+
+@pytest.mark.parametrize("ps,stride0,HD,k,C", [(7, 1, 1, 10, 64), (3, 2, 2, 5, 12), (1, 2, 4, 30, 64),
+                                                (5, 1, 1, 4, 20)])
+def test_aggregate_stacked(dev, ps, stride0, HD, k, C):
+    """Stacked aggregation against the oracle, and its sum over the neighbours
+    against snls_aggregate on the same neighbours."""
+    p = small_params(T=3, C=C, HD=HD, H=21, W=26, ws=9, wt=1, ps=ps, stride0=stride0, k=k)
+    r = np.random.default_rng(9500 + ps + k)
+    q, kk, v, flows = _inputs(p, 9600 + ps)
+    gd, gi = B.snls_search(_d(q, dev), _d(kk, dev), _d(flows, dev), p)
+    st = B.snls_aggregate_stacked(_d(v, dev), gd, gi, p, 0.3)
+    out = B.snls_aggregate(_d(v, dev), gd, gi, p, 0.3)
+    torch.cuda.synchronize()
+    ref = oracle.aggregate_stacked(v, _h(gd), _h(gi), p, 0.3)
+    assert_close(_h(st), ref, "stacked aggregation")
+    summed = _h(st).astype(np.float64).sum(2).transpose(0, 2, 1, 3, 4, 5).reshape(tuple(out.shape))
+    assert_close(summed, _h(out).astype(np.float64), "stacked aggregation summed over k", rel=1e-4)
+
+
 # --------------------------------------------------- non-finite inputs --
 
 @pytest.mark.parametrize("dist_type,ps,ws", [(0, 3, 5), (0, 7, 9), (1, 3, 5), (0, 4, 8)])
