@@ -164,7 +164,9 @@ snls_status snls_aggregate(const float* v, const float* dists, const float* inds
  * (B,HD,T,nH,nW,k) is dL/d dists or NULL.  Outputs, fully overwritten:
  * grad_q, grad_k, grad_v (B,T,C,H,W) and grad_flows (B,T,2wt,2,H,W) (may be
  * NULL when wt == 0).  workspace: device scratch of at least
- * snls_workspace_size(SNLS_OP_BACKWARD, p) bytes, 256-byte aligned.
+ * snls_workspace_size(SNLS_OP_BACKWARD, p) bytes, 256-byte aligned (the
+ * per-neighbour aggregation terms, channels-last copies of q, k, v and
+ * grad_out, and channels-last gradient accumulators: about 7 videos).
  * Gradients are accumulated with floating-point atomics, so the last bits
  * may differ between runs.
  * Errors: SNLS_ERR_INVALID_ARG, SNLS_ERR_UNSUPPORTED, SNLS_ERR_WORKSPACE,

@@ -580,6 +580,12 @@ __global__ void __launch_bounds__(256) aggregate_gather_kernel(const float* __re
     if (c < nc) ob[c * g.HW] = cnt > 0 ? acc[c] * inv : 0.f;
 }
 
+snls_status launch_to_channels_last(const float* x, const Geo& g, float* xcl, hipStream_t s) {
+  dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
+  hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, x, g, xcl);
+  return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+}
+
 snls_status launch_softmax_weights(const float* dists, const float* inds, const Geo& g, float scale, float* wts,
                                    hipStream_t s) {
   if (g.rows == 0) return SNLS_OK;

@@ -23,8 +23,6 @@ snls_status device_ready() {
   return SNLS_OK;
 }
 
-size_t backward_ws_bytes(const Geo& g) { return (size_t)g.rows * (size_t)g.k * sizeof(float); }
-
 // Only the scored top-k paths need scratch: the scores of every candidate.
 size_t search_ws_bytes(const Geo& g) {
   return g.k >= 1 && (tile_supported(g) || p1_supported(g)) ? tile_ws_bytes(g) : 0;

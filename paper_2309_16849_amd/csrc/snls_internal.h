@@ -37,6 +37,9 @@ snls_status check_topk_args(int64_t rows, int32_t n_cand, int32_t k, int32_t dis
 // Device workspace of snls_aggregate: softmax weights (rows x k) then a
 // channels-last copy of V, 256-byte aligned.
 size_t aggregate_ws_bytes(const Geo& g);
+// Device workspace of snls_backward: per-neighbour aggregation terms (rows x
+// k), channels-last copies of q, k, v, grad_out and accumulators of dq, dk, dv.
+size_t backward_ws_bytes(const Geo& g);
 // Device workspace of snls_aggregate_stacked: softmax weights (rows x k).
 size_t aggregate_stacked_ws_bytes(const Geo& g);
 
@@ -71,6 +74,7 @@ snls_status launch_topk(const float* dall, const float* iall, int64_t rows, int 
                         float* dists, float* inds, hipStream_t s);
 snls_status launch_aggregate(const float* v, const float* dists, const float* inds, const Geo& g, float scale,
                              float* out, void* ws, hipStream_t s);
+snls_status launch_to_channels_last(const float* x, const Geo& g, float* xcl, hipStream_t s);
 snls_status launch_softmax_weights(const float* dists, const float* inds, const Geo& g, float scale, float* wts,
                                    hipStream_t s);
 snls_status launch_chain_flows(const float* fflow, const float* bflow, int B, int T, int H, int W, int wt,

@@ -545,6 +545,30 @@ def test_backward_matches_oracle(dev):
     assert np.any(_h(grads[3]) != 0)
 
 
+@pytest.mark.parametrize("kw", [dict(dist_type=1, ps=3, ws=5, k=6), dict(HD=2, C=40, ps=5, ws=5, k=5),
+                                dict(C=96, ps=3, ws=3, k=4, H=17, W=19), dict(stride0=2, ps=1, ws=7, k=9, HD=4, C=16),
+                                dict(stride0=2, ps=3, ws=5, k=7, dist_type=1, wt=2, T=5)],
+                         ids=["l2", "heads", "c96", "p1-s2", "l2-s2"])
+def test_backward_shapes(dev, kw):
+    """Gradients against the oracle over distances, heads, channel counts
+    above one wave and query strides."""
+    p = small_params(T=3, C=8, H=20, W=23, ws=5, wt=1, ps=3, k=5)
+    p.update(kw)
+    r = np.random.default_rng(6100 + len(str(kw)))
+    q, k, v, flows = _inputs(p, 6200 + p["C"] + p["ps"])
+    q *= 0.3
+    k *= 0.3
+    go = r.standard_normal(q.shape, dtype=np.float32)
+    scale = 0.4
+    qd, kd, vd, fd = (_d(a, dev) for a in (q, k, v, flows))
+    gd, gi = B.snls_search(qd, kd, fd, p)
+    grads = B.snls_backward(qd, kd, vd, fd, gd, gi, _d(go, dev), p, scale)
+    torch.cuda.synchronize()
+    ref = oracle.backward(q, k, v, flows, _h(gd), _h(gi), go, p, scale)
+    for name, g_gpu, g_ref in zip(("dq", "dk", "dv", "dflows"), grads, ref):
+        assert_close(_h(g_gpu), g_ref, name)
+
+
 def test_backward_adjoint_full_size(dev):
     """train256 at full size: v -> out is linear for fixed neighbours, so
     <out(x), y> = <x, grad_v(y)> with both sides from the GPU."""
