@@ -14,8 +14,10 @@
 // position for 64 channels) and accumulated.
 //
 // Kernels: softmax weights per (row, neighbour); transpose of V to
-// (B,T,H,W,C); the merged gather; plus the plain per-tap gather used when a
-// configuration exceeds the merged kernel's limits.
+// (B,T,H,W,C); the tiled gather (query stride 1); the merged gather; the
+// per-query gather of single-pixel patches (any query stride); plus the
+// plain per-tap gather used when a configuration exceeds the other kernels'
+// limits.
 #include "snls_internal.h"
 
 namespace snls {
@@ -32,22 +34,35 @@ constexpr float QSCALE = 16777216.f;   // fixed point 2^24
 
 // Softmax weights of each row (0 for non-finite scores, for neighbours whose
 // frame is not an integer in [0,T) or whose position is not finite).
+// G lanes per row (G: the power of two >= k, at most 64): lane i of a row
+// reads neighbours i, i + G, ... (consecutive lanes, consecutive addresses)
+// and the row's maximum and normaliser are reduced across its G lanes.
+template <int G>
 __global__ void __launch_bounds__(256) softmax_weights_kernel(const float* __restrict__ dists,
                                                               const float* __restrict__ inds, Geo g, float scale,
                                                               float* __restrict__ wts) {
-  long long row = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (row >= g.rows) return;
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long row = gid / G;
+  const int sub = (int)(gid % G);
+  const bool live = row < g.rows;  // every lane takes part in the shuffles
   const float sscale = (g.dist == SNLS_DIST_PROD ? 1.f : -1.f) * scale;
   const float* d = dists + row * g.k;
   const float* ind = inds + row * g.k * 3;
   float m = -INFINITY;
-  for (int l = 0; l < g.k; ++l)
-    if (isfinite(d[l])) m = fmaxf(m, sscale * d[l]);
+  if (live)
+    for (int l = sub; l < g.k; l += G)
+      if (isfinite(d[l])) m = fmaxf(m, sscale * d[l]);
+#pragma unroll
+  for (int off = G / 2; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
   float z = 0.f;
-  for (int l = 0; l < g.k; ++l)
-    if (isfinite(d[l])) z += expf(sscale * d[l] - m);
+  if (live)
+    for (int l = sub; l < g.k; l += G)
+      if (isfinite(d[l])) z += expf(sscale * d[l] - m);
+#pragma unroll
+  for (int off = G / 2; off > 0; off >>= 1) z += __shfl_xor(z, off);
+  if (!live) return;
   const float inv = z > 0.f ? 1.f / z : 0.f;
-  for (int l = 0; l < g.k; ++l) {
+  for (int l = sub; l < g.k; l += G) {
     const float tf = ind[3 * l], dh = ind[3 * l + 1], dw = ind[3 * l + 2];
     const bool ok = isfinite(d[l]) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < 1.0e6f &&
                     fabsf(dw) < 1.0e6f;
@@ -517,6 +532,145 @@ __global__ void __launch_bounds__(256) aggregate_tile_kernel(const float* __rest
   }
 }
 
+// (B,T,C,H,W) -> (B,T,HD,H,W,C_h): channels last within each head, so that
+// one head's channels of a pixel are contiguous (64 B for 16 channels).
+__global__ void __launch_bounds__(256) to_head_channels_last_kernel(const float* __restrict__ v, Geo g,
+                                                                    float* __restrict__ vhl) {
+  __shared__ float tileb[64][65];
+  const long long bt = blockIdx.z;
+  const int c0 = blockIdx.y * 64;
+  const long long p0 = (long long)blockIdx.x * 64;
+  const float* src = v + bt * g.C * g.HW;
+  float* dst = vhl + bt * g.C * g.HW;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i;
+    const long long p = p0 + tx;
+    tileb[i][tx] = (c < g.C && p < g.HW) ? src[(long long)c * g.HW + p] : 0.f;
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const long long p = p0 + i;
+    const int c = c0 + tx;
+    if (c < g.C && p < g.HW) dst[((long long)(c / g.Ch) * g.HW + p) * g.Ch + c % g.Ch] = tileb[tx][i];
+  }
+}
+
+// Single-pixel patches (P = 1): a query covers only its own pixel (count 1),
+// so the output at a query pixel is the weighted sum of the k bilinear reads
+// of its neighbours and every other pixel is 0 (a query stride above 1
+// leaves holes).  A workgroup takes 64 consecutive query rows: their scores
+// and positions are copied to LDS with consecutive threads on consecutive
+// addresses, and one thread per row turns the scores into softmax weights.
+// Then each thread takes (query, group of 4 channels) pairs -- consecutive
+// lanes the channel groups of one query, then the next query -- and reads
+// per neighbour four 16-byte pieces of the head-major channels-last V (the
+// lanes of a query read one contiguous pixel record per tap).  Each pair
+// also clears the other pixels of its S_Q x S_Q cell.
+namespace aggp1 {
+constexpr int NQ = 64;    // query rows per workgroup
+constexpr int KMAX = 60;  // neighbours per row (LDS below 64 KB)
+// dynamic LDS: NQ rows of scores / weights (odd pitch), then NQ rows of positions
+SNLS_DEV int pitch(int k) { return k | 1; }
+inline size_t lds_bytes(int k) { return (size_t)NQ * ((k | 1) + 3 * k) * sizeof(float); }
+}  // namespace aggp1
+
+__global__ void __launch_bounds__(256) aggregate_p1_kernel(const float* __restrict__ vhl,
+                                                           const float* __restrict__ dists,
+                                                           const float* __restrict__ inds, Geo g, float scale,
+                                                           float* __restrict__ out) {
+  using namespace aggp1;
+  extern __shared__ float lds_p1[];
+  const int k = g.k, KP = pitch(k);
+  float* wl_s = lds_p1;              // scores, then weights (0: neighbour skipped)
+  float* ind_s = lds_p1 + NQ * KP;   // (frame, disp_h, disp_w) per neighbour
+  const int tid = threadIdx.x;
+  const long long row0 = (long long)blockIdx.x * NQ;
+  const int nq = (int)min((long long)NQ, g.rows - row0);
+  for (int e = tid; e < nq * k; e += 256) wl_s[(e / k) * KP + e % k] = dists[row0 * k + e];
+  for (int e = tid; e < nq * 3 * k; e += 256) ind_s[e] = inds[row0 * 3 * k + e];
+  __syncthreads();
+  if (tid < nq) {
+    const float sscale = (g.dist == SNLS_DIST_PROD ? 1.f : -1.f) * scale;
+    float* d = &wl_s[tid * KP];
+    const float* ind = &ind_s[tid * 3 * k];
+    float m = -INFINITY;
+    for (int l = 0; l < k; ++l)
+      if (isfinite(d[l])) m = fmaxf(m, sscale * d[l]);
+    float z = 0.f;
+    for (int l = 0; l < k; ++l)
+      if (isfinite(d[l])) z += expf(sscale * d[l] - m);
+    const float inv = z > 0.f ? 1.f / z : 0.f;
+    for (int l = 0; l < k; ++l) {
+      const float tf = ind[3 * l], dh = ind[3 * l + 1], dw = ind[3 * l + 2];
+      const bool ok = isfinite(d[l]) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < 1.0e6f &&
+                      fabsf(dw) < 1.0e6f;
+      d[l] = ok ? expf(sscale * d[l] - m) * inv : 0.f;
+    }
+  }
+  __syncthreads();
+  const int ngrp = g.Ch / 4;
+  for (int pr = tid; pr < nq * ngrp; pr += 256) {
+    const int jq = pr / ngrp, cg = pr - jq * ngrp;
+    const long long row = row0 + jq;
+    const int mw = (int)(row % g.nW);
+    long long r = row / g.nW;
+    const int mh = (int)(r % g.nH);
+    r /= g.nH;
+    const int t = (int)(r % g.T);
+    r /= g.T;
+    const int hd = (int)(r % g.HD);
+    const int b = (int)(r / g.HD);
+    const int h = mh * g.s0, w = mw * g.s0;
+    const float* wrow = &wl_s[jq * KP];
+    const float* ind = &ind_s[jq * 3 * k];
+    // head plane of V (frame added per neighbour), this thread's 4 channels
+    const float* vh = vhl + ((long long)b * g.T * g.HD + hd) * g.HW * g.Ch + 4 * cg;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    // branch-free body (a skipped neighbour reads nothing and adds 0), so
+    // the reads of several neighbours are in flight together
+#pragma unroll 2
+    for (int l = 0; l < k; ++l) {
+      const float wl = wrow[l];
+      const bool use = wl != 0.f;
+      const float tf = use ? ind[3 * l] : 0.f;
+      const float dh = use ? ind[3 * l + 1] : 0.f, dw = use ? ind[3 * l + 2] : 0.f;
+      int ny, nx;
+      float ay, ax;
+      split_disp(dh, &ny, &ay);
+      split_disp(dw, &nx, &ax);
+      const int y0 = h + ny, x0 = w + nx;
+      const float* vb = vh + (long long)(int)tf * g.HD * g.HW * g.Ch;
+      const bool y0in = use && y0 >= 0 && y0 < g.H, y1in = use && y0 + 1 >= 0 && y0 + 1 < g.H;
+      const bool x0in = x0 >= 0 && x0 < g.W, x1in = x0 + 1 >= 0 && x0 + 1 < g.W;
+      const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+      const long long o = ((long long)y0 * g.W + x0) * g.Ch;
+      const float4 v00 = (y0in && x0in) ? *reinterpret_cast<const float4*>(vb + o) : zero;
+      const float4 v01 = (y0in && x1in) ? *reinterpret_cast<const float4*>(vb + o + g.Ch) : zero;
+      const float4 v10 = (y1in && x0in) ? *reinterpret_cast<const float4*>(vb + o + (long long)g.W * g.Ch) : zero;
+      const float4 v11 =
+          (y1in && x1in) ? *reinterpret_cast<const float4*>(vb + o + (long long)(g.W + 1) * g.Ch) : zero;
+      auto tap = [&](float a00, float a01, float a10, float a11) {
+        const float top = (1.f - ax) * a00 + ax * a01;
+        const float bot = (1.f - ax) * a10 + ax * a11;
+        return (1.f - ay) * top + ay * bot;
+      };
+      acc.x = fmaf(wl, tap(v00.x, v01.x, v10.x, v11.x), acc.x);
+      acc.y = fmaf(wl, tap(v00.y, v01.y, v10.y, v11.y), acc.y);
+      acc.z = fmaf(wl, tap(v00.z, v01.z, v10.z, v11.z), acc.z);
+      acc.w = fmaf(wl, tap(v00.w, v01.w, v10.w, v11.w), acc.w);
+    }
+    float* ob = out + (((long long)b * g.T + t) * g.C + hd * g.Ch + 4 * cg) * g.HW;
+    const float res[4] = {acc.x, acc.y, acc.z, acc.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float* pl = ob + (long long)i * g.HW;
+      for (int a = 0; a < g.s0 && h + a < g.H; ++a)
+        for (int e = 0; e < g.s0 && w + e < g.W; ++e) pl[(long long)(h + a) * g.W + w + e] = (a | e) ? 0.f : res[i];
+    }
+  }
+}
+
 // Plain per-tap gather for configurations beyond the merged kernel's limits
 // (more than 7 frames per window or more than 256 channels per head).
 constexpr int kAggChunk = 16;
@@ -589,8 +743,24 @@ snls_status launch_to_channels_last(const float* x, const Geo& g, float* xcl, hi
 snls_status launch_softmax_weights(const float* dists, const float* inds, const Geo& g, float scale, float* wts,
                                    hipStream_t s) {
   if (g.rows == 0) return SNLS_OK;
-  hipLaunchKernelGGL(softmax_weights_kernel, dim3((unsigned)((g.rows + 255) / 256)), dim3(256), 0, s, dists, inds, g,
-                     scale, wts);
+  const int G = g.k <= 1 ? 1 : g.k <= 2 ? 2 : g.k <= 4 ? 4 : g.k <= 8 ? 8 : g.k <= 16 ? 16 : g.k <= 32 ? 32 : 64;
+  const long long nthr = g.rows * G;
+  if ((nthr + 255) / 256 > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
+  const dim3 grid((unsigned)((nthr + 255) / 256));
+  switch (G) {
+#define SNLS_SOFTMAX_CASE(N)                                                                                   \
+  case N:                                                                                                      \
+    hipLaunchKernelGGL(softmax_weights_kernel<N>, grid, dim3(256), 0, s, dists, inds, g, scale, wts);          \
+    break;
+    SNLS_SOFTMAX_CASE(1)
+    SNLS_SOFTMAX_CASE(2)
+    SNLS_SOFTMAX_CASE(4)
+    SNLS_SOFTMAX_CASE(8)
+    SNLS_SOFTMAX_CASE(16)
+    SNLS_SOFTMAX_CASE(32)
+    SNLS_SOFTMAX_CASE(64)
+#undef SNLS_SOFTMAX_CASE
+  }
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
 }
 
@@ -622,8 +792,20 @@ snls_status launch_aggregate(const float* v, const float* dists, const float* in
                        tiles_x, tiles_y, out);
     return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
   }
-  hipLaunchKernelGGL(softmax_weights_kernel, dim3((unsigned)((g.rows + 255) / 256)), dim3(256), 0, s, dists, inds, g,
-                     scale, wts);
+  if (g.ps == 1 && g.Ch % 4 == 0 && g.k <= aggp1::KMAX) {
+    // single-pixel patches: per-query gather, holes cleared
+    const long long nblk = (g.rows + aggp1::NQ - 1) / aggp1::NQ;
+    if (nblk > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
+    dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
+    hipLaunchKernelGGL(to_head_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
+    hipLaunchKernelGGL(aggregate_p1_kernel, dim3((unsigned)nblk), dim3(256), aggp1::lds_bytes(g.k), s, vcl, dists,
+                       inds, g, scale, out);
+    return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+  }
+  {
+    const snls_status st = launch_softmax_weights(dists, inds, g, scale, wts, s);
+    if (st != SNLS_OK) return st;
+  }
   if (nslot <= agg::NSLOT && g.Ch <= 256 && (long long)g.T * g.HW * g.C < (1LL << 31) && g.ps <= 11) {
     dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
     hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);

@@ -162,16 +162,19 @@ def test_aggregate_tiled_motion(dev, ps, k, C, HD, scale):
     assert_close(_h(out), ref, "tiled aggregate (motion neighbours)")
 
 
-@pytest.mark.parametrize("seed", [0, 1])
-def test_aggregate_tiled_odd_neighbours(dev, seed):
+@pytest.mark.parametrize("seed,ps,stride0,HD", [(0, 5, 1, 1), (1, 5, 1, 1), (2, 1, 2, 2), (3, 1, 3, 1),
+                                                (4, 3, 2, 1), (5, 1, 1, 4)])
+def test_aggregate_tiled_odd_neighbours(dev, seed, ps, stride0, HD):
     """Caller-given neighbours: frames outside the window or the clip,
     non-integer frames, huge and non-finite displacements, non-finite scores,
-    neighbours far from the others (direct path) and integer positions."""
-    p = small_params(T=4, C=64, H=21, W=35, ws=5, wt=1, ps=5, k=6)
+    neighbours far from the others (direct path) and integer positions.
+    Query stride 1 takes the tiled gather, single-pixel patches with a larger
+    stride the per-query gather, the others the merged gather."""
+    p = small_params(T=4, C=64, HD=HD, H=21, W=35, ws=5, wt=1, ps=ps, stride0=stride0, k=6)
     r = np.random.default_rng(9300 + seed)
     v = r.standard_normal((1, 4, 64, 21, 35), dtype=np.float32)
     nH, nW = oracle.grid(p)
-    shp = (1, 1, 4, nH, nW, 6)
+    shp = (1, HD, 4, nH, nW, 6)
     d = r.standard_normal(shp).astype(np.float32)
     t_q = np.arange(4)[None, None, :, None, None, None]
     ind = np.zeros(shp + (3,), np.float32)
@@ -187,11 +190,28 @@ def test_aggregate_tiled_odd_neighbours(dev, seed):
     ind[..., 1] = np.where((m > 0.19) & (m < 0.21), 3.0e6, ind[..., 1])  # absurd displacement
     ind[..., 2] = np.where((m > 0.21) & (m < 0.22), np.nan, ind[..., 2])
     d = np.where((m > 0.22) & (m < 0.24), -np.inf, d).astype(np.float32)
-    d[0, 0, 1, 3, 4, :] = -np.inf  # a row with no finite score
+    d[0, 0, 1, 3, 4 % nW, :] = -np.inf  # a row with no finite score
     out = B.snls_aggregate(_d(v, dev), _d(d, dev), _d(ind, dev), p, 0.7)
     torch.cuda.synchronize()
     ref = oracle.aggregate(v, d, ind, p, 0.7)
     assert_close(_h(out), ref, "tiled aggregate (odd neighbours)")
+
+
+@pytest.mark.parametrize("stride0,HD,C,k,H,W", [(2, 4, 64, 30, 37, 29), (1, 1, 16, 7, 20, 23), (3, 2, 8, 5, 17, 16),
+                                                (2, 1, 4, 1, 9, 10), (2, 2, 64, 12, 33, 40), (2, 1, 8, 60, 19, 21),
+                                                (2, 1, 8, 61, 15, 14), (1, 3, 12, 3, 70, 9)])
+def test_aggregate_p1(dev, stride0, HD, C, k, H, W):
+    """Single-pixel patches: per-query gather of the searched neighbours,
+    holes of the query grid cleared."""
+    p = small_params(T=4, C=C, HD=HD, H=H, W=W, ws=7, wt=1, ps=1, stride0=stride0, k=k)
+    x, flows = _motion_inputs(p, 9400 + stride0 + k)
+    v = np.random.default_rng(9500 + k).standard_normal(x.shape, dtype=np.float32)
+    xd = _d(x, dev)
+    gd, gi = B.snls_search(xd, xd, _d(flows, dev), p)
+    out = B.snls_aggregate(_d(v, dev), gd, gi, p, 0.5)
+    torch.cuda.synchronize()
+    ref = oracle.aggregate(v, _h(gd), _h(gi), p, 0.5)
+    assert_close(_h(out), ref, "single-pixel aggregate")
 
 
 def _swap_mask(p, swaps):
@@ -229,7 +249,10 @@ def _tile_cases(n=28, seed=31):
     return cases
 
 
-TILE_CASES = _tile_cases()
+TILE_CASES = _tile_cases() + [
+    (small_params(T=3, C=16, H=23, W=29, ws=9, wt=1, ps=7, k=10), "edge"),
+    (small_params(T=3, C=8, H=17, W=19, ws=5, wt=1, ps=3, k=7, stride1=0.5), "edge"),
+]
 TILE_IDS = ["t%d-ws%d-wt%d-ps%d-sk%g-k%d-%s" % (i, p["ws"], p["wt"], p["ps"], p["stride1"], p["k"], kd)
             for i, (p, kd) in enumerate(TILE_CASES)]
 
@@ -245,6 +268,10 @@ def _tile_flows(p, kind, r):
         return (r.choice([-1.0, 1.0], fshp) * 60.0 + r.uniform(-1, 1, fshp)).astype(np.float32)
     if kind == "int":
         return r.integers(-3, 4, fshp).astype(np.float32)
+    if kind == "edge":  # just below integers: adding a cell offset can round up to the next integer
+        m = r.integers(-3, 4, fshp).astype(np.float32)
+        below = np.nextafter(m, np.float32(-np.inf), dtype=np.float32)
+        return np.where(r.random(fshp) < 0.7, below, r.uniform(-3, 3, fshp)).astype(np.float32)
     return r.uniform(-3, 3, fshp).astype(np.float32)
 
 
@@ -303,6 +330,8 @@ P1_CASES = [
     (small_params(T=3, C=16, HD=1, H=22, W=30, ws=7, wt=1, ps=1, stride0=2, k=9), "wide"),
     (small_params(T=2, C=4, H=17, W=18, ws=5, wt=1, ps=1, stride0=2, k=6), "far"),
     (small_params(T=5, C=33, HD=1, H=25, W=21, ws=14, wt=2, ps=1, stride0=4, k=17), "frac"),
+    (small_params(T=3, C=16, HD=2, H=21, W=27, ws=15, wt=1, ps=1, stride0=2, k=30), "edge"),
+    (small_params(T=3, C=12, HD=1, H=16, W=19, ws=9, wt=1, ps=1, stride0=1, k=10), "edge"),
 ]
 
 
