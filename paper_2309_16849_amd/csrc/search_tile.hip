@@ -653,6 +653,161 @@ __global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __rest
   }
 }
 
+// ---- exact top-k, one wave per scored row (k <= 64, <= 64 * NV candidates) ----
+//
+// Lane l holds candidates l, l + 64, ... as 32-bit keys ordered like the
+// ranking scores (empty slots 0, below every real candidate).  The k-th
+// largest of the 64 lane maxima is a lower bound T of the row's k-th best
+// (at least k lanes hold a candidate >= T), and on scored rows only a few
+// more than k candidates reach it.  Those are compacted into one LDS slot
+// per lane and sorted by (score descending, id ascending) with a bitonic
+// network across the wave.  When more than 64 reach T, the exact k-th key
+// is found by bisection over the keys instead: every key above it plus the
+// smallest ids among the keys equal to it make exactly k entries.
+namespace wtk {
+constexpr int WAVES = 4;  // rows per workgroup
+}  // namespace wtk
+
+SNLS_DEV unsigned order_key(float f) {
+  const unsigned b = __float_as_uint(f);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+SNLS_DEV float key_score(unsigned u) { return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u); }
+SNLS_DEV int lanes_below(unsigned long long m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+}
+SNLS_DEV unsigned long long shfl_xor64(unsigned long long x, int m) {
+  const unsigned lo = __shfl_xor((unsigned)x, m), hi = __shfl_xor((unsigned)(x >> 32), m);
+  return ((unsigned long long)hi << 32) | lo;
+}
+// Bitonic sort of one value per lane, descending across lanes 0..63.
+template <typename V, typename X>
+SNLS_DEV V sort64_desc(V x, int lane, X xchg) {
+#pragma unroll
+  for (int size = 2; size <= 64; size <<= 1)
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      const V p = xchg(x, stride);
+      const bool take_max = ((lane & stride) == 0) == ((lane & size) == 0);
+      x = take_max ? (x > p ? x : p) : (x < p ? x : p);
+    }
+  return x;
+}
+
+template <int NV>
+__global__ void __launch_bounds__(wtk::WAVES * 64) wave_topk_kernel(const float* __restrict__ scores,
+                                                                    const float* __restrict__ gnorm,
+                                                                    const float* __restrict__ qnorm, int pitch,
+                                                                    const float* __restrict__ flows, Geo g,
+                                                                    float* __restrict__ dists,
+                                                                    float* __restrict__ inds) {
+  __shared__ unsigned long long slot[wtk::WAVES][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const long long row = (long long)blockIdx.x * wtk::WAVES + wv;
+  if (row >= g.rows) return;  // whole wave
+  const int ncell = g.ws * g.ws;
+  const int w = (int)(row % g.nW) * g.s0;
+  const int h = (int)((row / g.nW) % g.nH) * g.s0;
+  const int t = (int)((row / ((long long)g.nW * g.nH)) % g.T);
+  const int b = (int)(row / ((long long)g.nW * g.nH * g.T * g.HD));
+  const float* srow = scores + row * pitch;
+  const bool l2 = g.dist == SNLS_DIST_L2;
+  const float qn = l2 ? qnorm[row] : 0.f;
+  const float* grow = l2 ? gnorm + row * pitch : nullptr;
+  // candidate ids of the frames inside the clip (the others score -inf)
+  const int lo = (max(0, t - g.wt) - t + g.wt) * ncell, hi = (min(g.T - 1, t + g.wt) - t + g.wt + 1) * ncell;
+  unsigned u[NV];
+  unsigned umax = 0;
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int c = lane + 64 * v;
+    unsigned key = 0;
+    if (c < g.ncand) {
+      float sc = -INFINITY;
+      if (c >= lo && c < hi) {
+        const float ip = srow[c];
+        if (l2) {
+          const float dd = qn - 2.f * ip + grow[c];
+          sc = ip > -INFINITY && dd == dd ? -dd : -INFINITY;
+        } else {
+          sc = ip == ip ? ip : -INFINITY;
+        }
+      }
+      key = order_key(sc);
+    }
+    u[v] = key;
+    umax = max(umax, key);
+  }
+  auto xchg32 = [](unsigned x, int m) { return (unsigned)__shfl_xor(x, m); };
+  const unsigned smax = sort64_desc(umax, lane, xchg32);
+  const unsigned top = (unsigned)__shfl(smax, 0);
+  const unsigned T1 = (unsigned)__shfl(smax, g.k - 1);
+  auto count_ge = [&](unsigned x) {
+    int n = 0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) n += __popcll(__ballot(u[v] >= x));
+    return n;
+  };
+  unsigned long long* sl = slot[wv];
+  sl[lane] = 0ull;  // pads rank below every entry
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  auto entry = [&](unsigned key, int id) { return ((unsigned long long)key << 32) | (unsigned)(~id); };
+  if (count_ge(T1) <= 64) {
+    int base = 0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const bool take = u[v] >= T1;
+      const unsigned long long bal = __ballot(take);
+      if (take) sl[base + lanes_below(bal)] = entry(u[v], lane + 64 * v);
+      base += __popcll(bal);
+    }
+  } else {
+    // exact k-th key: the largest x with count_ge(x) >= k
+    unsigned klo = T1;
+    unsigned long long khi = (unsigned long long)top + 1;
+    while (khi - klo > 1) {
+      const unsigned mid = (unsigned)(klo + (khi - klo) / 2);
+      if (count_ge(mid) >= g.k) klo = mid;
+      else khi = mid;
+    }
+    const int need = g.k - (klo < top ? count_ge(klo + 1) : 0);  // entries equal to the k-th key
+    int base = 0, eqn = 0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const bool eq = u[v] == klo;
+      const unsigned long long beq = __ballot(eq);
+      const bool take = u[v] > klo || (eq && eqn + lanes_below(beq) < need);
+      eqn += __popcll(beq);
+      const unsigned long long bal = __ballot(take);
+      if (take) sl[base + lanes_below(bal)] = entry(u[v], lane + 64 * v);
+      base += __popcll(bal);
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const unsigned long long best = sort64_desc(sl[lane], lane, shfl_xor64);
+  if (lane >= g.k) return;
+  // every candidate was ranked, so the k best are real candidates; the clamp
+  // only keeps a placeholder id in bounds
+  const int cid = min((int)~(unsigned)best, g.ncand - 1);
+  const int dw = cid % g.ws, dh = (cid / g.ws) % g.ws, dt = cid / ncell - g.wt;
+  float fh = 0.f, fw = 0.f;
+  if (dt != 0) {
+    const long long pix = (long long)h * g.W + w;
+    const long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dt, g.wt)) * 2;
+    fh = flows[base * g.HW + pix];
+    fw = flows[(base + 1) * g.HW + pix];
+  }
+  dists[row * g.k + lane] = from_score(key_score((unsigned)(best >> 32)), g.dist);
+  float* irow = inds + (row * g.k + lane) * 3;
+  irow[0] = (float)(t + dt);
+  irow[1] = cand_disp(fh, g.s1, dh, g.r);
+  irow[2] = cand_disp(fw, g.s1, dw, g.r);
+}
+
 // The tiled path handles S_Q = 1, P <= 7, Ws <= 9 with the inner product
 // (S_K <= 1) or the squared L2 distance (S_K = 1).
 bool tile_supported(const Geo& g) {
@@ -676,6 +831,24 @@ size_t tile_ws_bytes(const Geo& g) {
 // Top-k of the scored rows (any scores kernel of the tiled family).
 static snls_status launch_tile_topk(const float* scores, const float* gnorm, const float* qnorm, int pitch,
                                     const float* flows, const Geo& g, float* dists, float* inds, hipStream_t s) {
+  // Large k: the thread-per-row list insertions diverge on nearly every
+  // candidate, the wave-per-row selection does not.
+  const int nv = (g.ncand + 63) / 64;
+  if (g.k > 16 && g.k <= 64 && nv <= 32) {
+    const unsigned wblocks = (unsigned)((g.rows + wtk::WAVES - 1) / wtk::WAVES);
+#define SNLS_WTK(N)                                                                                               \
+  hipLaunchKernelGGL(wave_topk_kernel<N>, dim3(wblocks), dim3(wtk::WAVES * 64), 0, s, scores, gnorm, qnorm, pitch, \
+                     flows, g, dists, inds)
+    if (nv <= 4) SNLS_WTK(4);
+    else if (nv <= 8) SNLS_WTK(8);
+    else if (nv <= 12) SNLS_WTK(12);
+    else if (nv <= 16) SNLS_WTK(16);
+    else if (nv <= 20) SNLS_WTK(20);
+    else if (nv <= 25) SNLS_WTK(25);
+    else SNLS_WTK(32);
+#undef SNLS_WTK
+    return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+  }
   const unsigned tblocks = (unsigned)((g.rows + tk::ROWS - 1) / tk::ROWS);
   if (g.k <= 12)
     hipLaunchKernelGGL(tile_topk_kernel<12>, dim3(tblocks), dim3(tk::ROWS), 0, s, scores, gnorm, qnorm, pitch, flows,

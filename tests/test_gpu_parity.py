@@ -335,6 +335,36 @@ P1_CASES = [
 ]
 
 
+# Exact ties: 0/1 features and integer offsets make every score an exact
+# integer on both sides, so the order (score, then smaller id) must match the
+# oracle element for element -- the large-k selection's bisection path and
+# its choice among keys equal to the k-th.
+TIE_CASES = [
+    small_params(T=3, C=4, H=20, W=21, ws=9, wt=1, ps=1, stride0=2, k=40),
+    small_params(T=3, C=3, H=17, W=19, ws=7, wt=1, ps=3, k=20),
+    small_params(T=3, C=3, H=17, W=19, ws=7, wt=1, ps=3, k=10),
+    small_params(T=2, C=2, H=16, W=18, ws=5, wt=1, ps=3, k=30, dist_type=1),
+    small_params(T=3, C=1, H=12, W=13, ws=9, wt=2, ps=1, k=64),
+]
+
+
+@pytest.mark.parametrize("case", range(len(TIE_CASES)))
+def test_topk_exact_ties(dev, case):
+    p = TIE_CASES[case]
+    r = np.random.default_rng(8900 + case)
+    shp = (p["B"], p["T"], p["C"], p["H"], p["W"])
+    q = r.integers(0, 2, shp).astype(np.float32)
+    k = r.integers(0, 2, shp).astype(np.float32)
+    fshp = (p["B"], p["T"], 2 * p["wt"], 2, p["H"], p["W"])
+    flows = r.integers(-2, 3, fshp).astype(np.float32)
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    torch.cuda.synchronize()
+    res = oracle.search(q, k, flows, p)
+    kk = p["k"]
+    np.testing.assert_array_equal(_h(gd).reshape(-1, kk), res["dists"][:, :kk].astype(np.float32))
+    np.testing.assert_array_equal(_h(gi).reshape(-1, kk, 3), res["inds"][:, :kk].astype(np.float32))
+
+
 @pytest.mark.parametrize("case", range(len(P1_CASES)),
                          ids=["p%d-ws%d-s%d-%s" % (i, p["ws"], p["stride0"], kd) for i, (p, kd) in enumerate(P1_CASES)])
 def test_p1_search(dev, case):
