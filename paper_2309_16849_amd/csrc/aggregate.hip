@@ -777,6 +777,16 @@ snls_status launch_aggregate(const float* v, const float* dists, const float* in
   size_t woff = ((size_t)g.rows * g.k * sizeof(float) + 255) & ~(size_t)255;
   float* vcl = reinterpret_cast<float*>(static_cast<char*>(ws) + woff);
   const int nslot = 2 * g.wt + 1;
+  if (g.ps == 1 && g.Ch % 4 == 0 && g.k <= aggp1::KMAX) {
+    // single-pixel patches: per-query gather, holes cleared
+    const long long nblk = (g.rows + aggp1::NQ - 1) / aggp1::NQ;
+    if (nblk > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
+    dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
+    hipLaunchKernelGGL(to_head_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
+    hipLaunchKernelGGL(aggregate_p1_kernel, dim3((unsigned)nblk), dim3(256), aggp1::lds_bytes(g.k), s, vcl, dists,
+                       inds, g, scale, out);
+    return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+  }
   // merged kernel limits: frames per window, channels per head, 32-bit
   // offsets inside one batch entry, per-bin weight sums below 2^31 in 2^-24
   // fixed point (at most P^2 <= 121 covering patches)
@@ -790,16 +800,6 @@ snls_status launch_aggregate(const float* v, const float* dists, const float* in
     if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(aggregate_tile_kernel, dim3((unsigned)nwg), dim3(256), 0, s, vcl, dists, inds, g, scale,
                        tiles_x, tiles_y, out);
-    return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
-  }
-  if (g.ps == 1 && g.Ch % 4 == 0 && g.k <= aggp1::KMAX) {
-    // single-pixel patches: per-query gather, holes cleared
-    const long long nblk = (g.rows + aggp1::NQ - 1) / aggp1::NQ;
-    if (nblk > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
-    dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
-    hipLaunchKernelGGL(to_head_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
-    hipLaunchKernelGGL(aggregate_p1_kernel, dim3((unsigned)nblk), dim3(256), aggp1::lds_bytes(g.k), s, vcl, dists,
-                       inds, g, scale, out);
     return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
   }
   {

@@ -139,7 +139,8 @@ def test_aggregate(dev, case):
 # Query stride 1 with up to 7 frames and 64 channels per head goes through
 # the tiled gather: neighbours of smooth motion land in the per-slot bin
 # boxes; scattered neighbours, frames outside the window and odd caller-given
-# positions take its direct path.
+# positions take its direct path.  (Single-pixel patches take the per-query
+# gather at every stride.)
 
 def _motion_inputs(p, seed, amp=4.0):
     from workloads import make_motion_video
@@ -168,8 +169,8 @@ def test_aggregate_tiled_odd_neighbours(dev, seed, ps, stride0, HD):
     """Caller-given neighbours: frames outside the window or the clip,
     non-integer frames, huge and non-finite displacements, non-finite scores,
     neighbours far from the others (direct path) and integer positions.
-    Query stride 1 takes the tiled gather, single-pixel patches with a larger
-    stride the per-query gather, the others the merged gather."""
+    Single-pixel patches take the per-query gather, other patches with query
+    stride 1 the tiled gather, the rest the merged gather."""
     p = small_params(T=4, C=64, HD=HD, H=21, W=35, ws=5, wt=1, ps=ps, stride0=stride0, k=6)
     r = np.random.default_rng(9300 + seed)
     v = r.standard_normal((1, 4, 64, 21, 35), dtype=np.float32)
