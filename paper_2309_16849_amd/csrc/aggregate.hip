@@ -305,32 +305,37 @@ __global__ void __launch_bounds__(256) aggregate_merged_kernel(const float* __re
 //    mean offset of the tile's neighbours in that slot (a neighbour whose
 //    taps leave the box, or whose frame is outside the window, is marked
 //    for the direct path);
-//  * phase 2 (one wave per output row, pixel after pixel): the P*P*k
-//    records of the pixel's covering queries are added into the wave's bins
-//    (integer atomics: the sums do not depend on the order), then each
-//    non-empty bin is one position whose channel vector is read once from
-//    the channels-last copy of V (lane = channel), in bin order.
+//  * phase 2 (one wave per output row, pixel after pixel): the wave's bins
+//    hold the records of the pixel's P x P covering queries (integer
+//    atomics: the sums do not depend on the order); moving one pixel along
+//    the row removes one query column and adds one, so after the row's first
+//    pixel only 2*P*k records change per pixel; each non-empty bin is one
+//    position whose channel vector is read once from the channels-last copy
+//    of V (lane = channel), in bin order.
 namespace aggt {
-constexpr int TY = 4, TX = 16;       // output tile; wave w owns tile row w
+constexpr int TY = 8, TX = 8;        // output tile; wave w owns tile row w
 constexpr int WAVES = TY;
+constexpr int NT = WAVES * 64;       // threads per workgroup
 constexpr int NSLOT = 7;             // frames per window: 2*wt + 1 <= 7
 constexpr int BOX = 8;               // offsets per axis and slot
 constexpr int SB = BOX * BOX;        // bins per slot (one per lane)
-constexpr int MAXREC = 2304;         // (covering query, neighbour) records per tile
-constexpr int MAXQ = 512;            // covering queries per tile
+constexpr int MAXREC = 2048;         // (covering query, neighbour) records per tile
+constexpr int MAXQ = 256;            // covering queries per tile
 constexpr float QSCALE = 16777216.f; // fixed point 2^24
 }  // namespace aggt
 
-__global__ void __launch_bounds__(256) aggregate_tile_kernel(const float* __restrict__ vcl,
-                                                             const float* __restrict__ dists,
-                                                             const float* __restrict__ inds, Geo g, float scale,
-                                                             int tiles_x, int tiles_y, float* __restrict__ out) {
+__global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* __restrict__ vcl,
+                                                                  const float* __restrict__ dists,
+                                                                  const float* __restrict__ inds, Geo g,
+                                                                  float scale, int tiles_x, int tiles_y,
+                                                                  float* __restrict__ out) {
   using namespace aggt;
   __shared__ int4 rtap[MAXREC];     // fixed-point tap weights (0,0) (0,1) (1,0) (1,1)
   __shared__ int rcode[MAXREC];     // bin of tap (0,0); -1 nothing; -2 direct path
   __shared__ float qm[MAXQ], qinv[MAXQ];  // softmax max and 1/sum per covering query
   __shared__ int sstat[3 * NSLOT];  // per slot: sum of row offsets, of column offsets, count
   __shared__ int sbase[2 * NSLOT];  // per slot: box origin (row, column offset)
+  __shared__ int ndirect;           // records of the tile outside the bin boxes
   __shared__ int bins[WAVES][NSLOT * SB];
   __shared__ float obuf[WAVES][64][TX + 1];
 
@@ -352,11 +357,12 @@ __global__ void __launch_bounds__(256) aggregate_tile_kernel(const float* __rest
   const float sscale = (g.dist == SNLS_DIST_PROD ? 1.f : -1.f) * scale;
   const long long rowb = (((long long)b * g.HD + hd) * g.T + t) * g.nH;
 
-  for (int i = tid; i < WAVES * NSLOT * SB; i += 256) (&bins[0][0])[i] = 0;
+  for (int i = tid; i < WAVES * NSLOT * SB; i += NT) (&bins[0][0])[i] = 0;
   if (tid < 3 * NSLOT) sstat[tid] = 0;
+  if (tid == 0) ndirect = 0;
 
   // ---- phase 1a: softmax statistics of the covering queries ----
-  for (int j = tid; j < NQ; j += 256) {
+  for (int j = tid; j < NQ; j += NT) {
     const int h = hq0 + j / QX, w = wq0 + j % QX;
     float m = -INFINITY, z = 0.f;
     if (h >= 0 && h < g.H && w >= 0 && w < g.W) {
@@ -395,15 +401,40 @@ __global__ void __launch_bounds__(256) aggregate_tile_kernel(const float* __rest
   };
 
   // ---- phase 1b: mean offset per frame slot (centres the bin boxes) ----
-  for (int e = tid; e < NR; e += 256) {
-    float wl, ah, aw;
-    int t2, nh, nw;
-    neighbour(e, wl, t2, nh, nw, ah, aw);
-    const int slot = t2 - t + g.wt;
-    if (wl != 0.f && slot >= 0 && slot < nslot) {
-      atomicAdd(&sstat[slot], min(max(nh, -4096), 4096));
-      atomicAdd(&sstat[NSLOT + slot], min(max(nw, -4096), 4096));
-      atomicAdd(&sstat[2 * NSLOT + slot], 1);
+  // per-thread sums per slot, then wave sums and one LDS atomic per wave
+  {
+    int ssh[NSLOT], ssw[NSLOT], ssc[NSLOT];
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) ssh[s] = ssw[s] = ssc[s] = 0;
+    for (int e = tid; e < NR; e += NT) {
+      float wl, ah, aw;
+      int t2, nh, nw;
+      neighbour(e, wl, t2, nh, nw, ah, aw);
+      const int slot = t2 - t + g.wt;
+      if (wl != 0.f && slot >= 0 && slot < nslot) {
+        const int ch = min(max(nh, -4096), 4096), cw = min(max(nw, -4096), 4096);
+#pragma unroll
+        for (int s = 0; s < NSLOT; ++s)
+          if (slot == s) {
+            ssh[s] += ch;
+            ssw[s] += cw;
+            ssc[s] += 1;
+          }
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) {
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        ssh[s] += __shfl_xor(ssh[s], off);
+        ssw[s] += __shfl_xor(ssw[s], off);
+        ssc[s] += __shfl_xor(ssc[s], off);
+      }
+      if (lane == 0 && ssc[s] != 0) {
+        atomicAdd(&sstat[s], ssh[s]);
+        atomicAdd(&sstat[NSLOT + s], ssw[s]);
+        atomicAdd(&sstat[2 * NSLOT + s], ssc[s]);
+      }
     }
   }
   __syncthreads();
@@ -415,7 +446,7 @@ __global__ void __launch_bounds__(256) aggregate_tile_kernel(const float* __rest
   __syncthreads();
 
   // ---- phase 1c: records ----
-  for (int e = tid; e < NR; e += 256) {
+  for (int e = tid; e < NR; e += NT) {
     float wl, ah, aw;
     int t2, nh, nw;
     neighbour(e, wl, t2, nh, nw, ah, aw);
@@ -433,59 +464,85 @@ __global__ void __launch_bounds__(256) aggregate_tile_kernel(const float* __rest
     }
     rcode[e] = code;
     rtap[e] = tp;
+    const unsigned long long bd = __ballot(code == -2);
+    if (lane == 0 && bd) atomicAdd(&ndirect, __popcll(bd));
   }
   __syncthreads();
 
   // ---- phase 2: output row wv, pixel after pixel ----
+  // The bins of pixel x hold the fixed-point tap weights of the records of
+  // its P x P covering queries.  Pixel x + 1 is covered by the same queries
+  // except one query column leaving and one entering, and integer sums do
+  // not depend on the order, so the bins slide along the row: all P columns
+  // at the first pixel, then +1 column and -1 column per pixel.
   const int y = y0 + wv;
-  const int PPK = P * P * K;
-  const float inv_k = 1.f / (float)K, inv_p = 1.f / (float)P;
+  const int PK = P * K, PPK = P * P * K;
+  const float inv_k = 1.f / (float)K, inv_p = 1.f / (float)P, inv_pk = 1.f / (float)PK;
   const float* vb = vcl + (long long)b * g.T * g.HW * g.C + (long long)hd * g.Ch;
   const int cov_y = cover_count_1d(y, 1, g.nH, g.lo, P);
   unsigned slots = 0;  // slots with entries in the tile (wave-uniform)
   for (int s = 0; s < nslot; ++s)
     if (sstat[2 * NSLOT + s] != 0) slots |= 1u << s;
+  const bool any_direct = ndirect != 0;
   int* const wbins = bins[wv];
+  // add (sign +1) or remove (-1) the records of query columns c0 .. c0+nc-1
+  auto slide = [&](int c0, int nc, int sign) {
+    for (int e0 = 0; e0 < nc * PK; e0 += 64) {
+      const int e = e0 + lane;
+      const int cc = (int)(((float)e + 0.5f) * inv_pk);
+      const int rem = e - cc * PK;
+      const int qy = (int)(((float)rem + 0.5f) * inv_k);
+      const int l = rem - qy * K;
+      const int ri = ((wv + qy) * QX + c0 + cc) * K + l;
+      const int code = e < nc * PK ? rcode[ri] : -1;
+      if (code >= 0) {
+        const int4 tp = rtap[ri];
+        if (tp.x) atomicAdd(&wbins[code], sign * tp.x);
+        if (tp.y) atomicAdd(&wbins[code + 1], sign * tp.y);
+        if (tp.z) atomicAdd(&wbins[code + BOX], sign * tp.z);
+        if (tp.w) atomicAdd(&wbins[code + BOX + 1], sign * tp.w);
+      }
+    }
+  };
   for (int px = 0; px < TX; ++px) {
     const int x = x0 + px;
     if (y >= g.H || x >= g.W) break;  // wave-uniform
     float acc = 0.f;
-    for (int e0 = 0; e0 < PPK; e0 += 64) {
-      const int e = e0 + lane;
-      // covering query (qy, qx) of the pixel's P x P patch positions, neighbour l
-      const int jq = (int)(((float)e + 0.5f) * inv_k);
-      const int l = e - jq * K;
-      const int qy = (int)(((float)jq + 0.5f) * inv_p);
-      const int qx = jq - qy * P;
-      const int ri = ((wv + qy) * QX + px + qx) * K + l;
-      int code = -1;
-      if (e < PPK) code = rcode[ri];
-      if (code >= 0) {
-        const int4 tp = rtap[ri];
-        if (tp.x) atomicAdd(&wbins[code], tp.x);
-        if (tp.y) atomicAdd(&wbins[code + 1], tp.y);
-        if (tp.z) atomicAdd(&wbins[code + BOX], tp.z);
-        if (tp.w) atomicAdd(&wbins[code + BOX + 1], tp.w);
-      }
+    if (px == 0) {
+      slide(0, P, 1);
+    } else {
+      slide(px + P - 1, 1, 1);
+      slide(px - 1, 1, -1);
+    }
+    if (any_direct) {
       // neighbours outside the bin boxes: the whole wave reads their taps directly
-      unsigned long long om = __ballot(code == -2);
-      while (om) {
-        const int src = __ffsll((long long)om) - 1;
-        om &= om - 1;
-        const int e_ = __builtin_amdgcn_readlane(ri, src);
-        float wl, ah, aw;
-        int t2, nh, nw;
-        neighbour(e_, wl, t2, nh, nw, ah, aw);
-        const float* vf = vb + (long long)t2 * g.HW * g.C;
+      for (int e0 = 0; e0 < PPK; e0 += 64) {
+        const int e = e0 + lane;
+        const int jq = (int)(((float)e + 0.5f) * inv_k);
+        const int l = e - jq * K;
+        const int qy = (int)(((float)jq + 0.5f) * inv_p);
+        const int qx = jq - qy * P;
+        const int ri = ((wv + qy) * QX + px + qx) * K + l;
+        const int code = e < PPK ? rcode[ri] : -1;
+        unsigned long long om = __ballot(code == -2);
+        while (om) {
+          const int src = __ffsll((long long)om) - 1;
+          om &= om - 1;
+          const int e_ = __builtin_amdgcn_readlane(ri, src);
+          float wl, ah, aw;
+          int t2, nh, nw;
+          neighbour(e_, wl, t2, nh, nw, ah, aw);
+          const float* vf = vb + (long long)t2 * g.HW * g.C;
 #pragma unroll
-        for (int eh = 0; eh < 2; ++eh)
+          for (int eh = 0; eh < 2; ++eh)
 #pragma unroll
-          for (int ew = 0; ew < 2; ++ew) {
-            const int Y = y + nh + eh, X = x + nw + ew;
-            const float tw = wl * (eh ? ah : 1.f - ah) * (ew ? aw : 1.f - aw);
-            if (Y >= 0 && Y < g.H && X >= 0 && X < g.W && tw != 0.f && lane < g.Ch)
-              acc = fmaf(tw, vf[((long long)Y * g.W + X) * g.C + lane], acc);
-          }
+            for (int ew = 0; ew < 2; ++ew) {
+              const int Y = y + nh + eh, X = x + nw + ew;
+              const float tw = wl * (eh ? ah : 1.f - ah) * (ew ? aw : 1.f - aw);
+              if (Y >= 0 && Y < g.H && X >= 0 && X < g.W && tw != 0.f && lane < g.Ch)
+                acc = fmaf(tw, vf[((long long)Y * g.W + X) * g.C + lane], acc);
+            }
+        }
       }
     }
     wave_lds_sync();
@@ -493,7 +550,6 @@ __global__ void __launch_bounds__(256) aggregate_tile_kernel(const float* __rest
     for (int s = 0; s < nslot; ++s) {
       if (!(slots & (1u << s))) continue;
       const int v = wbins[s * SB + lane];
-      if (v != 0) wbins[s * SB + lane] = 0;
       const int Y = y + sbase[s] + (lane >> 3), X = x + sbase[NSLOT + s] + (lane & 7);
       const bool nz = v != 0 && Y >= 0 && Y < g.H && X >= 0 && X < g.W;
       const int off = ((t + s - g.wt) * (int)g.HW + Y * g.W + X) * g.C;
@@ -798,7 +854,7 @@ snls_status launch_aggregate(const float* v, const float* dists, const float* in
     const int tiles_x = (g.W + aggt::TX - 1) / aggt::TX, tiles_y = (g.H + aggt::TY - 1) / aggt::TY;
     const long long nwg = (long long)tiles_x * tiles_y * g.B * g.T * g.HD;
     if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
-    hipLaunchKernelGGL(aggregate_tile_kernel, dim3((unsigned)nwg), dim3(256), 0, s, vcl, dists, inds, g, scale,
+    hipLaunchKernelGGL(aggregate_tile_kernel, dim3((unsigned)nwg), dim3(aggt::NT), 0, s, vcl, dists, inds, g, scale,
                        tiles_x, tiles_y, out);
     return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
   }
