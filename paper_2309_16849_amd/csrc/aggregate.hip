@@ -322,6 +322,7 @@ constexpr int SB = BOX * BOX;        // bins per slot (one per lane)
 constexpr int MAXREC = 2048;         // (covering query, neighbour) records per tile
 constexpr int MAXQ = 256;            // covering queries per tile
 constexpr float QSCALE = 16777216.f; // fixed point 2^24
+static_assert(MAXREC <= WAVES * 64 * (TX + 1), "the covering queries' scores fit in the output buffer");
 }  // namespace aggt
 
 __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* __restrict__ vcl,
@@ -361,17 +362,22 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
   if (tid < 3 * NSLOT) sstat[tid] = 0;
   if (tid == 0) ndirect = 0;
 
-  // ---- phase 1a: softmax statistics of the covering queries ----
-  for (int j = tid; j < NQ; j += NT) {
+  // ---- phase 1a: scores of the covering queries (coalesced, into the
+  // output buffer, which phase 2 alone uses), softmax statistics ----
+  float* const dq = &obuf[0][0][0];
+  for (int e = tid; e < NR; e += NT) {
+    const int j = e / K, l = e - (e / K) * K;
     const int h = hq0 + j / QX, w = wq0 + j % QX;
+    dq[e] = (h >= 0 && h < g.H && w >= 0 && w < g.W) ? dists[((rowb + h) * g.nW + w) * K + l] : -INFINITY;
+  }
+  __syncthreads();
+  for (int j = tid; j < NQ; j += NT) {
+    const float* d = dq + j * K;
     float m = -INFINITY, z = 0.f;
-    if (h >= 0 && h < g.H && w >= 0 && w < g.W) {
-      const float* d = dists + ((rowb + h) * g.nW + w) * K;
-      for (int l = 0; l < K; ++l)
-        if (isfinite(d[l])) m = fmaxf(m, sscale * d[l]);
-      for (int l = 0; l < K; ++l)
-        if (isfinite(d[l])) z += expf(sscale * d[l] - m);
-    }
+    for (int l = 0; l < K; ++l)
+      if (isfinite(d[l])) m = fmaxf(m, sscale * d[l]);
+    for (int l = 0; l < K; ++l)
+      if (isfinite(d[l])) z += expf(sscale * d[l] - m);
     qm[j] = m;
     qinv[j] = z > 0.f ? 1.f / z : 0.f;
   }
@@ -379,13 +385,14 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
 
   // A neighbour's weight (0: contributes nothing) and its position; the
   // same tests as the softmax of the other aggregation kernels.
-  auto neighbour = [&](int e, float& wl, int& t2, int& nh, int& nw, float& ah, float& aw) {
+  // (score from LDS in phase 1, from global memory in phase 2)
+  auto neighbour = [&](int e, float& wl, int& t2, int& nh, int& nw, float& ah, float& aw, bool lds) {
     const int j = e / K, l = e - (e / K) * K;
     const int h = hq0 + j / QX, w = wq0 + j % QX;
     wl = 0.f;
     if (qinv[j] == 0.f) return;  // query outside the frame, or no finite score
     const long long row = (rowb + h) * g.nW + w;
-    const float d = dists[row * K + l];
+    const float d = lds ? dq[e] : dists[row * K + l];
     const float* ind = inds + (row * K + l) * 3;
     const float tf = ind[0], dh = ind[1], dw = ind[2];
     const bool ok = isfinite(d) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < 1.0e6f &&
@@ -409,8 +416,13 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
     for (int e = tid; e < NR; e += NT) {
       float wl, ah, aw;
       int t2, nh, nw;
-      neighbour(e, wl, t2, nh, nw, ah, aw);
+      neighbour(e, wl, t2, nh, nw, ah, aw, true);
       const int slot = t2 - t + g.wt;
+      // kept for phase 1c: weight, fractions, offsets (16 bits each: an
+      // offset beyond them is far outside every bin box), frame slot
+      const int ph = min(max(nh, -32768), 32767), pw = min(max(nw, -32768), 32767);
+      rtap[e] = make_int4(__float_as_int(wl), __float_as_int(ah), __float_as_int(aw), (ph & 0xffff) | (pw << 16));
+      rcode[e] = wl != 0.f ? slot : INT_MIN;
       if (wl != 0.f && slot >= 0 && slot < nslot) {
         const int ch = min(max(nh, -4096), 4096), cw = min(max(nw, -4096), 4096);
 #pragma unroll
@@ -447,13 +459,13 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
 
   // ---- phase 1c: records ----
   for (int e = tid; e < NR; e += NT) {
-    float wl, ah, aw;
-    int t2, nh, nw;
-    neighbour(e, wl, t2, nh, nw, ah, aw);
+    const int4 st = rtap[e];
+    const int slot = rcode[e];
     int code = -1;
     int4 tp = make_int4(0, 0, 0, 0);
-    if (wl != 0.f) {
-      const int slot = t2 - t + g.wt;
+    if (slot != INT_MIN) {
+      const float wl = __int_as_float(st.x), ah = __int_as_float(st.y), aw = __int_as_float(st.z);
+      const int nh = (st.w << 16) >> 16, nw = st.w >> 16;
       const int rh = slot >= 0 && slot < nslot ? nh - sbase[slot] : -1;
       const int rw = slot >= 0 && slot < nslot ? nw - sbase[NSLOT + slot] : -1;
       code = (rh >= 0 && rh < BOX - 1 && rw >= 0 && rw < BOX - 1) ? slot * SB + rh * BOX + rw : -2;
@@ -531,7 +543,7 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
           const int e_ = __builtin_amdgcn_readlane(ri, src);
           float wl, ah, aw;
           int t2, nh, nw;
-          neighbour(e_, wl, t2, nh, nw, ah, aw);
+          neighbour(e_, wl, t2, nh, nw, ah, aw, false);
           const float* vf = vb + (long long)t2 * g.HW * g.C;
 #pragma unroll
           for (int eh = 0; eh < 2; ++eh)
