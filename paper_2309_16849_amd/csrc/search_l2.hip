@@ -45,6 +45,7 @@ __global__ void __launch_bounds__(l2n::NT) l2_norms_kernel(const float* __restri
   __shared__ float reg[REGF];  // K region chunk; then the per-query |k~|^2 grids and column sums
   __shared__ int ubox[4];              // union: min row, max row, min col, max col (region origins)
   __shared__ int qoy[NQ], qox[NQ];     // query's grid origin inside the region
+  __shared__ int qay[NQ], qax[NQ];     // and in the frame (per-query blocks)
   __shared__ float qpart[NT];
 
   const int tid = threadIdx.x, jq = tid / TPQ, sub = tid % TPQ;
@@ -82,10 +83,12 @@ __global__ void __launch_bounds__(l2n::NT) l2_norms_kernel(const float* __restri
   __syncthreads();
   const int ry0 = ubox[0], rx0 = ubox[2];
   const int rh = ubox[1] - ry0 + E + 1, rw = ubox[3] - rx0 + E + 1;  // region extent (taps included)
-  const bool staged = ubox[1] >= ubox[0] && rh <= RH && rw <= RW;  // else read K from global memory
+  const bool staged = ubox[1] >= ubox[0] && rh <= RH && rw <= RW;  // else per-query blocks
   if (sub == 0) {
     qoy[jq] = oy - ry0;
     qox[jq] = ox - rx0;
+    qay[jq] = oy;
+    qax[jq] = ox;
   }
   const float ah = fh_u - flh, aw = fw_u - flw;
 
@@ -98,41 +101,54 @@ __global__ void __launch_bounds__(l2n::NT) l2_norms_kernel(const float* __restri
   auto kval = [&](int c, int y, int x) -> float {
     return (y >= 0 && y < g.H && x >= 0 && x < g.W) ? kb[(long long)c * g.HW + (long long)y * g.W + x] : 0.f;
   };
-  for (int c0 = 0; c0 < g.Ch; c0 += CC) {
-    const int nc = min(CC, g.Ch - c0);
+  // Thread sub owns grid columns sub and sub + TPQ (acc[2*zy + half] is row
+  // zy of column sub + TPQ*half) and walks down them, so the horizontal
+  // interpolation of a key row serves two grid rows.
+  static_assert(EG == 2 * TPQ && PPT == 2 * EG, "two grid columns per thread");
+  // The tile's key region is staged CC channels at a time when it fits;
+  // otherwise each query's own EG x EG block, one channel at a time.
+  const int xx = tid & 63;  // region staging: lane = column, waves = rows
+  const int cpc = staged ? CC : 1;
+  const int bpitch = staged ? RP : EG, cstr = staged ? RH * RP : 0;
+  const int qbase = staged ? qoy[jq] * RP + qox[jq] : jq * EG * EG;
+  static_assert(NQ * EG * EG <= CC * RH * RP, "per-query blocks fit in the region buffer");
+  for (int c0 = 0; c0 < g.Ch; c0 += cpc) {
+    const int nc = min(cpc, g.Ch - c0);
+    __syncthreads();  // previous chunk fully read
     if (staged) {
-      __syncthreads();  // previous chunk fully read
-      for (int e = tid; e < nc * rh * rw; e += NT) {
-        const int c = e / (rh * rw), rem = e - c * (rh * rw);
-        const int yy = rem / rw, xx = rem - yy * rw;
-        reg[(c * RH + yy) * RP + xx] = kval(c0 + c, ry0 + yy, rx0 + xx);
+      if (xx < rw)
+        for (int c = 0; c < nc; ++c) {
+#pragma unroll
+          for (int i = 0; i < RH / (NT / 64); ++i) {
+            const int yy = (tid >> 6) + (NT / 64) * i;
+            if (yy < rh) reg[(c * RH + yy) * RP + xx] = kval(c0 + c, ry0 + yy, rx0 + xx);
+          }
+        }
+    } else {
+      for (int e = tid; e < NQ * EG * EG; e += NT) {
+        const int jj = e / (EG * EG), rem = e % (EG * EG);
+        reg[e] = kval(c0, qay[jj] + rem / EG, qax[jj] + rem % EG);
       }
-      __syncthreads();
     }
+    __syncthreads();
     if (inside) {
       for (int c = 0; c < nc; ++c) {
+        const float* base = &reg[c * cstr + qbase];
 #pragma unroll
-        for (int i = 0; i < PPT; ++i) {
-          const int z = sub + TPQ * i, zy = z / EG, zx = z % EG;
-          if (zy < E && zx < E) {
-            float v00, v01, v10, v11;
-            if (staged) {
-              const float* rp = &reg[(c * RH + qoy[jq] + zy) * RP + qox[jq] + zx];
-              v00 = rp[0];
-              v01 = rp[1];
-              v10 = rp[RP];
-              v11 = rp[RP + 1];
-            } else {
-              const int y = oy + zy, x = ox + zx;
-              v00 = kval(c0 + c, y, x);
-              v01 = kval(c0 + c, y, x + 1);
-              v10 = kval(c0 + c, y + 1, x);
-              v11 = kval(c0 + c, y + 1, x + 1);
+        for (int half = 0; half < 2; ++half) {
+          const int zx = sub + TPQ * half;
+          if (zx < E) {
+            float h0 = (1.f - aw) * base[zx] + aw * base[zx + 1];
+#pragma unroll
+            for (int zy = 0; zy < EG - 1; ++zy) {
+              if (zy < E) {
+                const float* r1 = base + (zy + 1) * bpitch + zx;
+                const float h1 = (1.f - aw) * r1[0] + aw * r1[1];
+                const float kv = (1.f - ah) * h0 + ah * h1;
+                acc[2 * zy + half] = fmaf(kv, kv, acc[2 * zy + half]);
+                h0 = h1;
+              }
             }
-            const float top = (1.f - aw) * v00 + aw * v01;
-            const float bot = (1.f - aw) * v10 + aw * v11;
-            const float kv = (1.f - ah) * top + ah * bot;
-            acc[i] = fmaf(kv, kv, acc[i]);
           }
         }
       }
@@ -142,7 +158,7 @@ __global__ void __launch_bounds__(l2n::NT) l2_norms_kernel(const float* __restri
   __syncthreads();
   float* gq = &reg[jq * EG * EG];
 #pragma unroll
-  for (int i = 0; i < PPT; ++i) gq[sub + TPQ * i] = acc[i];  // zero for queries outside the frame
+  for (int i = 0; i < PPT; ++i) gq[(i >> 1) * EG + sub + TPQ * (i & 1)] = acc[i];  // zero outside the frame
   __syncthreads();
   // patch rows and columns whose query pixel is inside the frame
   const int ip0 = max(0, -h - g.lo), ip1 = min(g.ps - 1, g.H - 1 - h - g.lo);

@@ -303,6 +303,8 @@ L2_TILE_CASES = [
     (small_params(T=4, C=9, H=9, W=8, ws=8, wt=2, ps=6, k=13, dist_type=1), "frac"),
     (small_params(B=2, T=1, C=16, H=21, W=22, ws=9, wt=0, ps=4, k=12, dist_type=1), "frac"),
     (small_params(T=3, C=70, H=19, W=26, ws=9, wt=1, ps=2, k=10, dist_type=1), "smooth"),
+    (small_params(T=3, C=16, H=21, W=26, ws=9, wt=1, ps=7, k=10, dist_type=1), "edge"),
+    (small_params(T=3, C=16, H=25, W=30, ws=9, wt=1, ps=7, k=10, dist_type=1), "far"),
 ]
 
 
