@@ -116,13 +116,21 @@ __global__ void __launch_bounds__(l2n::NT) l2_norms_kernel(const float* __restri
     const int nc = min(cpc, g.Ch - c0);
     __syncthreads();  // previous chunk fully read
     if (staged) {
-      if (xx < rw)
-        for (int c = 0; c < nc; ++c) {
+      // the whole chunk's loads in flight before the LDS stores
+      float st[CC][RH / (NT / 64)];
 #pragma unroll
-          for (int i = 0; i < RH / (NT / 64); ++i) {
-            const int yy = (tid >> 6) + (NT / 64) * i;
-            if (yy < rh) reg[(c * RH + yy) * RP + xx] = kval(c0 + c, ry0 + yy, rx0 + xx);
-          }
+      for (int c = 0; c < CC; ++c)
+#pragma unroll
+        for (int i = 0; i < RH / (NT / 64); ++i) {
+          const int yy = (tid >> 6) + (NT / 64) * i;
+          st[c][i] = (xx < rw && yy < rh && c < nc) ? kval(c0 + c, ry0 + yy, rx0 + xx) : 0.f;
+        }
+#pragma unroll
+      for (int c = 0; c < CC; ++c)
+#pragma unroll
+        for (int i = 0; i < RH / (NT / 64); ++i) {
+          const int yy = (tid >> 6) + (NT / 64) * i;
+          if (xx < rw && yy < rh && c < nc) reg[(c * RH + yy) * RP + xx] = st[c][i];
         }
     } else {
       for (int e = tid; e < NQ * EG * EG; e += NT) {
