@@ -290,6 +290,225 @@ __global__ void __launch_bounds__(256) backward_search_kernel(const float* __res
   }
 }
 
+// ---- merged scatters (P <= 7, at most 64 channels per head) ----
+//
+// For one neighbour l of a row, the taps of the P x P patch pixels cover a
+// (P+1) x (P+1) block of key positions at the neighbour's integer offset;
+// each lane (channel) sums the block in registers and adds it with (P+1)^2
+// atomics instead of 4 P^2.  dQ of a patch pixel sums over all k neighbours
+// of the row and is added once per pixel.
+template <int P>
+__global__ void __launch_bounds__(256) backward_agg_block_kernel(const float* __restrict__ vcl,
+                                                                 const float* __restrict__ dists,
+                                                                 const float* __restrict__ inds,
+                                                                 const float* __restrict__ gocl, Geo g,
+                                                                 float scale, float* __restrict__ dvcl,
+                                                                 float* __restrict__ grad_flows,
+                                                                 float* __restrict__ Gws) {
+  constexpr int PB = P + 1;
+  const int lane = threadIdx.x & 63;
+  const long long row = (long long)blockIdx.x * bwd::WAVES + (threadIdx.x >> 6);
+  if (row >= g.rows) return;  // whole wave
+  const RowPos rp = row_pos(row, g);
+  const float* drow = dists + row * g.k;
+  const float* irow = inds + row * g.k * 3;
+  const float sscale = (g.dist == SNLS_DIST_PROD ? 1.f : -1.f) * scale;
+  float m, z;
+  softmax_stats(drow, g.k, sscale, lane, &m, &z);
+  const long long qbase = ((long long)rp.b * g.T + rp.t) * g.HW;
+  const int cc = rp.hd * g.Ch + lane;
+  const bool act = lane < g.Ch;
+  const int lo = -(P / 2);
+  // g~ = grad_out / count of the patch pixels (0 outside the frame)
+  float gg[P * P];
+#pragma unroll
+  for (int ph = 0; ph < P; ++ph)
+#pragma unroll
+    for (int pw = 0; pw < P; ++pw) {
+      const int y = rp.h + lo + ph, x = rp.w + lo + pw;
+      float v = 0.f;
+      if (act && y >= 0 && y < g.H && x >= 0 && x < g.W) {
+        const float inv =
+            1.f / (float)(cover_count_1d(y, g.s0, g.nH, lo, P) * cover_count_1d(x, g.s0, g.nW, lo, P));
+        v = gocl[(qbase + (long long)y * g.W + x) * g.C + cc] * inv;
+      }
+      gg[ph * P + pw] = v;
+    }
+  for (int l = 0; l < g.k; ++l) {
+    int t2, ny, nx;
+    float ay, ax;
+    if (!isfinite(drow[l]) || !(z > 0.f) || !neighbour(irow, l, g, &t2, &ny, &nx, &ay, &ax)) {
+      if (lane == 0) Gws[row * g.k + l] = 0.f;
+      continue;
+    }
+    const float wl = expf(sscale * drow[l] - m) / z;
+    const float* vf = vcl + ((long long)rp.b * g.T + t2) * g.HW * g.C + cc;
+    const int Y0 = rp.h + lo + ny, X0 = rp.w + lo + nx;  // block origin
+    // the block of V values (0 outside the frame)
+    float vb[PB * PB];
+#pragma unroll
+    for (int a = 0; a < PB; ++a)
+#pragma unroll
+      for (int c = 0; c < PB; ++c) {
+        const int Y = Y0 + a, X = X0 + c;
+        vb[a * PB + c] = act && Y >= 0 && Y < g.H && X >= 0 && X < g.W ? vf[((long long)Y * g.W + X) * g.C] : 0.f;
+      }
+    const float w00 = (1.f - ay) * (1.f - ax), w01 = (1.f - ay) * ax, w10 = ay * (1.f - ax), w11 = ay * ax;
+    float Gl = 0.f, fh = 0.f, fw = 0.f;
+    float blk[PB * PB];
+#pragma unroll
+    for (int i = 0; i < PB * PB; ++i) blk[i] = 0.f;
+#pragma unroll
+    for (int ph = 0; ph < P; ++ph)
+#pragma unroll
+      for (int pw = 0; pw < P; ++pw) {
+        const float gv = gg[ph * P + pw];
+        const float v00 = vb[ph * PB + pw], v01 = vb[ph * PB + pw + 1];
+        const float v10 = vb[(ph + 1) * PB + pw], v11 = vb[(ph + 1) * PB + pw + 1];
+        const float val = w00 * v00 + w01 * v01 + w10 * v10 + w11 * v11;
+        Gl = fmaf(gv, val, Gl);
+        fh = fmaf(gv, (1.f - ax) * (v10 - v00) + ax * (v11 - v01), fh);
+        fw = fmaf(gv, (1.f - ay) * (v01 - v00) + ay * (v11 - v10), fw);
+        const float sv = wl * gv;
+        blk[ph * PB + pw] = fmaf(w00, sv, blk[ph * PB + pw]);
+        blk[ph * PB + pw + 1] = fmaf(w01, sv, blk[ph * PB + pw + 1]);
+        blk[(ph + 1) * PB + pw] = fmaf(w10, sv, blk[(ph + 1) * PB + pw]);
+        blk[(ph + 1) * PB + pw + 1] = fmaf(w11, sv, blk[(ph + 1) * PB + pw + 1]);
+      }
+    float* dvf = dvcl + ((long long)rp.b * g.T + t2) * g.HW * g.C + cc;
+#pragma unroll
+    for (int a = 0; a < PB; ++a)
+#pragma unroll
+      for (int c = 0; c < PB; ++c) {
+        const int Y = Y0 + a, X = X0 + c;
+        if (act && Y >= 0 && Y < g.H && X >= 0 && X < g.W && blk[a * PB + c] != 0.f)
+          atomicAdd(dvf + ((long long)Y * g.W + X) * g.C, blk[a * PB + c]);
+      }
+    Gl = wave_sum(Gl);
+    fh = wave_sum(fh);
+    fw = wave_sum(fw);
+    if (lane == 0) {
+      Gws[row * g.k + l] = Gl;
+      add_flow_grad(grad_flows, g, rp, t2, wl * fh, wl * fw);
+    }
+  }
+}
+
+template <int P>
+__global__ void __launch_bounds__(256) backward_search_block_kernel(const float* __restrict__ qcl,
+                                                                    const float* __restrict__ kcl,
+                                                                    const float* __restrict__ dists,
+                                                                    const float* __restrict__ inds,
+                                                                    const float* __restrict__ grad_dists, Geo g,
+                                                                    float scale, const float* __restrict__ Gws,
+                                                                    float* __restrict__ dqcl,
+                                                                    float* __restrict__ dkcl,
+                                                                    float* __restrict__ grad_flows) {
+  constexpr int PB = P + 1;
+  const int lane = threadIdx.x & 63;
+  const long long row = (long long)blockIdx.x * bwd::WAVES + (threadIdx.x >> 6);
+  if (row >= g.rows) return;  // whole wave
+  const RowPos rp = row_pos(row, g);
+  const float* drow = dists + row * g.k;
+  const float* irow = inds + row * g.k * 3;
+  const float* Grow = Gws + row * g.k;
+  const bool ip = g.dist == SNLS_DIST_PROD;
+  const float sscale = (ip ? 1.f : -1.f) * scale;
+  float m, z;
+  softmax_stats(drow, g.k, sscale, lane, &m, &z);
+  float wg = 0.f;
+  if (z > 0.f)
+    for (int l = lane; l < g.k; l += 64)
+      if (isfinite(drow[l])) wg += expf(sscale * drow[l] - m) / z * Grow[l];
+  wg = wave_sum(wg);
+  const long long qbase = ((long long)rp.b * g.T + rp.t) * g.HW;
+  const int cc = rp.hd * g.Ch + lane;
+  const bool act = lane < g.Ch;
+  const int lo = -(P / 2);
+  float qv[P * P], dq[P * P];
+#pragma unroll
+  for (int ph = 0; ph < P; ++ph)
+#pragma unroll
+    for (int pw = 0; pw < P; ++pw) {
+      const int y = rp.h + lo + ph, x = rp.w + lo + pw;
+      const bool in = act && y >= 0 && y < g.H && x >= 0 && x < g.W;
+      qv[ph * P + pw] = in ? qcl[(qbase + (long long)y * g.W + x) * g.C + cc] : 0.f;
+      dq[ph * P + pw] = 0.f;
+    }
+  for (int l = 0; l < g.k; ++l) {
+    int t2, ny, nx;
+    float ay, ax;
+    if (!isfinite(drow[l]) || !neighbour(irow, l, g, &t2, &ny, &nx, &ay, &ax)) continue;
+    float dd = 0.f;
+    if (z > 0.f) dd = sscale * (expf(sscale * drow[l] - m) / z) * (Grow[l] - wg);
+    if (grad_dists) dd += grad_dists[row * g.k + l];
+    if (dd == 0.f) continue;
+    const float* kf = kcl + ((long long)rp.b * g.T + t2) * g.HW * g.C + cc;
+    const int Y0 = rp.h + lo + ny, X0 = rp.w + lo + nx;
+    float kb[PB * PB];
+#pragma unroll
+    for (int a = 0; a < PB; ++a)
+#pragma unroll
+      for (int c = 0; c < PB; ++c) {
+        const int Y = Y0 + a, X = X0 + c;
+        kb[a * PB + c] = act && Y >= 0 && Y < g.H && X >= 0 && X < g.W ? kf[((long long)Y * g.W + X) * g.C] : 0.f;
+      }
+    const float w00 = (1.f - ay) * (1.f - ax), w01 = (1.f - ay) * ax, w10 = ay * (1.f - ax), w11 = ay * ax;
+    float fh = 0.f, fw = 0.f;
+    float blk[PB * PB];
+#pragma unroll
+    for (int i = 0; i < PB * PB; ++i) blk[i] = 0.f;
+#pragma unroll
+    for (int ph = 0; ph < P; ++ph) {
+      const int y = rp.h + lo + ph;
+#pragma unroll
+      for (int pw = 0; pw < P; ++pw) {
+        const int x = rp.w + lo + pw;
+        if (y < 0 || y >= g.H || x < 0 || x >= g.W) continue;  // patch pixels outside the frame
+        const float k00 = kb[ph * PB + pw], k01 = kb[ph * PB + pw + 1];
+        const float k10 = kb[(ph + 1) * PB + pw], k11 = kb[(ph + 1) * PB + pw + 1];
+        const float kv = w00 * k00 + w01 * k01 + w10 * k10 + w11 * k11;
+        const float q = qv[ph * P + pw];
+        float dqv, dk;
+        if (ip) {
+          dqv = dd * kv;
+          dk = dd * q;
+        } else {
+          dqv = 2.f * dd * (q - kv);
+          dk = -dqv;
+        }
+        dq[ph * P + pw] += dqv;
+        blk[ph * PB + pw] = fmaf(w00, dk, blk[ph * PB + pw]);
+        blk[ph * PB + pw + 1] = fmaf(w01, dk, blk[ph * PB + pw + 1]);
+        blk[(ph + 1) * PB + pw] = fmaf(w10, dk, blk[(ph + 1) * PB + pw]);
+        blk[(ph + 1) * PB + pw + 1] = fmaf(w11, dk, blk[(ph + 1) * PB + pw + 1]);
+        fh = fmaf(dk, (1.f - ax) * (k10 - k00) + ax * (k11 - k01), fh);
+        fw = fmaf(dk, (1.f - ay) * (k01 - k00) + ay * (k11 - k10), fw);
+      }
+    }
+    float* dkf = dkcl + ((long long)rp.b * g.T + t2) * g.HW * g.C + cc;
+#pragma unroll
+    for (int a = 0; a < PB; ++a)
+#pragma unroll
+      for (int c = 0; c < PB; ++c) {
+        const int Y = Y0 + a, X = X0 + c;
+        if (act && Y >= 0 && Y < g.H && X >= 0 && X < g.W && blk[a * PB + c] != 0.f)
+          atomicAdd(dkf + ((long long)Y * g.W + X) * g.C, blk[a * PB + c]);
+      }
+    fh = wave_sum(fh);
+    fw = wave_sum(fw);
+    if (lane == 0) add_flow_grad(grad_flows, g, rp, t2, fh, fw);
+  }
+#pragma unroll
+  for (int ph = 0; ph < P; ++ph)
+#pragma unroll
+    for (int pw = 0; pw < P; ++pw) {
+      const int y = rp.h + lo + ph, x = rp.w + lo + pw;
+      if (act && y >= 0 && y < g.H && x >= 0 && x < g.W && dq[ph * P + pw] != 0.f)
+        atomicAdd(dqcl + (qbase + (long long)y * g.W + x) * g.C + cc, dq[ph * P + pw]);
+    }
+}
+
 // Workspace: G (rows x k), channels-last copies of q, k, v and grad_out, and
 // channels-last accumulators of dq, dk and dv (256-byte aligned pieces).
 static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
@@ -335,10 +554,31 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
   }
   if (g.rows > 0) {
     const unsigned blocks = (unsigned)((g.rows + bwd::WAVES - 1) / bwd::WAVES);
-    hipLaunchKernelGGL(backward_agg_kernel, dim3(blocks), dim3(64 * bwd::WAVES), 0, s, vcl, dists, inds, gocl, g,
-                       scale, dvcl, grad_flows, Gws);
-    hipLaunchKernelGGL(backward_search_kernel, dim3(blocks), dim3(64 * bwd::WAVES), 0, s, qcl, kcl, dists, inds,
-                       grad_dists, g, scale, Gws, dqcl, dkcl, grad_flows);
+    const dim3 grid(blocks), block(64 * bwd::WAVES);
+    if (g.ps <= 7 && g.Ch <= 64) {
+      switch (g.ps) {
+#define SNLS_BWD_CASE(P)                                                                                        \
+  case P:                                                                                                       \
+    hipLaunchKernelGGL(backward_agg_block_kernel<P>, grid, block, 0, s, vcl, dists, inds, gocl, g, scale, dvcl, \
+                       grad_flows, Gws);                                                                        \
+    hipLaunchKernelGGL(backward_search_block_kernel<P>, grid, block, 0, s, qcl, kcl, dists, inds, grad_dists, g, \
+                       scale, Gws, dqcl, dkcl, grad_flows);                                                     \
+    break;
+        SNLS_BWD_CASE(1)
+        SNLS_BWD_CASE(2)
+        SNLS_BWD_CASE(3)
+        SNLS_BWD_CASE(4)
+        SNLS_BWD_CASE(5)
+        SNLS_BWD_CASE(6)
+        SNLS_BWD_CASE(7)
+#undef SNLS_BWD_CASE
+      }
+    } else {
+      hipLaunchKernelGGL(backward_agg_kernel, grid, block, 0, s, vcl, dists, inds, gocl, g, scale, dvcl, grad_flows,
+                         Gws);
+      hipLaunchKernelGGL(backward_search_kernel, grid, block, 0, s, qcl, kcl, dists, inds, grad_dists, g, scale,
+                         Gws, dqcl, dkcl, grad_flows);
+    }
   }
   if (nvid > 0) {
     dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));

@@ -609,8 +609,11 @@ def test_backward_matches_oracle(dev):
 
 @pytest.mark.parametrize("kw", [dict(dist_type=1, ps=3, ws=5, k=6), dict(HD=2, C=40, ps=5, ws=5, k=5),
                                 dict(C=96, ps=3, ws=3, k=4, H=17, W=19), dict(stride0=2, ps=1, ws=7, k=9, HD=4, C=16),
-                                dict(stride0=2, ps=3, ws=5, k=7, dist_type=1, wt=2, T=5)],
-                         ids=["l2", "heads", "c96", "p1-s2", "l2-s2"])
+                                dict(stride0=2, ps=3, ws=5, k=7, dist_type=1, wt=2, T=5),
+                                dict(ps=7, ws=9, k=10, C=32, H=23, W=26), dict(ps=2, ws=4, k=6, C=8),
+                                dict(ps=4, ws=5, k=8, HD=2, C=16, stride0=2), dict(ps=6, ws=3, k=5, C=64, H=19, W=21),
+                                dict(ps=5, ws=5, k=12, C=24, dist_type=1)],
+                         ids=["l2", "heads", "c96", "p1-s2", "l2-s2", "p7", "p2", "p4-s2", "p6", "p5-l2"])
 def test_backward_shapes(dev, kw):
     """Gradients against the oracle over distances, heads, channel counts
     above one wave and query strides."""
