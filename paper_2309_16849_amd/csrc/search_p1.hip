@@ -90,11 +90,23 @@ __global__ void __launch_bounds__(p1::NT, 8) search_p1_scores_kernel(const float
     x0q[j] = x0;
   }
   __syncthreads();
-  if (rowtask) {
-    atomicMin(&ubox[0], y0);
-    atomicMax(&ubox[1], y0);
-    atomicMin(&ubox[2], x0);
-    atomicMax(&ubox[3], x0);
+  {
+    // union bounds: wave reductions, then one LDS atomic per wave
+    int a0 = rowtask ? y0 : INT_MAX, a1 = rowtask ? y0 : INT_MIN;
+    int a2 = rowtask ? x0 : INT_MAX, a3 = rowtask ? x0 : INT_MIN;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      a0 = min(a0, __shfl_xor(a0, off));
+      a1 = max(a1, __shfl_xor(a1, off));
+      a2 = min(a2, __shfl_xor(a2, off));
+      a3 = max(a3, __shfl_xor(a3, off));
+    }
+    if ((tid & 63) == 0 && a0 <= a1) {
+      atomicMin(&ubox[0], a0);
+      atomicMax(&ubox[1], a1);
+      atomicMin(&ubox[2], a2);
+      atomicMax(&ubox[3], a3);
+    }
   }
   __syncthreads();
   const int ry0 = ubox[0], rx0 = ubox[2];
@@ -114,16 +126,33 @@ __global__ void __launch_bounds__(p1::NT, 8) search_p1_scores_kernel(const float
   // rows (NRI rows each); a chunk's loads are issued before the products of
   // the previous chunk and written to LDS after them.
   const int xx = tid & 63;
+  // Branch-free region loads: a raw buffer load at an offset past the
+  // buffer's extent reads 0 (pixels outside the frame, channels past the
+  // head).  Offsets stay below 2^31: p1_supported requires Ch*H*W*4 < 2^31.
+  constexpr unsigned OOB = 0x80000000u;
+  const __amdgpu_buffer_rsrc_t k_rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)kb, (short)0, (int)(g.Ch * g.HW * 4), 0x00020000);
+  unsigned roff[NRI];  // byte offset of this thread's region pixels in channel 0 (OOB: none)
+#pragma unroll
+  for (int i = 0; i < NRI; ++i) {
+    const int yy = (tid >> 6) + (NT / 64) * i;
+    const int y = ry0 + yy, x = rx0 + xx;
+    roff[i] = (staged && xx < rw && yy < rh && y >= 0 && y < g.H && x >= 0 && x < g.W) ? (unsigned)((y * g.W + x) * 4)
+                                                                                        : OOB;
+  }
   float stg[CC][NRI];
   float qstg = 0.f;
   auto load_chunk = [&](int c0) {
 #pragma unroll
-    for (int c = 0; c < CC; ++c)
+    for (int c = 0; c < CC; ++c) {
+      const unsigned coff = (unsigned)(c0 + c) * (unsigned)g.HW * 4u;
+      const bool cin = c0 + c < g.Ch;
 #pragma unroll
       for (int i = 0; i < NRI; ++i) {
-        const int yy = (tid >> 6) + (NT / 64) * i;
-        stg[c][i] = (xx < rw && yy < rh && c0 + c < g.Ch) ? kval(c0 + c, ry0 + yy, rx0 + xx) : 0.f;
+        const unsigned off = (roff[i] != OOB && cin) ? roff[i] + coff : OOB;
+        stg[c][i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(k_rs, off, 0, 0));
       }
+    }
     if (tid < CC * NQ) {
       const int c = tid / NQ, jj = tid % NQ;
       const int qh = (ty * TQ + jj / TQ) * g.s0, qw = (tx * TQ + jj % TQ) * g.s0;
@@ -132,13 +161,13 @@ __global__ void __launch_bounds__(p1::NT, 8) search_p1_scores_kernel(const float
     }
   };
   auto store_chunk = [&](int buf) {
+    // rows past the region and columns up to the pitch receive zeros that are never read
+    if (xx < RP) {
 #pragma unroll
-    for (int c = 0; c < CC; ++c)
+      for (int c = 0; c < CC; ++c)
 #pragma unroll
-      for (int i = 0; i < NRI; ++i) {
-        const int yy = (tid >> 6) + (NT / 64) * i;
-        if (xx < rw && yy < rh) reg[buf][(c * RH + yy) * RP + xx] = stg[c][i];
-      }
+        for (int i = 0; i < NRI; ++i) reg[buf][(c * RH + (tid >> 6) + (NT / 64) * i) * RP + xx] = stg[c][i];
+    }
     if (tid < CC * NQ) qs[buf][tid / NQ][tid % NQ] = qstg;
   };
   // Per-query blocks (windows far apart): one channel at a time.
@@ -155,7 +184,6 @@ __global__ void __launch_bounds__(p1::NT, 8) search_p1_scores_kernel(const float
   };
   // this thread's row in the staging buffer
   const int toff = staged ? (y0 - ry0) * RP + (x0 - rx0) : j * QB + (y0 - y0q[j]) * NC;
-  const int cstride = staged ? RH * RP : 0;  // channel stride
 
   float cr[NC];  // correlations of key row y0, columns x0 ..
 #pragma unroll
@@ -176,10 +204,19 @@ __global__ void __launch_bounds__(p1::NT, 8) search_p1_scores_kernel(const float
       __syncthreads();
     }
     if (rowtask) {
-      const float* base = staged ? reg[buf] : &reg[0][0];
-      for (int c = 0; c < cpc && c0 + c < g.Ch; ++c) {
-        const float qv = qs[buf][c][j];
-        const float* r0 = base + c * cstride + toff;
+      if (staged) {
+#pragma unroll
+        for (int c = 0; c < CC; ++c) {
+          if (c0 + c < g.Ch) {
+            const float qv = qs[buf][c][j];
+            const float* r0 = reg[buf] + c * (RH * RP) + toff;
+#pragma unroll
+            for (int x = 0; x < NC; ++x) cr[x] = fmaf(qv, r0[x], cr[x]);
+          }
+        }
+      } else {
+        const float qv = qs[0][0][j];
+        const float* r0 = &reg[0][0] + toff;
 #pragma unroll
         for (int x = 0; x < NC; ++x) cr[x] = fmaf(qv, r0[x], cr[x]);
       }
