@@ -60,7 +60,6 @@ constexpr int MAXBLK = 5;               // shift-column blocks: union width <= 3
 constexpr int WSMAX = 9;
 constexpr int WP = WSMAX + 2;           // window-table pitch (shifts floor(disp_0) .. floor(disp_last) + 1)
 constexpr int WIN = WP * WP;
-constexpr int WSQ = WSMAX * WSMAX;      // candidates per query and frame
 
 // Staging buffers (double-buffered chunks of CC channels).
 constexpr int KST_F = (CC * KR * KP + 63) / 64 * 64;     // 6528 floats
