@@ -436,12 +436,15 @@ def test_aggregate_stacked(dev, ps, stride0, HD, k, C):
 
 # --------------------------------------------------- non-finite inputs --
 
-@pytest.mark.parametrize("dist_type,ps,ws", [(0, 3, 5), (0, 7, 9), (1, 3, 5), (0, 4, 8)])
-def test_nan_features_match_oracle(dev, dist_type, ps, ws):
+@pytest.mark.parametrize("dist_type,ps,ws,k,stride0", [(0, 3, 5, 10, 1), (0, 7, 9, 10, 1), (1, 3, 5, 10, 1),
+                                                       (0, 4, 8, 10, 1), (0, 7, 9, 20, 1), (0, 1, 9, 20, 2),
+                                                       (0, 1, 15, 30, 2), (1, 5, 7, 24, 1)])
+def test_nan_features_match_oracle(dev, dist_type, ps, ws, k, stride0):
     """NaN feature values away from the borders: every candidate whose patch
     reads one is invalid (a NaN similarity ranks as an invalid candidate), as
-    in the oracle; both the tiled and the direct kernels."""
-    p = small_params(T=3, C=8, H=40, W=42, ws=ws, wt=1, ps=ps, k=10, dist_type=dist_type)
+    in the oracle; the tiled, single-pixel and direct kernels, and both top-k
+    kernels."""
+    p = small_params(T=3, C=8, H=40, W=42, ws=ws, wt=1, ps=ps, k=k, stride0=stride0, dist_type=dist_type)
     r = np.random.default_rng(8100 + ps)
     q, k, v, flows = _inputs(p, 8200 + ps)
     m = ws // 2 + 6
@@ -457,12 +460,13 @@ def test_nan_features_match_oracle(dev, dist_type, ps, ws):
     compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
 
 
-@pytest.mark.parametrize("dist_type,ps,ws,stride0", [(0, 7, 9, 1), (0, 3, 5, 1), (1, 3, 5, 2)])
-def test_nonfinite_inputs_stay_in_bounds(dev, dist_type, ps, ws, stride0):
+@pytest.mark.parametrize("dist_type,ps,ws,stride0,k", [(0, 7, 9, 1, 12), (0, 3, 5, 1, 12), (1, 3, 5, 2, 12),
+                                                       (0, 1, 15, 2, 30), (0, 7, 9, 1, 20)])
+def test_nonfinite_inputs_stay_in_bounds(dev, dist_type, ps, ws, stride0, k):
     """NaN and +-inf anywhere in q, k and the flows (scores are then not
     specified): no NaN score is kept, and every kept neighbour is a distinct
     candidate of the query's own window."""
-    p = small_params(T=4, C=8, H=23, W=30, ws=ws, wt=2, ps=ps, k=12, stride0=stride0, dist_type=dist_type)
+    p = small_params(T=4, C=8, H=23, W=30, ws=ws, wt=2, ps=ps, k=k, stride0=stride0, dist_type=dist_type)
     r = np.random.default_rng(8300 + ps + stride0)
     q, k, v, flows = _inputs(p, 8400 + ps)
     for arr in (q, k, flows):
