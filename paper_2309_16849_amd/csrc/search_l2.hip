@@ -15,6 +15,18 @@
 // the frame.  (Per-cell fractions of fl32(F + d - r) can differ from a by
 // rounding in the last bit; the effect on G is far below the fp32 score
 // tolerance, and the positions reported come from the exact per-cell values.)
+//
+// |k~|^2 of a bilinear read with taps v_e and weights w_e expands into
+//     sum_e w_e^2 |v_e|^2 + 2 sum_{e<e'} w_e w_e' <v_e, v_e'>,
+// and the channel sums |v|^2 and <v, v'> of neighbouring key pixels do not
+// depend on the query.  A first kernel computes, per key pixel (y, x) of
+// every frame and head, five pair planes over the head's channels:
+//   N = |k(y,x)|^2, R = <k(y,x), k(y,x+1)>, D = <k(y,x), k(y+1,x)>,
+//   X = <k(y,x), k(y+1,x+1)>, A = <k(y,x+1), k(y+1,x)>
+// (pixels outside the frame read 0), so each position costs ten products of
+// plane values with the query's weights instead of four taps per channel.
+// Every term reads only planes of the position's own four taps, so a
+// non-finite key value reaches exactly the positions whose taps read it.
 #include "snls_internal.h"
 
 namespace snls {
@@ -35,14 +47,49 @@ constexpr int VSUM = NQ * WSMAX * EG;  // per-query column sums
 constexpr int REGF = CC * RH * RP > GRIDS + VSUM ? CC * RH * RP : GRIDS + VSUM;
 }  // namespace l2n
 
+constexpr int NPLANE = 5;  // N, R, D, X, A
+
+// Pair planes of one (b, t, head): one thread per key pixel.  Layout
+// planes[((b*T + t)*HD + hd)*5 + m][H][W].
+__global__ void __launch_bounds__(256) l2_pair_planes_kernel(const float* __restrict__ k, Geo g,
+                                                             float* __restrict__ planes) {
+  const long long slab = blockIdx.y;  // (b*T + t)*HD + hd
+  const long long pix = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (pix >= g.HW) return;
+  const int hd = (int)(slab % g.HD);
+  const long long bt = slab / g.HD;
+  const int y = (int)(pix / g.W), x = (int)(pix % g.W);
+  const bool rin = x + 1 < g.W, din = y + 1 < g.H;
+  const float* kb = k + (bt * g.C + (long long)hd * g.Ch) * g.HW + pix;
+  float n = 0.f, r = 0.f, d = 0.f, xx = 0.f, a = 0.f;
+  for (int c = 0; c < g.Ch; ++c, kb += g.HW) {
+    const float v00 = kb[0];
+    const float v01 = rin ? kb[1] : 0.f;
+    const float v10 = din ? kb[g.W] : 0.f;
+    const float v11 = rin && din ? kb[g.W + 1] : 0.f;
+    n = fmaf(v00, v00, n);
+    r = fmaf(v00, v01, r);
+    d = fmaf(v00, v10, d);
+    xx = fmaf(v00, v11, xx);
+    a = fmaf(v01, v10, a);
+  }
+  float* out = planes + slab * NPLANE * g.HW + pix;
+  out[0] = n;
+  out[g.HW] = r;
+  out[2 * g.HW] = d;
+  out[3 * g.HW] = xx;
+  out[4 * g.HW] = a;
+}
+
 // One workgroup = a TY x TX tile of queries of one (b, head, t) and one
 // frame step dt (grid z = dt + wt).
-__global__ void __launch_bounds__(l2n::NT) l2_norms_kernel(const float* __restrict__ q, const float* __restrict__ k,
+__global__ void __launch_bounds__(l2n::NT, 3) l2_norms_kernel(const float* __restrict__ q,
+                                                          const float* __restrict__ planes,
                                                           const float* __restrict__ flows, Geo g, int tiles_x,
                                                           float* __restrict__ G, int pitch,
                                                           float* __restrict__ Qn) {
   using namespace l2n;
-  __shared__ float reg[REGF];  // K region chunk; then the per-query |k~|^2 grids and column sums
+  __shared__ float reg[REGF];  // pair-plane region; then the per-query |k~|^2 grids and column sums
   __shared__ int ubox[4];              // union: min row, max row, min col, max col (region origins)
   __shared__ int qoy[NQ], qox[NQ];     // query's grid origin inside the region
   __shared__ int qay[NQ], qax[NQ];     // and in the frame (per-query blocks)
@@ -92,71 +139,93 @@ __global__ void __launch_bounds__(l2n::NT) l2_norms_kernel(const float* __restri
   }
   const float ah = fh_u - flh, aw = fw_u - flw;
 
-  const float* kb = k + (((long long)b * g.T + t2) * g.C + (long long)hd * g.Ch) * g.HW;
+  const float* kb = planes + (((long long)b * g.T + t2) * g.HD + hd) * NPLANE * g.HW;
   float acc[PPT];
 #pragma unroll
   for (int i = 0; i < PPT; ++i) acc[i] = 0.f;
 
-  // key value at (y, x) of channel plane c: 0 outside the frame
-  auto kval = [&](int c, int y, int x) -> float {
-    return (y >= 0 && y < g.H && x >= 0 && x < g.W) ? kb[(long long)c * g.HW + (long long)y * g.W + x] : 0.f;
+  // value of pair plane m at (y, x): 0 outside the frame
+  auto kval = [&](int m, int y, int x) -> float {
+    return (y >= 0 && y < g.H && x >= 0 && x < g.W) ? kb[(long long)m * g.HW + (long long)y * g.W + x] : 0.f;
+  };
+  // the query's bilinear weights and the ten coefficients of the expansion
+  const float w00 = (1.f - ah) * (1.f - aw), w01 = (1.f - ah) * aw, w10 = ah * (1.f - aw), w11 = ah * aw;
+  // contribution of plane m at grid position b[0] = (y, x) (pitch: row stride)
+  auto plane_term = [&](int m, const float* bp, int pitch) -> float {
+    switch (m) {
+      case 0:
+        return w00 * w00 * bp[0] + w01 * w01 * bp[1] + w10 * w10 * bp[pitch] + w11 * w11 * bp[pitch + 1];
+      case 1:
+        return 2.f * w00 * w01 * bp[0] + 2.f * w10 * w11 * bp[pitch];
+      case 2:
+        return 2.f * w00 * w10 * bp[0] + 2.f * w01 * w11 * bp[1];
+      case 3:
+        return 2.f * w00 * w11 * bp[0];
+      default:
+        return 2.f * w01 * w10 * bp[0];
+    }
   };
   // Thread sub owns grid columns sub and sub + TPQ (acc[2*zy + half] is row
-  // zy of column sub + TPQ*half) and walks down them, so the horizontal
-  // interpolation of a key row serves two grid rows.
+  // zy of column sub + TPQ*half).
   static_assert(EG == 2 * TPQ && PPT == 2 * EG, "two grid columns per thread");
-  // The tile's key region is staged CC channels at a time when it fits;
-  // otherwise each query's own EG x EG block, one channel at a time.
+  // The tile's region of the five planes is staged at once when it fits;
+  // otherwise each query's own EG x EG block, one plane at a time.
+  static_assert(NPLANE <= CC, "the planes fit in one chunk");
   const int xx = tid & 63;  // region staging: lane = column, waves = rows
-  const int cpc = staged ? CC : 1;
+  const int cpc = staged ? NPLANE : 1;
   const int bpitch = staged ? RP : EG, cstr = staged ? RH * RP : 0;
   const int qbase = staged ? qoy[jq] * RP + qox[jq] : jq * EG * EG;
   static_assert(NQ * EG * EG <= CC * RH * RP, "per-query blocks fit in the region buffer");
-  for (int c0 = 0; c0 < g.Ch; c0 += cpc) {
-    const int nc = min(cpc, g.Ch - c0);
+  for (int m0 = 0; m0 < NPLANE; m0 += cpc) {
     __syncthreads();  // previous chunk fully read
     if (staged) {
       // the whole chunk's loads in flight before the LDS stores
-      float st[CC][RH / (NT / 64)];
+      float st[NPLANE][RH / (NT / 64)];
 #pragma unroll
-      for (int c = 0; c < CC; ++c)
+      for (int m = 0; m < NPLANE; ++m)
 #pragma unroll
         for (int i = 0; i < RH / (NT / 64); ++i) {
           const int yy = (tid >> 6) + (NT / 64) * i;
-          st[c][i] = (xx < rw && yy < rh && c < nc) ? kval(c0 + c, ry0 + yy, rx0 + xx) : 0.f;
+          st[m][i] = (xx < rw && yy < rh) ? kval(m, ry0 + yy, rx0 + xx) : 0.f;
         }
 #pragma unroll
-      for (int c = 0; c < CC; ++c)
+      for (int m = 0; m < NPLANE; ++m)
 #pragma unroll
         for (int i = 0; i < RH / (NT / 64); ++i) {
           const int yy = (tid >> 6) + (NT / 64) * i;
-          if (xx < rw && yy < rh && c < nc) reg[(c * RH + yy) * RP + xx] = st[c][i];
+          if (xx < rw && yy < rh) reg[(m * RH + yy) * RP + xx] = st[m][i];
         }
     } else {
       for (int e = tid; e < NQ * EG * EG; e += NT) {
         const int jj = e / (EG * EG), rem = e % (EG * EG);
-        reg[e] = kval(c0, qay[jj] + rem / EG, qax[jj] + rem % EG);
+        reg[e] = kval(m0, qay[jj] + rem / EG, qax[jj] + rem % EG);
       }
     }
     __syncthreads();
     if (inside) {
-      for (int c = 0; c < nc; ++c) {
-        const float* base = &reg[c * cstr + qbase];
+      if (staged) {
+#pragma unroll
+        for (int m = 0; m < NPLANE; ++m) {
+          const float* base = &reg[m * cstr + qbase];
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            const int zx = sub + TPQ * half;
+            if (zx < E) {
+#pragma unroll
+              for (int zy = 0; zy < EG - 1; ++zy)
+                if (zy < E) acc[2 * zy + half] += plane_term(m, base + zy * bpitch + zx, bpitch);
+            }
+          }
+        }
+      } else {
+        const float* base = &reg[qbase];
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
           const int zx = sub + TPQ * half;
           if (zx < E) {
-            float h0 = (1.f - aw) * base[zx] + aw * base[zx + 1];
 #pragma unroll
-            for (int zy = 0; zy < EG - 1; ++zy) {
-              if (zy < E) {
-                const float* r1 = base + (zy + 1) * bpitch + zx;
-                const float h1 = (1.f - aw) * r1[0] + aw * r1[1];
-                const float kv = (1.f - ah) * h0 + ah * h1;
-                acc[2 * zy + half] = fmaf(kv, kv, acc[2 * zy + half]);
-                h0 = h1;
-              }
-            }
+            for (int zy = 0; zy < EG - 1; ++zy)
+              if (zy < E) acc[2 * zy + half] += plane_term(m0, base + zy * bpitch + zx, bpitch);
           }
         }
       }
@@ -215,14 +284,20 @@ __global__ void __launch_bounds__(l2n::NT) l2_norms_kernel(const float* __restri
   }
 }
 
+size_t l2_planes_bytes(const Geo& g) {
+  return ((size_t)NPLANE * g.B * g.T * g.HD * (size_t)g.HW * sizeof(float) + 255) & ~(size_t)255;
+}
+
 snls_status launch_l2_norms(const float* q, const float* k, const float* flows, const Geo& g, float* G, int pitch,
-                            float* Qn, hipStream_t s) {
+                            float* Qn, float* planes, hipStream_t s) {
   const int tiles_x = (g.W + l2n::TX - 1) / l2n::TX, tiles_y = (g.H + l2n::TY - 1) / l2n::TY;
   const long long ntile = (long long)tiles_x * tiles_y;
   if (ntile == 0 || g.rows == 0) return SNLS_OK;
   if (ntile > 0x7fffffffLL || (long long)g.B * g.HD * g.T > 65535 || 2 * g.wt + 1 > 65535) return SNLS_ERR_UNSUPPORTED;
+  const dim3 pgrid((unsigned)((g.HW + 255) / 256), (unsigned)(g.B * g.T * g.HD));
+  hipLaunchKernelGGL(l2_pair_planes_kernel, pgrid, dim3(256), 0, s, k, g, planes);
   dim3 grid((unsigned)ntile, (unsigned)(g.B * g.HD * g.T), (unsigned)(2 * g.wt + 1));
-  hipLaunchKernelGGL(l2_norms_kernel, grid, dim3(l2n::NT), 0, s, q, k, flows, g, tiles_x, G, pitch, Qn);
+  hipLaunchKernelGGL(l2_norms_kernel, grid, dim3(l2n::NT), 0, s, q, planes, flows, g, tiles_x, G, pitch, Qn);
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
 }
 

@@ -823,7 +823,8 @@ static size_t tile_plane_bytes(const Geo& g) {
 }
 size_t tile_ws_bytes(const Geo& g) {
   size_t b = tile_plane_bytes(g);                             // inner-product scores
-  if (g.dist == SNLS_DIST_L2) b += tile_plane_bytes(g) + (size_t)g.rows * sizeof(float);  // key and query norms
+  if (g.dist == SNLS_DIST_L2)  // key and query norm terms, key pair planes
+    b += tile_plane_bytes(g) + (((size_t)g.rows * sizeof(float) + 255) & ~(size_t)255) + l2_planes_bytes(g);
   return b;
 }
 
@@ -907,7 +908,9 @@ snls_status launch_search_tile(const float* q, const float* k, const float* flow
   if (g.dist == SNLS_DIST_L2) {
     gnorm = reinterpret_cast<float*>(reinterpret_cast<char*>(scores) + tile_plane_bytes(g));
     qnorm = reinterpret_cast<float*>(reinterpret_cast<char*>(gnorm) + tile_plane_bytes(g));
-    const snls_status st = launch_l2_norms(q, k, flows, g, gnorm, pitch, qnorm, s);
+    float* planes = reinterpret_cast<float*>(reinterpret_cast<char*>(qnorm) +
+                                             (((size_t)g.rows * sizeof(float) + 255) & ~(size_t)255));
+    const snls_status st = launch_l2_norms(q, k, flows, g, gnorm, pitch, qnorm, planes, s);
     if (st != SNLS_OK) return st;
   }
   return launch_tile_topk(scores, gnorm, qnorm, pitch, flows, g, dists, inds, s);

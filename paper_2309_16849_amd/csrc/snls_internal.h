@@ -68,8 +68,11 @@ snls_status launch_search_p1(const float* q, const float* k, const float* flows,
                              float* inds, float* scores, hipStream_t s);
 snls_status launch_search_p1_scores(const float* q, const float* k, const float* flows, const Geo& g, float* scores,
                                     int pitch, hipStream_t s);
+// L2 norm terms: key pair planes (workspace of l2_planes_bytes(g) bytes),
+// then the key-norm terms G (rows x pitch) and the query norms Qn (rows).
+size_t l2_planes_bytes(const Geo& g);
 snls_status launch_l2_norms(const float* q, const float* k, const float* flows, const Geo& g, float* G, int pitch,
-                            float* Qn, hipStream_t s);
+                            float* Qn, float* planes, hipStream_t s);
 snls_status launch_topk(const float* dall, const float* iall, int64_t rows, int ncand, int k, int dist,
                         float* dists, float* inds, hipStream_t s);
 snls_status launch_aggregate(const float* v, const float* dists, const float* inds, const Geo& g, float scale,
