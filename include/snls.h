@@ -112,9 +112,13 @@ typedef struct {
  *             dists (B, HD, T, nH, nW, (2wt+1)*ws*ws), inds (..., 3)
  *   workspace device scratch of at least snls_workspace_size(SNLS_OP_SEARCH, p)
  *             bytes, 256-byte aligned; may be NULL when that size is 0.  The
- *             top-k path for the inner product with stride0 = 1, stride1 <= 1,
- *             ps <= 7 and ws <= 9 scores every candidate into it (4 bytes per
- *             query row and candidate) before selecting; its contents are not
+ *             top-k paths for stride0 = 1, ps <= 7, ws <= 9 (inner product
+ *             with stride1 <= 1, squared L2 with stride1 = 1) and for ps = 1,
+ *             stride1 = 1, ws <= 15 (inner product, any stride0) score every
+ *             candidate into it (4 bytes per query row and candidate) before
+ *             selecting; squared L2 adds the key-norm term of every
+ *             candidate, the query norm of every row and five key pair
+ *             products per key pixel, frame and head.  Its contents are not
  *             needed between calls
  * Errors: SNLS_ERR_INVALID_ARG for shapes/parameters out of range or NULL
  * buffers; SNLS_ERR_UNSUPPORTED for k > SNLS_MAX_K; SNLS_ERR_WORKSPACE for a
