@@ -151,6 +151,10 @@ snls_status launch_search_topk_direct(const float* q, const float* k, const floa
 
 snls_status launch_search_topk(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, void* ws, hipStream_t s) {
+  // single-pixel patches at a query stride above 1: no patch overlap for
+  // the tiles to share, the per-query kernel is faster
+  if (g.ps == 1 && g.s0 > 1 && p1_supported(g))
+    return launch_search_p1(q, k, flows, g, dists, inds, static_cast<float*>(ws), s);
   if (tile_supported(g)) return launch_search_tile(q, k, flows, g, dists, inds, static_cast<float*>(ws), s);
   if (p1_supported(g)) return launch_search_p1(q, k, flows, g, dists, inds, static_cast<float*>(ws), s);
   return launch_search_topk_direct(q, k, flows, g, dists, inds, s);

@@ -102,8 +102,9 @@ __global__ void __launch_bounds__(l2n::NT, 3) l2_norms_kernel(const float* __res
   const int t2 = t + dt;
   if (t2 < 0 || t2 >= g.T) return;  // whole workgroup
   const int ty = (int)blockIdx.x / tiles_x, tx = (int)blockIdx.x % tiles_x;
-  const int h = ty * TY + jq / TX, w = tx * TX + jq % TX;
-  const bool inside = h < g.H && w < g.W;
+  const int mh = ty * TY + jq / TX, mw = tx * TX + jq % TX;  // query grid position
+  const bool inside = mh < g.nH && mw < g.nW;
+  const int h = mh * g.s0, w = mw * g.s0;
   const int E = g.ws + g.ps - 1;  // grid side used (<= 15)
 
   // offset of the query's window and the integer origin of its grid
@@ -252,7 +253,7 @@ __global__ void __launch_bounds__(l2n::NT, 3) l2_norms_kernel(const float* __res
   }
   __syncthreads();
   if (!inside) return;  // no barrier follows
-  const long long row = ((((long long)b * g.HD + hd) * g.T + t) * g.nH + h) * g.nW + w;
+  const long long row = ((((long long)b * g.HD + hd) * g.T + t) * g.nH + mh) * g.nW + mw;
   float* grow = G + row * pitch + (dt + g.wt) * g.ws * g.ws;
   for (int e = sub; e < g.ws * g.ws; e += TPQ) {
     const int dh = e / g.ws, dw = e % g.ws;
@@ -290,7 +291,7 @@ size_t l2_planes_bytes(const Geo& g) {
 
 snls_status launch_l2_norms(const float* q, const float* k, const float* flows, const Geo& g, float* G, int pitch,
                             float* Qn, float* planes, hipStream_t s) {
-  const int tiles_x = (g.W + l2n::TX - 1) / l2n::TX, tiles_y = (g.H + l2n::TY - 1) / l2n::TY;
+  const int tiles_x = (g.nW + l2n::TX - 1) / l2n::TX, tiles_y = (g.nH + l2n::TY - 1) / l2n::TY;
   const long long ntile = (long long)tiles_x * tiles_y;
   if (ntile == 0 || g.rows == 0) return SNLS_OK;
   if (ntile > 0x7fffffffLL || (long long)g.B * g.HD * g.T > 65535 || 2 * g.wt + 1 > 65535) return SNLS_ERR_UNSUPPORTED;

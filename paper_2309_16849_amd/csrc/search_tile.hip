@@ -1,6 +1,6 @@
-// search_tile.hip -- tiled shifted non-local search with fused top-k for
-// the inner-product distance, query stride 1 and key stride S_K <= 1
-// (Sec. 3.2).
+// search_tile.hip -- tiled shifted non-local search: scores of every
+// candidate for the inner product (key stride S_K <= 1, any query stride),
+// then the top-k of the scored rows (Sec. 3.2).
 //
 // Window cell d of a query sits at displacement disp_d = F + S_K (d - r);
 // with n_d = floor(disp_d) and a_d = disp_d - n_d its bilinear score is an
@@ -18,8 +18,10 @@
 // defeat plain tiling; the union of the shifted windows is still shared by
 // neighbouring queries).
 //
-// Work split (one workgroup = one 10 x 8 query tile of one (b, head, t),
-// looping over the frames of the temporal window):
+// Work split (one workgroup = one query tile of one (b, head, t), looping
+// over the frames of the temporal window; at query stride 1 and P = 7 the
+// tile is 10 x 8 queries, at stride S_Q the queries whose patches fit the
+// same 16-row halo, e.g. 5 x 4 at S_Q = 2):
 //  * 64 groups of 16 lanes; lane y of a group is halo row y (16 halo rows =
 //    tile rows + P - 1), a group owns one task = (shift row D_h, block of
 //    6 shift columns D_w);
@@ -177,7 +179,6 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
                                                                              int tiles_x, int tiles_y,
                                                                              float* __restrict__ scores, int pitch) {
   using namespace tile;
-  constexpr int TQH = HROWS - PS + 1;
   constexpr int HW = TQW + PS - 1;
   constexpr int LO = -(PS / 2);
   constexpr int QC4 = (HW + 3) / 4;  // 4-column items per q row
@@ -205,8 +206,18 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
   const int t = img % g.T;
   const int hd = (img / g.T) % g.HD;
   const int b = img / (g.T * g.HD);
-  const int y0 = ty * TQH, x0 = tx * TQW;  // tile origin (query = pixel, stride 1)
-  const int Y0 = y0 + LO, X0 = x0 + LO;    // halo origin
+  // Query stride S_Q: the tile is tqh x tqw queries (query-grid units) whose
+  // patches fit the HROWS x HW halo; at S_Q = 1 that is TQH x TQW.
+  const int s0 = g.s0;
+  const int tqh = (HROWS - PS) / s0 + 1, tqw = (TQW - 1) / s0 + 1, qn = tqh * tqw;
+  const int my0 = ty * tqh, mx0 = tx * tqw;  // tile origin (query grid)
+  const int y0 = my0 * s0, x0 = mx0 * s0;    // tile origin (pixels)
+  const int Y0 = y0 + LO, X0 = x0 + LO;      // halo origin
+  // halo row of this lane as the patch origin of a query row (-1: none), and
+  // the halo columns that are query patch origins
+  const int jh_lane = (lane16 % s0 == 0 && lane16 / s0 < tqh) ? lane16 / s0 : -1;
+  unsigned xmask = 0;
+  for (int xq = 0; xq < TQW; xq += s0) xmask |= 1u << xq;
   const int ws = g.ws, r = g.r;
 
   const float* qb = q + (((long long)b * g.T + t) * g.C + (long long)hd * g.Ch) * g.HW;
@@ -217,12 +228,12 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
   const __amdgpu_buffer_rsrc_t q_rs =
       __builtin_amdgcn_make_buffer_rsrc((void*)qb, (short)0, (int)(g.Ch * g.HW * 4), 0x00020000);
 
-  // window offset of this thread's query (tid < QN) for frame step dt
+  // window offset of this thread's query (tid < qn) for frame step dt
   auto fetch_flow = [&](int dtt, float& fh, float& fw) {
     fh = 0.f;
     fw = 0.f;
-    const int h = y0 + tid / TQW, w = x0 + tid % TQW;
-    if (dtt != 0 && tid < QN && h < g.H && w < g.W) {
+    const int h = y0 + s0 * (tid / tqw), w = x0 + s0 * (tid % tqw);
+    if (dtt != 0 && tid < qn && h < g.H && w < g.W) {
       const long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dtt, g.wt)) * 2;
       const long long pix = (long long)h * g.W + w;
       fh = flows[base * g.HW + pix];
@@ -251,8 +262,8 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
     }
     __syncthreads();
     {
-      const int jh = tid / TQW, jw = tid % TQW;
-      const bool inside = tid < QN && y0 + jh < g.H && x0 + jw < g.W;
+      const int jh = tid / tqw, jw = tid % tqw;
+      const bool inside = tid < qn && y0 + s0 * jh < g.H && x0 + s0 * jw < g.W;
       const float fh = fh_next, fw = fw_next;
       // Integer shifts a query's window reads: floor(disp) .. floor(disp) + 1
       // for its first .. last cell (disp grows with the cell index).
@@ -263,7 +274,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
       const int hi_h = (int)floorf(cand_disp(fh_u, g.s1, ws - 1, r)) + 1;
       const int lo_w = (int)floorf(cand_disp(fw_u, g.s1, 0, r));
       const int hi_w = (int)floorf(cand_disp(fw_u, g.s1, ws - 1, r)) + 1;
-      if (tid < QN) {
+      if (tid < qn) {
         sm.qlo_h[tid] = lo_h;
         sm.qlo_w[tid] = lo_w;
         sm.qf_h[tid] = fh;
@@ -445,11 +456,11 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
         // window tables: the first channel part writes, the others add in turn
         for (int pp = 0; pp < csplit; ++pp) {
           if (pp > 0) __syncthreads();
-          if (active && part == pp && lane16 < TQH) {
-            const int jh = lane16;
+          if (active && part == pp && jh_lane >= 0) {
 #pragma unroll
-            for (int jw = 0; jw < TQW; ++jw) {
-              const int j = jh * TQW + jw;
+            for (int jw = 0; jw < TQW; ++jw) {  // halo column of the patch origin
+              if (!((xmask >> jw) & 1u)) continue;
+              const int j = jh_lane * tqw + __builtin_popcount(xmask & ((1u << jw) - 1u));
               const int u = d_h - sm.qlo_h[j];
               const int vbase = dmin_w + blk * S - sm.qlo_w[j];
               if (u >= 0 && u < WP) {
@@ -485,20 +496,22 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
         return ok && dv == dv ? dv : -INFINITY;  // NaN scores as invalid
       };
       // ---- 4-tap combination and exact validity ----
-      for (int e = tid; e < QN * ws; e += NTHREADS) {
+      for (int e = tid; e < qn * ws; e += NTHREADS) {
         const int j = e / ws, dh = e % ws;
-        const int h = y0 + j / TQW, w = x0 + j % TQW;
-        if (h >= g.H || w >= g.W) continue;
-        float* srow = scores + ((rowb + h) * g.nW + w) * pitch + cbase + dh * ws;
+        const int mh = my0 + j / tqw, mw = mx0 + j % tqw;
+        if (mh >= g.nH || mw >= g.nW) continue;
+        const int h = mh * s0, w = mw * s0;
+        float* srow = scores + ((rowb + mh) * g.nW + mw) * pitch + cbase + dh * ws;
         for (int dw = 0; dw < ws; ++dw) srow[dw] = cell_score(j, h, w, dh, dw);
       }
     } else {
       // Union too wide for the LDS layout: score this frame directly.
       __syncthreads();
-      for (int e = tid; e < QN * ws; e += NTHREADS) {
+      for (int e = tid; e < qn * ws; e += NTHREADS) {
         const int j = e / ws, dh = e % ws;
-        const int h = y0 + j / TQW, w = x0 + j % TQW;
-        if (h >= g.H || w >= g.W) continue;
+        const int mh = my0 + j / tqw, mw = mx0 + j % tqw;
+        if (mh >= g.nH || mw >= g.nW) continue;
+        const int h = mh * s0, w = mw * s0;
         const float fh = sm.qf_h[j], fw = sm.qf_w[j];
         const float disp_h = cand_disp(fh, g.s1, dh, r);
         const bool okh = centre_ok(h, disp_h, g.H);
@@ -506,7 +519,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
           const float disp_w = cand_disp(fw, g.s1, dw, r);
           float d = -INFINITY;
           if (okh && centre_ok(w, disp_w, g.W)) d = score_candidate(q, k, g, b, hd, t, h, w, t2, disp_h, disp_w);
-          scores[((rowb + h) * g.nW + w) * pitch + cbase + dh * ws + dw] = d;
+          scores[((rowb + mh) * g.nW + mw) * pitch + cbase + dh * ws + dw] = d;
         }
       }
     }
@@ -807,11 +820,11 @@ __global__ void __launch_bounds__(wtk::WAVES * 64) wave_topk_kernel(const float*
   irow[2] = cand_disp(fw, g.s1, dw, g.r);
 }
 
-// The tiled path handles S_Q = 1, P <= 7, Ws <= 9 with the inner product
+// The tiled path handles any S_Q, P <= 7, Ws <= 9 with the inner product
 // (S_K <= 1) or the squared L2 distance (S_K = 1).
 bool tile_supported(const Geo& g) {
   const bool dist_ok = g.dist == SNLS_DIST_PROD ? g.s1 > 0.f && g.s1 <= 1.0f : g.s1 == 1.0f;
-  return dist_ok && g.s0 == 1 && g.ps <= 7 && g.ws <= tile::WSMAX && g.W >= 4 && g.k >= 1 &&
+  return dist_ok && g.ps <= 7 && g.ws <= tile::WSMAX && g.W >= 4 && g.k >= 1 &&
          (long long)g.Ch * g.HW * 4 < (1LL << 31);
 }
 
@@ -878,9 +891,10 @@ snls_status launch_search_p1(const float* q, const float* k, const float* flows,
 
 snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, float* scores, hipStream_t s) {
-  const int tqh = tile::HROWS - g.ps + 1;
-  const int tiles_x = (g.W + tile::TQW - 1) / tile::TQW;
-  const int tiles_y = (g.H + tqh - 1) / tqh;
+  // tile of tqh x tqw queries (the kernel derives the same from S_Q)
+  const int tqh = (tile::HROWS - g.ps) / g.s0 + 1, tqw = (tile::TQW - 1) / g.s0 + 1;
+  const int tiles_x = (g.nW + tqw - 1) / tqw;
+  const int tiles_y = (g.nH + tqh - 1) / tqh;
   const long long nwg = (long long)tiles_x * tiles_y * g.B * g.HD * g.T;
   if (nwg == 0) return SNLS_OK;
   if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;

@@ -226,8 +226,8 @@ def _swap_mask(p, swaps):
 
 
 # ------------------------------------------------------ tiled kernel --
-# Cases inside the tiled kernel's domain (inner product, S_Q = 1, S_K <= 1,
-# P <= 7, Ws <= 9, k <= 16): every patch size, key strides 1, 3/4, 1/2 and
+# Cases inside the tiled kernel's domain (inner product, S_K <= 1, P <= 7,
+# Ws <= 9; query strides 1 to 5): every patch size, key strides 1, 3/4, 1/2 and
 # 1/4, ragged tiles and channel chunks, narrow shift unions (few tasks:
 # channel-split groups), wide ones (several rounds) and unions too wide for
 # the LDS layout (the per-candidate fallback).
@@ -253,6 +253,13 @@ def _tile_cases(n=28, seed=31):
 TILE_CASES = _tile_cases() + [
     (small_params(T=3, C=16, H=23, W=29, ws=9, wt=1, ps=7, k=10), "edge"),
     (small_params(T=3, C=8, H=17, W=19, ws=5, wt=1, ps=3, k=7, stride1=0.5), "edge"),
+    # query strides above 1: smaller tiles of strided queries on the same halo
+    (small_params(T=3, C=16, H=37, W=41, ws=9, wt=1, ps=7, k=10, stride0=2), "smooth"),
+    (small_params(T=3, C=12, HD=2, H=29, W=33, ws=7, wt=2, ps=5, k=12, stride0=2), "frac"),
+    (small_params(T=2, C=8, H=31, W=26, ws=5, wt=1, ps=3, k=9, stride0=3, stride1=0.5), "wide"),
+    (small_params(T=3, C=8, H=23, W=25, ws=9, wt=1, ps=4, k=16, stride0=4), "edge"),
+    (small_params(T=2, C=6, H=19, W=21, ws=8, wt=1, ps=6, k=20, stride0=2), "far"),
+    (small_params(T=3, C=10, H=21, W=27, ws=9, wt=1, ps=2, k=10, stride0=5), "int"),
 ]
 TILE_IDS = ["t%d-ws%d-wt%d-ps%d-sk%g-k%d-%s" % (i, p["ws"], p["wt"], p["ps"], p["stride1"], p["k"], kd)
             for i, (p, kd) in enumerate(TILE_CASES)]
@@ -305,6 +312,8 @@ L2_TILE_CASES = [
     (small_params(T=3, C=70, H=19, W=26, ws=9, wt=1, ps=2, k=10, dist_type=1), "smooth"),
     (small_params(T=3, C=16, H=21, W=26, ws=9, wt=1, ps=7, k=10, dist_type=1), "edge"),
     (small_params(T=3, C=16, H=25, W=30, ws=9, wt=1, ps=7, k=10, dist_type=1), "far"),
+    (small_params(T=3, C=16, H=33, W=35, ws=9, wt=1, ps=7, k=10, dist_type=1, stride0=2), "smooth"),
+    (small_params(T=2, C=8, H=27, W=22, ws=5, wt=1, ps=3, k=20, dist_type=1, stride0=3), "frac"),
 ]
 
 
