@@ -325,6 +325,11 @@ constexpr float QSCALE = 16777216.f; // fixed point 2^24
 static_assert(MAXREC <= WAVES * 64 * (TX + 1), "the covering queries' scores fit in the output buffer");
 }  // namespace aggt
 
+// floor(a / s) for s > 0 and any sign of a
+SNLS_DEV int floor_div(int a, int s) { return a >= 0 ? a / s : -((-a + s - 1) / s); }
+
+// SQ: the query stride when known at compile time (1), else 0 (g.s0).
+template <int SQ>
 __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* __restrict__ vcl,
                                                                   const float* __restrict__ dists,
                                                                   const float* __restrict__ inds, Geo g,
@@ -352,9 +357,11 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
   const int ty = trem / tiles_x, tx = trem % tiles_x;
   const int t = img % g.T, hd = (img / g.T) % g.HD, b = img / (g.T * g.HD);
   const int y0 = ty * TY, x0 = tx * TX;
-  const int P = g.ps, K = g.k, nslot = 2 * g.wt + 1;
-  const int QY = TY + P - 1, QX = TX + P - 1, NQ = QY * QX, NR = NQ * K;
-  const int hq0 = y0 - g.lo - P + 1, wq0 = x0 - g.lo - P + 1;  // first covering query
+  const int P = g.ps, K = g.k, nslot = 2 * g.wt + 1, s0 = SQ ? SQ : g.s0;
+  // covering queries of the tile: query-grid rows hq0 .. hq0+QY-1 and
+  // columns wq0 .. wq0+QX-1 (query m covers pixels m*s0 + lo .. + P-1)
+  const int QY = (TY + P - 2) / s0 + 1, QX = (TX + P - 2) / s0 + 1, NQ = QY * QX, NR = NQ * K;
+  const int hq0 = floor_div(y0 - g.lo - P + 1 + s0 - 1, s0), wq0 = floor_div(x0 - g.lo - P + 1 + s0 - 1, s0);
   const float sscale = (g.dist == SNLS_DIST_PROD ? 1.f : -1.f) * scale;
   const long long rowb = (((long long)b * g.HD + hd) * g.T + t) * g.nH;
 
@@ -367,8 +374,8 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
   float* const dq = &obuf[0][0][0];
   for (int e = tid; e < NR; e += NT) {
     const int j = e / K, l = e - (e / K) * K;
-    const int h = hq0 + j / QX, w = wq0 + j % QX;
-    dq[e] = (h >= 0 && h < g.H && w >= 0 && w < g.W) ? dists[((rowb + h) * g.nW + w) * K + l] : -INFINITY;
+    const int h = hq0 + j / QX, w = wq0 + j % QX;  // query grid position
+    dq[e] = (h >= 0 && h < g.nH && w >= 0 && w < g.nW) ? dists[((rowb + h) * g.nW + w) * K + l] : -INFINITY;
   }
   __syncthreads();
   for (int j = tid; j < NQ; j += NT) {
@@ -483,15 +490,18 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
 
   // ---- phase 2: output row wv, pixel after pixel ----
   // The bins of pixel x hold the fixed-point tap weights of the records of
-  // its P x P covering queries.  Pixel x + 1 is covered by the same queries
-  // except one query column leaving and one entering, and integer sums do
-  // not depend on the order, so the bins slide along the row: all P columns
-  // at the first pixel, then +1 column and -1 column per pixel.
+  // its covering queries: query rows ra .. rb of the wave's output row and
+  // query columns ca(x) .. cb(x).  Moving along the row, columns leave and
+  // enter one at a time, and integer sums do not depend on the order, so the
+  // bins slide: only the records of changed columns are added or removed.
   const int y = y0 + wv;
-  const int PK = P * K, PPK = P * P * K;
-  const float inv_k = 1.f / (float)K, inv_p = 1.f / (float)P, inv_pk = 1.f / (float)PK;
+  const float inv_k = 1.f / (float)K;
   const float* vb = vcl + (long long)b * g.T * g.HW * g.C + (long long)hd * g.Ch;
-  const int cov_y = cover_count_1d(y, 1, g.nH, g.lo, P);
+  const int cov_y = cover_count_1d(y, s0, g.nH, g.lo, P);
+  const int ra = floor_div(y - g.lo - P + 1 + s0 - 1, s0) - hq0, rb = floor_div(y - g.lo, s0) - hq0;
+  const int nrow = rb - ra + 1;  // covering query rows (0 < nrow <= QY)
+  const int RK = nrow * K;       // records of one query column
+  const float inv_rk = 1.f / (float)max(RK, 1);
   unsigned slots = 0;  // slots with entries in the tile (wave-uniform)
   for (int s = 0; s < nslot; ++s)
     if (sstat[2 * NSLOT + s] != 0) slots |= 1u << s;
@@ -499,14 +509,14 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
   int* const wbins = bins[wv];
   // add (sign +1) or remove (-1) the records of query columns c0 .. c0+nc-1
   auto slide = [&](int c0, int nc, int sign) {
-    for (int e0 = 0; e0 < nc * PK; e0 += 64) {
+    for (int e0 = 0; e0 < nc * RK; e0 += 64) {
       const int e = e0 + lane;
-      const int cc = (int)(((float)e + 0.5f) * inv_pk);
-      const int rem = e - cc * PK;
+      const int cc = (int)(((float)e + 0.5f) * inv_rk);
+      const int rem = e - cc * RK;
       const int qy = (int)(((float)rem + 0.5f) * inv_k);
       const int l = rem - qy * K;
-      const int ri = ((wv + qy) * QX + c0 + cc) * K + l;
-      const int code = e < nc * PK ? rcode[ri] : -1;
+      const int ri = ((ra + qy) * QX + c0 + cc) * K + l;
+      const int code = e < nc * RK ? rcode[ri] : -1;
       if (code >= 0) {
         const int4 tp = rtap[ri];
         if (tp.x) atomicAdd(&wbins[code], sign * tp.x);
@@ -516,26 +526,38 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
       }
     }
   };
+  int pa = 0, pb = -1;  // query columns in the bins
   for (int px = 0; px < TX; ++px) {
     const int x = x0 + px;
     if (y >= g.H || x >= g.W) break;  // wave-uniform
     float acc = 0.f;
-    if (px == 0) {
-      slide(0, P, 1);
+    const int ca = floor_div(x - g.lo - P + 1 + s0 - 1, s0) - wq0, cb = floor_div(x - g.lo, s0) - wq0;
+    if constexpr (SQ == 1) {  // columns px .. px+P-1: all P at the first pixel, then one in, one out
+      if (px == 0) {
+        slide(0, P, 1);
+      } else {
+        slide(px + P - 1, 1, 1);
+        slide(px - 1, 1, -1);
+      }
     } else {
-      slide(px + P - 1, 1, 1);
-      slide(px - 1, 1, -1);
+      const int add0 = max(pb + 1, ca);
+      if (cb >= add0) slide(add0, cb - add0 + 1, 1);
+      const int del1 = min(ca - 1, pb);
+      if (del1 >= pa) slide(pa, del1 - pa + 1, -1);
+      pa = ca;
+      pb = cb;
     }
     if (any_direct) {
       // neighbours outside the bin boxes: the whole wave reads their taps directly
-      for (int e0 = 0; e0 < PPK; e0 += 64) {
+      const int ncov = (cb - ca + 1) * RK;
+      for (int e0 = 0; e0 < ncov; e0 += 64) {
         const int e = e0 + lane;
-        const int jq = (int)(((float)e + 0.5f) * inv_k);
-        const int l = e - jq * K;
-        const int qy = (int)(((float)jq + 0.5f) * inv_p);
-        const int qx = jq - qy * P;
-        const int ri = ((wv + qy) * QX + px + qx) * K + l;
-        const int code = e < PPK ? rcode[ri] : -1;
+        const int cc = (int)(((float)e + 0.5f) * inv_rk);
+        const int rem = e - cc * RK;
+        const int qy = (int)(((float)rem + 0.5f) * inv_k);
+        const int l = rem - qy * K;
+        const int ri = ((ra + qy) * QX + ca + cc) * K + l;
+        const int code = e < ncov ? rcode[ri] : -1;
         unsigned long long om = __ballot(code == -2);
         while (om) {
           const int src = __ffsll((long long)om) - 1;
@@ -586,7 +608,7 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
       }
     }
     wave_lds_sync();
-    const int cnt = cov_y * cover_count_1d(x, 1, g.nW, g.lo, P);
+    const int cnt = cov_y * cover_count_1d(x, s0, g.nW, g.lo, P);
     obuf[wv][lane][px] = cnt > 0 ? acc * (1.f / (float)cnt) : 0.f;
   }
   // write the row: TX consecutive pixels per channel
@@ -858,16 +880,21 @@ snls_status launch_aggregate(const float* v, const float* dists, const float* in
   // merged kernel limits: frames per window, channels per head, 32-bit
   // offsets inside one batch entry, per-bin weight sums below 2^31 in 2^-24
   // fixed point (at most P^2 <= 121 covering patches)
-  const long long nq_tile = (long long)(aggt::TY + g.ps - 1) * (aggt::TX + g.ps - 1);
-  if (g.s0 == 1 && nslot <= aggt::NSLOT && g.Ch <= 64 && (long long)g.T * g.HW * g.C < (1LL << 31) &&
+  const long long nq_tile =
+      (long long)((aggt::TY + g.ps - 2) / g.s0 + 1) * ((aggt::TX + g.ps - 2) / g.s0 + 1);  // covering queries
+  if (nslot <= aggt::NSLOT && g.Ch <= 64 && (long long)g.T * g.HW * g.C < (1LL << 31) &&
       g.ps <= 11 && nq_tile <= aggt::MAXQ && nq_tile * g.k <= aggt::MAXREC) {
     dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
     hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
     const int tiles_x = (g.W + aggt::TX - 1) / aggt::TX, tiles_y = (g.H + aggt::TY - 1) / aggt::TY;
     const long long nwg = (long long)tiles_x * tiles_y * g.B * g.T * g.HD;
     if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
-    hipLaunchKernelGGL(aggregate_tile_kernel, dim3((unsigned)nwg), dim3(aggt::NT), 0, s, vcl, dists, inds, g, scale,
-                       tiles_x, tiles_y, out);
+    if (g.s0 == 1)
+      hipLaunchKernelGGL(aggregate_tile_kernel<1>, dim3((unsigned)nwg), dim3(aggt::NT), 0, s, vcl, dists, inds, g,
+                         scale, tiles_x, tiles_y, out);
+    else
+      hipLaunchKernelGGL(aggregate_tile_kernel<0>, dim3((unsigned)nwg), dim3(aggt::NT), 0, s, vcl, dists, inds, g,
+                         scale, tiles_x, tiles_y, out);
     return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
   }
   {

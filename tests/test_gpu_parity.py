@@ -149,10 +149,13 @@ def _motion_inputs(p, seed, amp=4.0):
     return fr[None].copy(), fl[None].copy()
 
 
-@pytest.mark.parametrize("ps,k,C,HD,scale", [(7, 10, 64, 1, 1.0), (3, 10, 64, 1, 1.0), (5, 16, 32, 2, 0.3),
-                                              (7, 4, 48, 1, 0.05), (1, 12, 64, 1, 1.0)])
-def test_aggregate_tiled_motion(dev, ps, k, C, HD, scale):
-    p = small_params(T=5, C=C, HD=HD, H=37, W=53, ws=9, wt=2, ps=ps, k=k)
+@pytest.mark.parametrize("ps,k,C,HD,scale,stride0", [(7, 10, 64, 1, 1.0, 1), (3, 10, 64, 1, 1.0, 1),
+                                                      (5, 16, 32, 2, 0.3, 1), (7, 4, 48, 1, 0.05, 1),
+                                                      (1, 12, 64, 1, 1.0, 1), (7, 10, 64, 1, 1.0, 2),
+                                                      (3, 10, 32, 2, 0.5, 2), (5, 8, 16, 1, 1.0, 3),
+                                                      (4, 6, 16, 1, 1.0, 4), (2, 9, 8, 1, 1.0, 5)])
+def test_aggregate_tiled_motion(dev, ps, k, C, HD, scale, stride0):
+    p = small_params(T=5, C=C, HD=HD, H=37, W=53, ws=9, wt=2, ps=ps, k=k, stride0=stride0)
     x, flows = _motion_inputs(p, 9100 + ps + k)
     v = np.random.default_rng(9200 + ps).standard_normal(x.shape, dtype=np.float32)
     xd = _d(x, dev)
