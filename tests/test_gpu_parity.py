@@ -554,13 +554,13 @@ def _covering_rows(p, pix):
     return np.array(sorted(rows), np.int64)
 
 
-@pytest.mark.parametrize("idx", [0, 1, 2, 3, 4, 5, 6, 7, 8])
+@pytest.mark.parametrize("idx", [0, 1, 2, 3, 4, 5, 6, 7, 8, 9])
 def test_workload_parity(dev, idx):
     """Search + top-k + aggregation of each workload at its full size (the
     launch configuration bench.py times), on sampled rows and pixels: the five
     workloads, then the paper's own benchmark shapes (320 x 320 at query
     strides 1 and 2, the 152 x 152 x 192 memory shape) and the 480 x 854
-    workload at key stride 1/2."""
+    workload at key stride 1/2 and at query stride 2."""
     c = _cfg(idx)
     p, scale = c["params"], c["scale"]
     print("workload %d (%s) %s" % (idx, c["name"], p), flush=True)

@@ -56,6 +56,10 @@ CONFIGS = [
     # pixel apart.
     dict(name="denoise480x854_sk05", B=1, T=5, C=64, H=480, W=854, HD=1, ws=9, wt=2, ps=7, stride0=1, stride1=0.5,
          k=10, dist_type=0, scale=1.0, video="motion", amp=16.0, backward=False, data_of="denoise480x854"),
+    # Query stride 2 on the same video (a quarter of the queries, strided
+    # patches overlapping by 5 of 7 pixels).
+    dict(name="denoise480x854_s2", B=1, T=5, C=64, H=480, W=854, HD=1, ws=9, wt=2, ps=7, stride0=2, stride1=1.0,
+         k=10, dist_type=0, scale=1.0, video="motion", amp=16.0, backward=False, data_of="denoise480x854"),
 ]
 
 # The five workloads every parity test covers; the paper's benchmark shapes
