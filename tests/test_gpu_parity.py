@@ -450,7 +450,8 @@ def test_aggregate_stacked(dev, ps, stride0, HD, k, C):
 
 @pytest.mark.parametrize("dist_type,ps,ws,k,stride0", [(0, 3, 5, 10, 1), (0, 7, 9, 10, 1), (1, 3, 5, 10, 1),
                                                        (0, 4, 8, 10, 1), (0, 7, 9, 20, 1), (0, 1, 9, 20, 2),
-                                                       (0, 1, 15, 30, 2), (1, 5, 7, 24, 1)])
+                                                       (0, 1, 15, 30, 2), (1, 5, 7, 24, 1), (0, 7, 9, 10, 2),
+                                                       (1, 3, 5, 10, 3)])
 def test_nan_features_match_oracle(dev, dist_type, ps, ws, k, stride0):
     """NaN feature values away from the borders: every candidate whose patch
     reads one is invalid (a NaN similarity ranks as an invalid candidate), as
