@@ -255,15 +255,19 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
         __builtin_amdgcn_make_buffer_rsrc((void*)kb, (short)0, (int)(g.Ch * g.HW * 4), 0x00020000);
 
     // ---- offsets of the tile's queries and the union of shifts ----
-    if (tid < 4) sm.uni[tid] = (tid & 1) ? INT_MIN : INT_MAX;
+    // (thread-index arithmetic is redone per frame rather than kept live
+    // across the frame's channel loops)
+    int tidf = tid;
+    asm volatile("" : "+v"(tidf));
+    if (tidf < 4) sm.uni[tidf] = (tidf & 1) ? INT_MIN : INT_MAX;
     if (first) {
       fetch_flow(dt, fh_next, fw_next);
       first = false;
     }
     __syncthreads();
     {
-      const int jh = tid / tqw, jw = tid % tqw;
-      const bool inside = tid < qn && y0 + s0 * jh < g.H && x0 + s0 * jw < g.W;
+      const int jh = tidf / tqw, jw = tidf % tqw;
+      const bool inside = tidf < qn && y0 + s0 * jh < g.H && x0 + s0 * jw < g.W;
       const float fh = fh_next, fw = fw_next;
       // Integer shifts a query's window reads: floor(disp) .. floor(disp) + 1
       // for its first .. last cell (disp grows with the cell index).
@@ -274,24 +278,26 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
       const int hi_h = (int)floorf(cand_disp(fh_u, g.s1, ws - 1, r)) + 1;
       const int lo_w = (int)floorf(cand_disp(fw_u, g.s1, 0, r));
       const int hi_w = (int)floorf(cand_disp(fw_u, g.s1, ws - 1, r)) + 1;
-      if (tid < qn) {
-        sm.qlo_h[tid] = lo_h;
-        sm.qlo_w[tid] = lo_w;
-        sm.qf_h[tid] = fh;
-        sm.qf_w[tid] = fw;
+      if (tidf < qn) {
+        sm.qlo_h[tidf] = lo_h;
+        sm.qlo_w[tidf] = lo_w;
+        sm.qf_h[tidf] = fh;
+        sm.qf_w[tidf] = fw;
       }
       // union bounds: wave reductions, then one LDS atomic per wave
-      if (tid < ((QN + 63) & ~63)) {
+      if (tidf < ((QN + 63) & ~63)) {
         int a0 = inside ? lo_h : INT_MAX, a1 = inside ? hi_h : INT_MIN;
         int a2 = inside ? lo_w : INT_MAX, a3 = inside ? hi_w : INT_MIN;
+        const int ln = tidf & 63;
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) {
-          a0 = min(a0, __shfl_xor(a0, off));
-          a1 = max(a1, __shfl_xor(a1, off));
-          a2 = min(a2, __shfl_xor(a2, off));
-          a3 = max(a3, __shfl_xor(a3, off));
+          const int src = (ln ^ off) << 2;
+          a0 = min(a0, __builtin_amdgcn_ds_bpermute(src, a0));
+          a1 = max(a1, __builtin_amdgcn_ds_bpermute(src, a1));
+          a2 = min(a2, __builtin_amdgcn_ds_bpermute(src, a2));
+          a3 = max(a3, __builtin_amdgcn_ds_bpermute(src, a3));
         }
-        if ((tid & 63) == 0) {
+        if (ln == 0) {
           atomicMin(&sm.uni[0], a0);
           atomicMax(&sm.uni[1], a1);
           atomicMin(&sm.uni[2], a2);
@@ -395,19 +401,25 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
           for (int n = 0; n < NIT; ++n) {
             const int pk = it_pack[n];
             if (pk & (1 << 24)) {
-              const int sh = ((pk >> 13) & 7) - 3, mask = (pk >> 16) & 15;
-              const float v0 = __uint_as_float(stg[n].x), v1 = __uint_as_float(stg[n].y);
-              const float v2 = __uint_as_float(stg[n].z), v3 = __uint_as_float(stg[n].w);
-              float o[4];
+              // bits 13..19 of the pack read 3 | 15 << 3 for an aligned item
+              // with all four columns inside the frame: stored as loaded
+              if (((pk >> 13) & 127) != (3 | (15 << 3))) {
+                const int sh = ((pk >> 13) & 7) - 3, mask = (pk >> 16) & 15;
+                const unsigned v0 = stg[n].x, v1 = stg[n].y, v2 = stg[n].z, v3 = stg[n].w;
+                unsigned o[4];
 #pragma unroll
-              for (int j = 0; j < 4; ++j) {
-                const int src = j + sh;  // in 0..3 for every column inside the frame
-                const float val = src <= 0 ? v0 : (src == 1 ? v1 : (src == 2 ? v2 : v3));
-                o[j] = (mask >> j) & 1 ? val : 0.f;
+                for (int j = 0; j < 4; ++j) {
+                  const int src = j + sh;  // in 0..3 for every column inside the frame
+                  const unsigned val = src <= 0 ? v0 : (src == 1 ? v1 : (src == 2 ? v2 : v3));
+                  o[j] = (mask >> j) & 1 ? val : 0u;
+                }
+                stg[n] = u32x4{o[0], o[1], o[2], o[3]};
               }
               float* dst = (n == 1 && q_slot) ? &sm.qst[bsel][pk & 8191] : &sm.kst[bsel][pk & 8191];
-#pragma unroll
-              for (int j = 0; j < 4; ++j) dst[j] = o[j];
+              dst[0] = __uint_as_float(stg[n].x);
+              dst[1] = __uint_as_float(stg[n].y);
+              dst[2] = __uint_as_float(stg[n].z);
+              dst[3] = __uint_as_float(stg[n].w);
             }
           }
         };
@@ -456,11 +468,14 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
         // window tables: the first channel part writes, the others add in turn
         for (int pp = 0; pp < csplit; ++pp) {
           if (pp > 0) __syncthreads();
-          if (active && part == pp && jh_lane >= 0) {
+          int jl = jh_lane;
+          unsigned xm = xmask;
+          asm volatile("" : "+v"(jl), "+s"(xm));  // computed here, not kept live across the channel loop
+          if (active && part == pp && jl >= 0) {
 #pragma unroll
             for (int jw = 0; jw < TQW; ++jw) {  // halo column of the patch origin
-              if (!((xmask >> jw) & 1u)) continue;
-              const int j = jh_lane * tqw + __builtin_popcount(xmask & ((1u << jw) - 1u));
+              if (!((xm >> jw) & 1u)) continue;
+              const int j = jl * tqw + __builtin_popcount(xm & ((1u << jw) - 1u));
               const int u = d_h - sm.qlo_h[j];
               const int vbase = dmin_w + blk * S - sm.qlo_w[j];
               if (u >= 0 && u < WP) {
