@@ -320,22 +320,46 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
     const int nblk = (UW + S - 1) / S;
 
     if (nblk <= MAXBLK) {
-      // A wave's 4 groups take 4 consecutive shift rows of one column block:
-      // their K reads then hit overlapping rows (broadcast) in distinct banks.
-      // A round covers as many shift rows as the waves and the K rows of the
-      // LDS layout allow; when a round has few tasks, the channels of each
-      // task are split over several waves (csplit parts).
+      // A task is (shift row, column block); a round covers as many shift
+      // rows as the groups and the K rows of the LDS layout allow.  Whole
+      // quads of rows go to whole waves -- a wave's 4 groups take 4
+      // consecutive shift rows of one block, so their K reads hit
+      // overlapping rows (broadcast) in distinct banks.  The rows past the
+      // last whole quad (tail) go to single groups packed after them.  The
+      // channels of a task are split into csplit parts (each part a group of
+      // its own) as far as the 64 groups allow: the full quads first, then
+      // the tail, which would otherwise keep whole waves busy for one row.
       const int span_max = KR - HROWS + 1;
-      const int rows_per_round = min(span_max, 4 * (NTHREADS / 64 / nblk));
+      const int rows_per_round = min(span_max, NGROUP / nblk);
       for (int rr0 = 0; rr0 < UH; rr0 += rows_per_round) {
         const int nrows = min(rows_per_round, UH - rr0);
-        const int units = nblk * ((nrows + 3) / 4);  // waves per channel part
-        const int csplit = units <= 4 ? 4 : (units <= 8 ? 2 : 1);
-        const int part = wave / units;
-        const int unit = wave - part * units;
-        const int blk = unit % nblk;
-        const int d_row = (unit / nblk) * 4 + (grp & 3);
-        const bool active = part < csplit && d_row < nrows;
+        const int uf = nblk * (nrows >> 2);  // whole quads: waves per channel part
+        const int tt = nblk * (nrows & 3);   // tail tasks
+        const int csf = 16 * uf + tt <= NGROUP ? 4 : (8 * uf + tt <= NGROUP ? 2 : 1);
+        const int gf = 4 * uf * csf;         // groups of the whole quads (a whole number of waves)
+        const int cst = gf + 4 * tt <= NGROUP ? 4 : (gf + 2 * tt <= NGROUP ? 2 : 1);
+
+        int part, blk, d_row;
+        bool active;
+        if (wave < gf / 4) {
+          part = wave / uf;
+          const int unit = wave - part * uf;
+          blk = unit % nblk;
+          d_row = (unit / nblk) * 4 + (grp & 3);
+          active = true;
+        } else {
+          // tail: the cst parts of a task are consecutive groups of one wave
+          // (lanes 16 or 32 apart), summed across the lanes before the
+          // window tables are written
+          const int e = grp - gf, rt = nrows & 3;
+          const int task = e / cst;
+          part = e - task * cst;
+          blk = rt > 0 ? task / rt : nblk;
+          d_row = (nrows & ~3) + (rt > 0 ? task - (task / rt) * rt : 0);
+          active = rt > 0 && blk < nblk;
+        }
+        // channel parts are whole waves: gf is a multiple of 4 groups
+        const int csplit = __builtin_amdgcn_readfirstlane(wave < gf / 4 ? csf : cst);
         const int dh_lo = dmin_h + rr0;
         const int krows = HROWS + nrows - 1;
         const int kcols = HW + nblk * S - 1;
@@ -433,7 +457,8 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
           if (more) load_items(c0 + CC);  // in flight during this chunk's products
           if (active) {
 #pragma unroll 1
-            for (int c = part; c < CC; c += csplit) {
+            for (int it = 0; it < CC / csplit; ++it) {  // CC is a multiple of csplit: same count for every part
+              const int c = part + it * csplit;
               const float* qr = &sm.qst[bsel][(c * HROWS + lane16) * QP];
               const float* kr = &sm.kst[bsel][(c * KR + krow) * KP + blk * S];
               // sliding window kw[i] = K(x + i) along the halo row
@@ -465,13 +490,27 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
             asm volatile("" : "+v"(s));  // materialise the sum here: keeps the row moves short-lived
             acc[jw][i] = s;
           }
-        // window tables: the first channel part writes, the others add in turn
-        for (int pp = 0; pp < csplit; ++pp) {
+        // tail parts: sum over the groups of the wave (fixed order, the same
+        // value in every part: (p0 + p1) + (p2 + p3))
+        if (wave >= gf / 4 && csplit > 1) {
+#pragma unroll
+          for (int jw = 0; jw < TQW; ++jw)
+#pragma unroll
+            for (int i = 0; i < S; ++i) {
+              float s = acc[jw][i];
+              s += __shfl_xor(s, 16);
+              if (csplit == 4) s += __shfl_xor(s, 32);
+              acc[jw][i] = s;
+            }
+        }
+        // window tables: the first channel part writes, the other parts of
+        // the whole quads add in turn (the tail's part 0 writes the sum)
+        for (int pp = 0; pp < csf; ++pp) {
           if (pp > 0) __syncthreads();
           int jl = jh_lane;
           unsigned xm = xmask;
           asm volatile("" : "+v"(jl), "+s"(xm));  // computed here, not kept live across the channel loop
-          if (active && part == pp && jl >= 0) {
+          if (active && part == pp && (pp == 0 || wave < gf / 4) && jl >= 0) {
 #pragma unroll
             for (int jw = 0; jw < TQW; ++jw) {  // halo column of the patch origin
               if (!((xm >> jw) & 1u)) continue;
