@@ -140,6 +140,16 @@ __global__ void __launch_bounds__(p1::NT, 8) search_p1_scores_kernel(const float
     roff[i] = (staged && xx < rw && yy < rh && y >= 0 && y < g.H && x >= 0 && x < g.W) ? (unsigned)((y * g.W + x) * 4)
                                                                                         : OOB;
   }
+  // this thread's q staging item (tid < CC * NQ): channel tid / NQ of query
+  // tid % NQ, as a byte offset in channel 0 (OOB: outside the frame)
+  const __amdgpu_buffer_rsrc_t q_rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)qb, (short)0, (int)(g.Ch * g.HW * 4), 0x00020000);
+  unsigned qoff = OOB;
+  if (tid < CC * NQ) {
+    const int c = tid / NQ, jj = tid % NQ;
+    const int qh = (ty * TQ + jj / TQ) * g.s0, qw = (tx * TQ + jj % TQ) * g.s0;
+    if (qh < g.H && qw < g.W) qoff = (unsigned)(((long long)c * g.HW + (long long)qh * g.W + qw) * 4);
+  }
   float stg[CC][NRI];
   float qstg = 0.f;
   auto load_chunk = [&](int c0) {
@@ -154,10 +164,9 @@ __global__ void __launch_bounds__(p1::NT, 8) search_p1_scores_kernel(const float
       }
     }
     if (tid < CC * NQ) {
-      const int c = tid / NQ, jj = tid % NQ;
-      const int qh = (ty * TQ + jj / TQ) * g.s0, qw = (tx * TQ + jj % TQ) * g.s0;
-      qstg = (c0 + c < g.Ch && qh < g.H && qw < g.W) ? qb[(long long)(c0 + c) * g.HW + (long long)qh * g.W + qw]
-                                                     : 0.f;
+      const bool cin = c0 + tid / NQ < g.Ch;
+      const unsigned off = (qoff != OOB && cin) ? qoff + (unsigned)c0 * (unsigned)g.HW * 4u : OOB;
+      qstg = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(q_rs, off, 0, 0));
     }
   };
   auto store_chunk = [&](int buf) {

@@ -300,6 +300,45 @@ def test_tiled_search_topk(dev, case):
     compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
 
 
+# Task packing of the tiled scores kernel: every tile of every frame gets
+# offsets whose integer parts span a chosen number of rows and columns, so
+# the union of its windows is 10..22 shift rows by 10..26 shift columns.
+# That runs every tail length (0-3 rows past the last whole quad of 4), every
+# number of 6-column blocks (2-5), the channel split of the tail (1, 2 or 4
+# parts) and unions that take two rounds of rows.
+def _packing_flows(p, seed):
+    r = np.random.default_rng(seed)
+    tqh, tqw = 16 - p["ps"] + 1, 8  # query tile of the tiled kernel at query stride 1
+    fl = np.zeros((p["B"], p["T"], 2 * p["wt"], 2, p["H"], p["W"]), np.float32)
+    n = 0
+    for t in range(p["T"]):
+        for slot in range(2 * p["wt"]):
+            for y0 in range(0, p["H"], tqh):
+                for x0 in range(0, p["W"], tqw):
+                    sh, sw = (n * 5) % 13, (n * 7) % 17
+                    n += 1
+                    yy, xx = np.mgrid[y0:min(y0 + tqh, p["H"]), x0:min(x0 + tqw, p["W"])]
+                    j = (yy - y0) * tqw + (xx - x0)
+                    base_h, base_w = r.integers(-2, 3, 2)
+                    fl[:, t, slot, 0, yy, xx] = base_h + 0.3 + (j % (sh + 1))
+                    fl[:, t, slot, 1, yy, xx] = base_w + 0.6 + ((j * 3) % (sw + 1))
+    return fl
+
+
+@pytest.mark.parametrize("ps,dist_type", [(7, 0), (7, 1), (3, 0)])
+def test_tiled_task_packing(dev, ps, dist_type):
+    p = small_params(T=3, C=8, H=40 if ps == 7 else 42, W=48, ws=9, wt=1, ps=ps, k=10, dist_type=dist_type)
+    r = np.random.default_rng(9100 + ps + dist_type)
+    shp = (p["B"], p["T"], p["C"], p["H"], p["W"])
+    q = r.standard_normal(shp, dtype=np.float32)
+    k = r.standard_normal(shp, dtype=np.float32)
+    flows = _packing_flows(p, 9200 + ps)
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    torch.cuda.synchronize()
+    res = oracle.search(q, k, flows, p)
+    compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
+
+
 # Squared L2 through the tiled path (key stride 1): inner products from the
 # tiled kernel, key and query norm terms from their own kernel; border queries
 # (clipped patches), wide unions (norms read straight from memory) and every
