@@ -428,7 +428,9 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
               // bits 13..19 of the pack read 3 | 15 << 3 for an aligned item
               // with all four columns inside the frame: stored as loaded
               if (((pk >> 13) & 127) != (3 | (15 << 3))) {
-                const int sh = ((pk >> 13) & 7) - 3, mask = (pk >> 16) & 15;
+                int pkb = pk;
+                asm volatile("" : "+v"(pkb));  // selects from the pack here, not from masks kept in SGPRs
+                const int sh = ((pkb >> 13) & 7) - 3, mask = (pkb >> 16) & 15;
                 const unsigned v0 = stg[n].x, v1 = stg[n].y, v2 = stg[n].z, v3 = stg[n].w;
                 unsigned o[4];
 #pragma unroll
