@@ -117,8 +117,9 @@ typedef struct {
  *             stride1 = 1, ws <= 15 (inner product, any stride0) score every
  *             candidate into it (4 bytes per query row and candidate) before
  *             selecting; squared L2 adds the key-norm term of every
- *             candidate, the query norm of every row and five key pair
- *             products per key pixel, frame and head.  Its contents are not
+ *             candidate, the query norm of every row, five key pair
+ *             products per key pixel, frame and head and the squared norm
+ *             of every query pixel per frame and head.  Its contents are not
  *             needed between calls
  * Errors: SNLS_ERR_INVALID_ARG for shapes/parameters out of range or NULL
  * buffers; SNLS_ERR_UNSUPPORTED for k > SNLS_MAX_K; SNLS_ERR_WORKSPACE for a

@@ -27,6 +27,8 @@
 // plane values with the query's weights instead of four taps per channel.
 // Every term reads only planes of the position's own four taps, so a
 // non-finite key value reaches exactly the positions whose taps read it.
+// A sixth plane holds |q(y,x)|^2 of the query video, so Qn is a sum of
+// P^2 plane values per query.
 #include "snls_internal.h"
 
 namespace snls {
@@ -47,11 +49,13 @@ constexpr int VSUM = NQ * WSMAX * EG;  // per-query column sums
 constexpr int REGF = CC * RH * RP > GRIDS + VSUM ? CC * RH * RP : GRIDS + VSUM;
 }  // namespace l2n
 
-constexpr int NPLANE = 5;  // N, R, D, X, A
+constexpr int NKP = 5;     // key planes N, R, D, X, A
+constexpr int NPLANE = 6;  // ... and the query pixel norm |q|^2
 
-// Pair planes of one (b, t, head): one thread per key pixel.  Layout
-// planes[((b*T + t)*HD + hd)*5 + m][H][W].
-__global__ void __launch_bounds__(256) l2_pair_planes_kernel(const float* __restrict__ k, Geo g,
+// Pair planes of one (b, t, head): one thread per pixel.  Layout
+// planes[((b*T + t)*HD + hd)*6 + m][H][W], m = N, R, D, X, A of k, |q|^2.
+__global__ void __launch_bounds__(256) l2_pair_planes_kernel(const float* __restrict__ q,
+                                                             const float* __restrict__ k, Geo g,
                                                              float* __restrict__ planes) {
   const long long slab = blockIdx.y;  // (b*T + t)*HD + hd
   const long long pix = (long long)blockIdx.x * 256 + threadIdx.x;
@@ -61,8 +65,11 @@ __global__ void __launch_bounds__(256) l2_pair_planes_kernel(const float* __rest
   const int y = (int)(pix / g.W), x = (int)(pix % g.W);
   const bool rin = x + 1 < g.W, din = y + 1 < g.H;
   const float* kb = k + (bt * g.C + (long long)hd * g.Ch) * g.HW + pix;
-  float n = 0.f, r = 0.f, d = 0.f, xx = 0.f, a = 0.f;
-  for (int c = 0; c < g.Ch; ++c, kb += g.HW) {
+  const float* qb = q + (bt * g.C + (long long)hd * g.Ch) * g.HW + pix;
+  float n = 0.f, r = 0.f, d = 0.f, xx = 0.f, a = 0.f, qq = 0.f;
+  for (int c = 0; c < g.Ch; ++c, kb += g.HW, qb += g.HW) {
+    const float qv = qb[0];
+    qq = fmaf(qv, qv, qq);
     const float v00 = kb[0];
     const float v01 = rin ? kb[1] : 0.f;
     const float v10 = din ? kb[g.W] : 0.f;
@@ -79,6 +86,7 @@ __global__ void __launch_bounds__(256) l2_pair_planes_kernel(const float* __rest
   out[2 * g.HW] = d;
   out[3 * g.HW] = xx;
   out[4 * g.HW] = a;
+  out[5 * g.HW] = qq;
 }
 
 // One workgroup = a TY x TX tile of queries of one (b, head, t) and one
@@ -171,26 +179,26 @@ __global__ void __launch_bounds__(l2n::NT, 3) l2_norms_kernel(const float* __res
   static_assert(EG == 2 * TPQ && PPT == 2 * EG, "two grid columns per thread");
   // The tile's region of the five planes is staged at once when it fits;
   // otherwise each query's own EG x EG block, one plane at a time.
-  static_assert(NPLANE <= CC, "the planes fit in one chunk");
+  static_assert(NKP <= CC, "the key planes fit in one chunk");
   const int xx = tid & 63;  // region staging: lane = column, waves = rows
-  const int cpc = staged ? NPLANE : 1;
+  const int cpc = staged ? NKP : 1;
   const int bpitch = staged ? RP : EG, cstr = staged ? RH * RP : 0;
   const int qbase = staged ? qoy[jq] * RP + qox[jq] : jq * EG * EG;
   static_assert(NQ * EG * EG <= CC * RH * RP, "per-query blocks fit in the region buffer");
-  for (int m0 = 0; m0 < NPLANE; m0 += cpc) {
+  for (int m0 = 0; m0 < NKP; m0 += cpc) {
     __syncthreads();  // previous chunk fully read
     if (staged) {
       // the whole chunk's loads in flight before the LDS stores
-      float st[NPLANE][RH / (NT / 64)];
+      float st[NKP][RH / (NT / 64)];
 #pragma unroll
-      for (int m = 0; m < NPLANE; ++m)
+      for (int m = 0; m < NKP; ++m)
 #pragma unroll
         for (int i = 0; i < RH / (NT / 64); ++i) {
           const int yy = (tid >> 6) + (NT / 64) * i;
           st[m][i] = (xx < rw && yy < rh) ? kval(m, ry0 + yy, rx0 + xx) : 0.f;
         }
 #pragma unroll
-      for (int m = 0; m < NPLANE; ++m)
+      for (int m = 0; m < NKP; ++m)
 #pragma unroll
         for (int i = 0; i < RH / (NT / 64); ++i) {
           const int yy = (tid >> 6) + (NT / 64) * i;
@@ -206,7 +214,7 @@ __global__ void __launch_bounds__(l2n::NT, 3) l2_norms_kernel(const float* __res
     if (inside) {
       if (staged) {
 #pragma unroll
-        for (int m = 0; m < NPLANE; ++m) {
+        for (int m = 0; m < NKP; ++m) {
           const float* base = &reg[m * cstr + qbase];
 #pragma unroll
           for (int half = 0; half < 2; ++half) {
@@ -262,15 +270,14 @@ __global__ void __launch_bounds__(l2n::NT, 3) l2_norms_kernel(const float* __res
     grow[e] = sacc;
   }
   if (dt == 0) {
-    // |q|^2 over the in-frame patch pixels (once per query: the query frame's workgroup)
-    const float* qb = q + (((long long)b * g.T + t) * g.C + (long long)hd * g.Ch) * g.HW;
+    // |q|^2 over the in-frame patch pixels (once per query: the query
+    // frame's workgroup), from the query pixel-norm plane
+    const float* qpl = planes + ((((long long)b * g.T + t) * g.HD + hd) * NPLANE + NKP) * g.HW;
     float sq = 0.f;
     const int pw_n = jp1 - jp0 + 1, npix = (ip1 - ip0 + 1) * pw_n;
-    for (int e = sub; e < npix * g.Ch; e += TPQ) {
-      const int c = e / npix, pp = e % npix;
-      const int y = h + g.lo + ip0 + pp / pw_n, x = w + g.lo + jp0 + pp % pw_n;
-      const float qv = qb[(long long)c * g.HW + (long long)y * g.W + x];
-      sq = fmaf(qv, qv, sq);
+    for (int e = sub; e < npix; e += TPQ) {
+      const int y = h + g.lo + ip0 + e / pw_n, x = w + g.lo + jp0 + e % pw_n;
+      sq += qpl[(long long)y * g.W + x];
     }
     qpart[tid] = sq;
     // the query's TPQ threads are lanes of one wave: order its LDS accesses
@@ -296,7 +303,7 @@ snls_status launch_l2_norms(const float* q, const float* k, const float* flows, 
   if (ntile == 0 || g.rows == 0) return SNLS_OK;
   if (ntile > 0x7fffffffLL || (long long)g.B * g.HD * g.T > 65535 || 2 * g.wt + 1 > 65535) return SNLS_ERR_UNSUPPORTED;
   const dim3 pgrid((unsigned)((g.HW + 255) / 256), (unsigned)(g.B * g.T * g.HD));
-  hipLaunchKernelGGL(l2_pair_planes_kernel, pgrid, dim3(256), 0, s, k, g, planes);
+  hipLaunchKernelGGL(l2_pair_planes_kernel, pgrid, dim3(256), 0, s, q, k, g, planes);
   dim3 grid((unsigned)ntile, (unsigned)(g.B * g.HD * g.T), (unsigned)(2 * g.wt + 1));
   hipLaunchKernelGGL(l2_norms_kernel, grid, dim3(l2n::NT), 0, s, q, planes, flows, g, tiles_x, G, pitch, Qn);
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;

@@ -24,7 +24,9 @@
 // same 16-row halo, e.g. 5 x 4 at S_Q = 2):
 //  * 64 groups of 16 lanes; lane y of a group is halo row y (16 halo rows =
 //    tile rows + P - 1), a group owns one task = (shift row D_h, block of
-//    6 shift columns D_w);
+//    6 shift columns D_w) or one channel part of a task (tasks that would
+//    leave groups idle have their channels split, the parts summed before
+//    the tables are written);
 //  * per channel chunk the halo of q and the union region of K are staged
 //    in LDS (channel-major planes); each lane accumulates c for its halo row
 //    over all halo columns x and its 6 shifts (84 accumulators);

@@ -135,10 +135,10 @@ def test_search_workspace(lib):
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(p1)) == rows1 * 676 * 4  # 675 padded to 676
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, stride0=2, ws=17, k=30))) == 0
     # squared L2 (key stride 1): the scores, the key-norm terms, the query-norm
-    # terms and five key pair planes per frame and head
+    # terms, five key pair planes and the query pixel-norm plane per frame and head
     plane = (rows * 28 * 4 + 255) // 256 * 256
     a256 = lambda n: (n + 255) // 256 * 256
-    pairs = a256(5 * 1 * 3 * 2 * 16 * 17 * 4)
+    pairs = a256(6 * 1 * 3 * 2 * 16 * 17 * 4)
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(dist_type=1))) == \
         2 * plane + a256(rows * 4) + pairs
     assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, None, BIG, None) == B.SNLS_ERR_WORKSPACE
