@@ -731,8 +731,9 @@ __global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __rest
 // (at least k lanes hold a candidate >= T), and on scored rows only a few
 // more than k candidates reach it.  Those are compacted into one LDS slot
 // per lane and sorted by (score descending, id ascending) with a bitonic
-// network across the wave.  When more than 64 reach T, the exact k-th key
-// is found by bisection over the keys instead: every key above it plus the
+// network across the wave; 65 to 128 take two slots per lane and a
+// 128-entry network.  When more than 128 reach T, the exact k-th key is
+// found by bisection over the keys instead: every key above it plus the
 // smallest ids among the keys equal to it make exactly k entries.
 namespace wtk {
 constexpr int WAVES = 4;  // rows per workgroup
@@ -771,7 +772,7 @@ __global__ void __launch_bounds__(wtk::WAVES * 64) wave_topk_kernel(const float*
                                                                     const float* __restrict__ flows, Geo g,
                                                                     float* __restrict__ dists,
                                                                     float* __restrict__ inds) {
-  __shared__ unsigned long long slot[wtk::WAVES][64];
+  __shared__ unsigned long long slot[wtk::WAVES][128];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const long long row = (long long)blockIdx.x * wtk::WAVES + wv;
   if (row >= g.rows) return;  // whole wave
@@ -820,11 +821,13 @@ __global__ void __launch_bounds__(wtk::WAVES * 64) wave_topk_kernel(const float*
   };
   unsigned long long* sl = slot[wv];
   sl[lane] = 0ull;  // pads rank below every entry
+  sl[lane + 64] = 0ull;
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   auto entry = [&](unsigned key, int id) { return ((unsigned long long)key << 32) | (unsigned)(~id); };
-  if (count_ge(T1) <= 64) {
+  const int n1 = count_ge(T1);
+  if (n1 <= 128) {
     int base = 0;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
@@ -858,7 +861,34 @@ __global__ void __launch_bounds__(wtk::WAVES * 64) wave_topk_kernel(const float*
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  const unsigned long long best = sort64_desc(sl[lane], lane, shfl_xor64);
+  unsigned long long best;
+  if (n1 > 64 && n1 <= 128) {
+    // up to 128 entries, two per lane (entry lane + 64 h): bitonic sort of
+    // the 128, descending; the step across the halves is within the lane
+    unsigned long long x0 = sl[lane], x1 = sl[lane + 64];
+#pragma unroll
+    for (int size = 2; size <= 128; size <<= 1)
+#pragma unroll
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        if (stride == 64) {  // size 128: element i pairs with i + 64, larger first
+          const unsigned long long hi = x0 > x1 ? x0 : x1, lo = x0 > x1 ? x1 : x0;
+          x0 = hi;
+          x1 = lo;
+        } else {
+          const unsigned long long p0 = shfl_xor64(x0, stride), p1 = shfl_xor64(x1, stride);
+          // element i = lane + 64 h keeps the larger of the pair when the
+          // pair's order within its size-block is descending and it is the
+          // lower index, or ascending and it is the higher index
+          const bool low = (lane & stride) == 0;
+          const bool desc0 = (lane & size) == 0, desc1 = ((lane + 64) & size) == 0;
+          x0 = (low == desc0) ? (x0 > p0 ? x0 : p0) : (x0 < p0 ? x0 : p0);
+          x1 = (low == desc1) ? (x1 > p1 ? x1 : p1) : (x1 < p1 ? x1 : p1);
+        }
+      }
+    best = x0;  // ranks 0..63 are the first halves
+  } else {
+    best = sort64_desc(sl[lane], lane, shfl_xor64);
+  }
   if (lane >= g.k) return;
   // every candidate was ranked, so the k best are real candidates; the clamp
   // only keeps a placeholder id in bounds

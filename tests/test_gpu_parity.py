@@ -389,6 +389,22 @@ P1_CASES = [
 ]
 
 
+# The wave top-k's three selection paths on a smooth motion video (the
+# multi-head workload's settings at 40 x 56): about 94% of the rows have at
+# most 64 candidates at or above the first threshold, about 6% between 65
+# and 128 (two entries per lane, 128-entry sort) and 17 rows more than 128
+# (bisection for the exact k-th key); counts from the oracle's full rows.
+def test_wave_topk_paths(dev):
+    p = small_params(B=1, T=8, C=64, HD=4, H=40, W=56, ws=15, wt=3, ps=1, stride0=2, k=30)
+    x, flows = _motion_inputs(p, 3, 6.0)
+    gd, gi = B.snls_search(_d(x, dev), _d(x, dev), _d(flows, dev), p)
+    out = B.snls_aggregate(_d(x, dev), gd, gi, p, 1.0)
+    torch.cuda.synchronize()
+    res = oracle.search(x, x, flows, p)
+    compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
+    assert_close(_h(out), oracle.aggregate(x, _h(gd), _h(gi), p, 1.0), "aggregate (P = 1)")
+
+
 # Exact ties: 0/1 features and integer offsets make every score an exact
 # integer on both sides, so the order (score, then smaller id) must match the
 # oracle element for element -- the large-k selection's bisection path and
