@@ -95,7 +95,10 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
 
 // Candidate displacement disp = fl32(F + fl32(S_K * (d - r))), rounded once
 // per operation (no contraction), the fp32 convention of the outputs.
-SNLS_DEV float cand_disp(float F, float s1, int d, int r) { return __fadd_rn(F, __fmul_rn(s1, (float)(d - r))); }
+SNLS_DEV float cand_disp(float F, float s1, int d, int r) {
+#pragma clang fp contract(off)  // two roundings, never one fused multiply-add
+  return F + s1 * (float)(d - r);
+}
 
 // Centre (h + disp) inside [0, H-1]; exact: -h and H-1-h are exact in fp32.
 SNLS_DEV bool centre_ok(int h, float disp, int H) { return disp >= (float)(-h) && disp <= (float)(H - 1 - h); }

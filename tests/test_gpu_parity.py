@@ -263,6 +263,11 @@ TILE_CASES = _tile_cases() + [
     (small_params(T=3, C=8, H=23, W=25, ws=9, wt=1, ps=4, k=16, stride0=4), "edge"),
     (small_params(T=2, C=6, H=19, W=21, ws=8, wt=1, ps=6, k=20, stride0=2), "far"),
     (small_params(T=3, C=10, H=21, W=27, ws=9, wt=1, ps=2, k=10, stride0=5), "int"),
+    # a key stride whose products S_K * (d - r) are not exact in fp32: the
+    # displacement rounds twice (product, then sum), never as one fused
+    # multiply-add, on both sides
+    (small_params(T=3, C=8, H=23, W=26, ws=9, wt=1, ps=5, k=10, stride1=0.3), "frac"),
+    (small_params(T=2, C=6, H=19, W=22, ws=7, wt=1, ps=3, k=8, stride1=0.7, stride0=2), "smooth"),
 ]
 TILE_IDS = ["t%d-ws%d-wt%d-ps%d-sk%g-k%d-%s" % (i, p["ws"], p["wt"], p["ps"], p["stride1"], p["k"], kd)
             for i, (p, kd) in enumerate(TILE_CASES)]
