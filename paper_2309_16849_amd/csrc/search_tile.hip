@@ -536,31 +536,38 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
         }
       }
       __syncthreads();
-      // score of window cell (dh, dw) of query j from its box-sum table:
-      // bilinear taps at floor(disp), fraction disp - floor(disp)
-      auto cell_score = [&](int j, int h, int w, int dh, int dw) -> float {
-        const float disp_h = cand_disp(sm.qf_h[j], g.s1, dh, r);
-        const float disp_w = cand_disp(sm.qf_w[j], g.s1, dw, r);
-        const bool ok = centre_ok(h, disp_h, g.H) && centre_ok(w, disp_w, g.W);
-        const float fl_h = floorf(disp_h), fl_w = floorf(disp_w);
-        const float ah = disp_h - fl_h, aw = disp_w - fl_w;
-        // table reads only matter for valid cells
-        const float* r0p = &sm.bw[j * WIN + (ok ? (int)fl_h - sm.qlo_h[j] : 0) * WP];
-        const float* r1p = r0p + WP;
-        const int col = ok ? (int)fl_w - sm.qlo_w[j] : 0;
-        const float top = (1.f - aw) * r0p[col] + aw * r0p[col + 1];
-        const float bot = (1.f - aw) * r1p[col] + aw * r1p[col + 1];
-        const float dv = (1.f - ah) * top + ah * bot;
-        return ok && dv == dv ? dv : -INFINITY;  // NaN scores as invalid
-      };
       // ---- 4-tap combination and exact validity ----
+      // Score of window cell (dh, dw) of query j from its box-sum table:
+      // bilinear taps at floor(disp), fraction disp - floor(disp).  One
+      // thread takes a window row; what depends only on the row (its
+      // displacement, validity, table row and the query's offsets) is set up
+      // once for the row's cells.
       for (int e = tid; e < qn * ws; e += NTHREADS) {
         const int j = e / ws, dh = e % ws;
         const int mh = my0 + j / tqw, mw = mx0 + j % tqw;
         if (mh >= g.nH || mw >= g.nW) continue;
         const int h = mh * s0, w = mw * s0;
         float* srow = scores + ((rowb + mh) * g.nW + mw) * pitch + cbase + dh * ws;
-        for (int dw = 0; dw < ws; ++dw) srow[dw] = cell_score(j, h, w, dh, dw);
+        const float fw = sm.qf_w[j];
+        const int lw = sm.qlo_w[j];
+        const float disp_h = cand_disp(sm.qf_h[j], g.s1, dh, r);
+        const bool okh = centre_ok(h, disp_h, g.H);
+        const float fl_h = floorf(disp_h), ah = disp_h - fl_h;
+        // table reads only matter for valid cells (row 0 / column 0 otherwise)
+        const float* r0p = &sm.bw[j * WIN + (okh ? (int)fl_h - sm.qlo_h[j] : 0) * WP];
+        const float* r1p = r0p + WP;
+        for (int dw = 0; dw < ws; ++dw) {
+          {
+            const float disp_w = cand_disp(fw, g.s1, dw, r);
+            const bool ok = okh && centre_ok(w, disp_w, g.W);
+            const float fl_w = floorf(disp_w), aw = disp_w - fl_w;
+            const int col = ok ? (int)fl_w - lw : 0;
+            const float top = (1.f - aw) * r0p[col] + aw * r0p[col + 1];
+            const float bot = (1.f - aw) * r1p[col] + aw * r1p[col + 1];
+            const float dv = (1.f - ah) * top + ah * bot;
+            srow[dw] = ok && dv == dv ? dv : -INFINITY;  // NaN scores as invalid
+          }
+        }
       }
     } else {
       // Union too wide for the LDS layout: score this frame directly.
