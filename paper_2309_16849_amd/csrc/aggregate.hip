@@ -329,7 +329,10 @@ static_assert(MAXREC <= WAVES * 64 * (TX + 1), "the covering queries' scores fit
 SNLS_DEV int floor_div(int a, int s) { return a >= 0 ? a / s : -((-a + s - 1) / s); }
 
 // SQ: the query stride when known at compile time (1), else 0 (g.s0).
-template <int SQ>
+// GW: bin positions gathered per pass (their channel-vector loads in flight
+// together): 4 for patches up to 5 x 5, 2 for larger ones (measured faster
+// each way on the 256 x 256 P = 3 and 480 x 854 P = 7 workloads).
+template <int SQ, int GW>
 __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* __restrict__ vcl,
                                                                   const float* __restrict__ dists,
                                                                   const float* __restrict__ inds, Geo g,
@@ -589,21 +592,34 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
       const int off = ((t + s - g.wt) * (int)g.HW + Y * g.W + X) * g.C;
       const float wgt = (float)v * (1.f / QSCALE);
       unsigned long long m = __ballot(nz);
-      // up to 8 positions per pass, their loads in flight together
+      // up to GW positions per pass (in bin order), their loads in flight
+      // together; the pass's count n is wave-uniform, and a padded slot
+      // re-reads the first position and adds nothing
       while (m) {
-        const int s0 = __ffsll((long long)m) - 1;
-        m &= m - 1;
-        const int s1 = m ? __ffsll((long long)m) - 1 : s0;
-        const bool two = m != 0;
-        if (two) m &= m - 1;
-        const float w0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wgt), s0));
-        const int o0 = __builtin_amdgcn_readlane(off, s0);
-        const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wgt), s1));
-        const int o1 = __builtin_amdgcn_readlane(off, s1);
+        int sl[GW];
+        int n = 0;
+#pragma unroll
+        for (int i = 0; i < GW; ++i) {
+          sl[i] = m ? __ffsll((long long)m) - 1 : sl[0];
+          if (m) {
+            m &= m - 1;
+            ++n;
+          }
+        }
+        float wv[GW];
+        int ov[GW];
+#pragma unroll
+        for (int i = 0; i < GW; ++i) {
+          wv[i] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wgt), sl[i]));
+          ov[i] = __builtin_amdgcn_readlane(off, sl[i]);
+        }
         if (lane < g.Ch) {
-          const float a0 = vb[o0 + lane], a1 = vb[o1 + lane];
-          acc = fmaf(w0, a0, acc);
-          if (two) acc = fmaf(w1, a1, acc);
+          float a[GW];
+#pragma unroll
+          for (int i = 0; i < GW; ++i) a[i] = vb[ov[i] + lane];
+#pragma unroll
+          for (int i = 0; i < GW; ++i)
+            if (i < n) acc = fmaf(wv[i], a[i], acc);
         }
       }
     }
@@ -889,12 +905,17 @@ snls_status launch_aggregate(const float* v, const float* dists, const float* in
     const int tiles_x = (g.W + aggt::TX - 1) / aggt::TX, tiles_y = (g.H + aggt::TY - 1) / aggt::TY;
     const long long nwg = (long long)tiles_x * tiles_y * g.B * g.T * g.HD;
     if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
-    if (g.s0 == 1)
-      hipLaunchKernelGGL(aggregate_tile_kernel<1>, dim3((unsigned)nwg), dim3(aggt::NT), 0, s, vcl, dists, inds, g,
-                         scale, tiles_x, tiles_y, out);
-    else
-      hipLaunchKernelGGL(aggregate_tile_kernel<0>, dim3((unsigned)nwg), dim3(aggt::NT), 0, s, vcl, dists, inds, g,
-                         scale, tiles_x, tiles_y, out);
+#define SNLS_AGGT(SQ, GW)                                                                                    \
+  hipLaunchKernelGGL((aggregate_tile_kernel<SQ, GW>), dim3((unsigned)nwg), dim3(aggt::NT), 0, s, vcl, dists, inds, \
+                     g, scale, tiles_x, tiles_y, out)
+    if (g.s0 == 1) {
+      if (g.ps <= 5) SNLS_AGGT(1, 4);
+      else SNLS_AGGT(1, 2);
+    } else {
+      if (g.ps <= 5) SNLS_AGGT(0, 4);
+      else SNLS_AGGT(0, 2);
+    }
+#undef SNLS_AGGT
     return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
   }
   {
