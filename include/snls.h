@@ -51,6 +51,10 @@
  *    k~ is the bilinear read of frame t+dt at (h+p_h+disp_h, w+p_w+disp_w)
  *    with taps outside the frame reading 0.
  *  - inds entries are (frame t+dt, disp_h, disp_w) stored as fp32.
+ *  - H and W must be below 1,000,000 (SNLS_ERR_UNSUPPORTED otherwise), so a
+ *    displacement of magnitude 1e6 or more leaves every frame: a neighbour
+ *    carrying one (aggregation, backward) contributes nothing, exactly as
+ *    its out-of-frame bilinear reads would give.
  *  - On an argument error the call returns before touching any buffer or
  *    launching anything.
  */

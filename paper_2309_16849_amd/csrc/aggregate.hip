@@ -64,8 +64,8 @@ __global__ void __launch_bounds__(256) softmax_weights_kernel(const float* __res
   const float inv = z > 0.f ? 1.f / z : 0.f;
   for (int l = sub; l < g.k; l += G) {
     const float tf = ind[3 * l], dh = ind[3 * l + 1], dw = ind[3 * l + 2];
-    const bool ok = isfinite(d[l]) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < 1.0e6f &&
-                    fabsf(dw) < 1.0e6f;
+    const bool ok = isfinite(d[l]) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < kFarDisp &&
+                    fabsf(dw) < kFarDisp;
     wts[row * g.k + l] = ok ? expf(sscale * d[l] - m) * inv : 0.f;
   }
 }
@@ -405,8 +405,8 @@ __global__ void __launch_bounds__(aggt::NT) aggregate_tile_kernel(const float* _
     const float d = lds ? dq[e] : dists[row * K + l];
     const float* ind = inds + (row * K + l) * 3;
     const float tf = ind[0], dh = ind[1], dw = ind[2];
-    const bool ok = isfinite(d) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < 1.0e6f &&
-                    fabsf(dw) < 1.0e6f;
+    const bool ok = isfinite(d) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < kFarDisp &&
+                    fabsf(dw) < kFarDisp;
     if (!ok) return;
     wl = expf(sscale * d - qm[j]) * qinv[j];
     t2 = (int)tf;
@@ -709,8 +709,8 @@ __global__ void __launch_bounds__(256) aggregate_p1_kernel(const float* __restri
     const float inv = z > 0.f ? 1.f / z : 0.f;
     for (int l = 0; l < k; ++l) {
       const float tf = ind[3 * l], dh = ind[3 * l + 1], dw = ind[3 * l + 2];
-      const bool ok = isfinite(d[l]) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < 1.0e6f &&
-                      fabsf(dw) < 1.0e6f;
+      const bool ok = isfinite(d[l]) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < kFarDisp &&
+                      fabsf(dw) < kFarDisp;
       d[l] = ok ? expf(sscale * d[l] - m) * inv : 0.f;
     }
   }

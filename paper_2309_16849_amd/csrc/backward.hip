@@ -76,7 +76,7 @@ SNLS_DEV bool neighbour(const float* __restrict__ irow, int l, const Geo& g, int
   float tf = irow[3 * l + 0];
   if (!(tf >= 0.f && tf < (float)g.T) || tf != floorf(tf)) return false;
   float dh = irow[3 * l + 1], dw = irow[3 * l + 2];
-  if (!(fabsf(dh) < 4.0e6f && fabsf(dw) < 4.0e6f)) return false;
+  if (!(fabsf(dh) < kFarDisp && fabsf(dw) < kFarDisp)) return false;
   *t2 = (int)tf;
   split_disp(dh, ny, ay);
   split_disp(dw, nx, ax);

@@ -125,7 +125,7 @@ __global__ void __launch_bounds__(l2n::NT, 3) l2_norms_kernel(const float* __res
   }
   // non-finite or absurd offsets: their candidates are invalid (the inner
   // product pass scores them so); any G value does
-  const float fh_u = fabsf(fh) < 1.0e6f ? fh : 0.f, fw_u = fabsf(fw) < 1.0e6f ? fw : 0.f;
+  const float fh_u = fabsf(fh) < kFarDisp ? fh : 0.f, fw_u = fabsf(fw) < kFarDisp ? fw : 0.f;
   const float flh = floorf(fh_u), flw = floorf(fw_u);
   const int oy = h + g.lo + (int)flh - g.r, ox = w + g.lo + (int)flw - g.r;  // key coords of grid (0, 0)
   if (tid < 4) ubox[tid] = (tid & 1) ? INT_MIN : INT_MAX;

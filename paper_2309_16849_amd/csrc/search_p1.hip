@@ -80,7 +80,7 @@ __global__ void __launch_bounds__(p1::NT, 8) search_p1_scores_kernel(const float
   const int drow = min(dh, g.ws - 1);
   const float disp_h = cand_disp(fh, g.s1, drow, g.r);
   const float disp_w0 = cand_disp(fw, g.s1, 0, g.r);
-  const bool sane = fabsf(fh) < 1.0e6f && fabsf(fw) < 1.0e6f;
+  const bool sane = fabsf(fh) < kFarDisp && fabsf(fw) < kFarDisp;
   const int below = dh == g.ws ? 1 : 0;  // the row under the last window row
   const int y0 = (sane ? h + (int)floorf(disp_h) : h) + below;
   const int x0 = sane ? w + (int)floorf(disp_w0) : w;

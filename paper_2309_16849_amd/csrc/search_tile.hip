@@ -275,7 +275,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
       // for its first .. last cell (disp grows with the cell index).
       // Offsets that are not finite or absurdly large count as zero here;
       // their candidates fail the exact validity test below.
-      const float fh_u = fabsf(fh) < 1.0e6f ? fh : 0.f, fw_u = fabsf(fw) < 1.0e6f ? fw : 0.f;
+      const float fh_u = fabsf(fh) < kFarDisp ? fh : 0.f, fw_u = fabsf(fw) < kFarDisp ? fw : 0.f;
       const int lo_h = (int)floorf(cand_disp(fh_u, g.s1, 0, r));
       const int hi_h = (int)floorf(cand_disp(fh_u, g.s1, ws - 1, r)) + 1;
       const int lo_w = (int)floorf(cand_disp(fw_u, g.s1, 0, r));
@@ -315,11 +315,23 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
     }
     __syncthreads();
     // (uniform values: kept in scalar registers)
-    const int u0 = __builtin_amdgcn_readfirstlane(sm.uni[0]), u1 = __builtin_amdgcn_readfirstlane(sm.uni[1]);
-    const int u2 = __builtin_amdgcn_readfirstlane(sm.uni[2]), u3 = __builtin_amdgcn_readfirstlane(sm.uni[3]);
+    // Only shifts that a valid cell can read matter: a valid cell of a query
+    // at row h has h + disp in [0, H-1], so its taps lie in rows
+    // [-h, H - h]; over the tile's queries that is [-h_last, H - y0] (and
+    // likewise for columns).  Clipping the union to that range bounds the
+    // rounds of a tile whose offsets are spread far outside the frame.
+    const int h_last = min(y0 + (tqh - 1) * s0, (g.nH - 1) * s0);
+    const int w_last = min(x0 + (tqw - 1) * s0, (g.nW - 1) * s0);
+    const int u0 = max(__builtin_amdgcn_readfirstlane(sm.uni[0]), -h_last);
+    const int u1 = min(__builtin_amdgcn_readfirstlane(sm.uni[1]), g.H - y0);
+    const int u2 = max(__builtin_amdgcn_readfirstlane(sm.uni[2]), -w_last);
+    const int u3 = min(__builtin_amdgcn_readfirstlane(sm.uni[3]), g.W - x0);
     const int dmin_h = u0, UH = u1 - u0 + 1;
     const int dmin_w = u2, UW = u3 - u2 + 1;
-    const int nblk = (UW + S - 1) / S;
+    // no shift left: every cell of the frame is invalid (the 4-tap pass below
+    // scores them so without reading the tables)
+    const bool none = UH <= 0 || UW <= 0;
+    const int nblk = none ? 0 : (UW + S - 1) / S;
 
     if (nblk <= MAXBLK) {
       // A task is (shift row, column block); a round covers as many shift
@@ -332,8 +344,8 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
       // its own) as far as the 64 groups allow: the full quads first, then
       // the tail, which would otherwise keep whole waves busy for one row.
       const int span_max = KR - HROWS + 1;
-      const int rows_per_round = min(span_max, NGROUP / nblk);
-      for (int rr0 = 0; rr0 < UH; rr0 += rows_per_round) {
+      const int rows_per_round = none ? 1 : min(span_max, NGROUP / nblk);
+      for (int rr0 = 0; rr0 < (none ? 0 : UH); rr0 += rows_per_round) {
         const int nrows = min(rows_per_round, UH - rr0);
         const int uf = nblk * (nrows >> 2);  // whole quads: waves per channel part
         const int tt = nblk * (nrows & 3);   // tail tasks
@@ -570,7 +582,12 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
         }
       }
     } else {
-      // Union too wide for the LDS layout: score this frame directly.
+      // Union too wide for the LDS layout: score this frame directly.  The
+      // workspace holds inner products for both distances (the top-k pass
+      // forms the squared L2 distance from them and the norm terms), so the
+      // direct scores are inner products too.
+      Geo gp = g;
+      gp.dist = SNLS_DIST_PROD;
       __syncthreads();
       for (int e = tid; e < qn * ws; e += NTHREADS) {
         const int j = e / ws, dh = e % ws;
@@ -583,7 +600,7 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
         for (int dw = 0; dw < ws; ++dw) {
           const float disp_w = cand_disp(fw, g.s1, dw, r);
           float d = -INFINITY;
-          if (okh && centre_ok(w, disp_w, g.W)) d = score_candidate(q, k, g, b, hd, t, h, w, t2, disp_h, disp_w);
+          if (okh && centre_ok(w, disp_w, g.W)) d = score_candidate(q, k, gp, b, hd, t, h, w, t2, disp_h, disp_w);
           scores[((rowb + mh) * g.nW + mw) * pitch + cbase + dh * ws + dw] = d;
         }
       }

@@ -29,6 +29,13 @@ struct Geo {
   long long rows;  // B*HD*T*nH*nW query rows
 };
 
+// Offsets and displacements of magnitude kFarDisp or more lie outside every
+// frame (check_params limits H and W to below it): every tap of such a read
+// is out of the frame, so such a neighbour contributes nothing and its
+// window needs no key region.  One constant for the forward and backward
+// kernels.
+constexpr float kFarDisp = 1.0e6f;
+
 // Host-side checks (validate.cpp).  Return SNLS_OK or an error code; they
 // never touch the GPU.
 snls_status check_params(const snls_params* p, bool need_k, Geo* g);
@@ -92,6 +99,7 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
 // ---------------------------------------------------------------- device --
 
 #define SNLS_DEV __device__ __forceinline__
+
 
 // Candidate displacement disp = fl32(F + fl32(S_K * (d - r))), rounded once
 // per operation (no contraction), the fp32 convention of the outputs.

@@ -21,6 +21,8 @@ snls_status check_params(const snls_params* p, bool need_k, Geo* g) {
   if (!(p->stride1 > 0.f) || !isfinite(p->stride1)) return SNLS_ERR_INVALID_ARG;
   if (p->dist_type != SNLS_DIST_PROD && p->dist_type != SNLS_DIST_L2) return SNLS_ERR_INVALID_ARG;
   if ((long long)p->H * p->W > kMaxPlane) return SNLS_ERR_UNSUPPORTED;
+  // displacements of kFarDisp or more must leave every frame
+  if (p->H >= (long long)kFarDisp || p->W >= (long long)kFarDisp) return SNLS_ERR_UNSUPPORTED;
   if (p->ws > 255 || p->ps > 255 || p->wt > 63) return SNLS_ERR_UNSUPPORTED;
   long long ncand = (long long)(2 * p->wt + 1) * p->ws * p->ws;
   if (ncand > INT_MAX / 4) return SNLS_ERR_UNSUPPORTED;

@@ -63,6 +63,18 @@ def test_search_rejects_bad_params(lib, kw):
     assert st == B.SNLS_ERR_INVALID_ARG
 
 
+def test_frame_side_limit(lib):
+    """H or W of 1,000,000 or more is rejected: displacements of that
+    magnitude must leave every frame (one cut-off for every kernel)."""
+    for kw in (dict(H=1000000, W=1), dict(H=1, W=1000000)):
+        prm = _params(**kw)
+        st = lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, FAKE, BIG, None)
+        assert st == B.SNLS_ERR_UNSUPPORTED, kw
+        assert lib.snls_workspace_size(B.SNLS_OP_AGGREGATE, ctypes.byref(prm)) == ctypes.c_size_t(-1).value
+    prm = _params(H=999999, W=1, ws=1, wt=0, ps=1, k=1)
+    assert lib.snls_workspace_size(B.SNLS_OP_AGGREGATE, ctypes.byref(prm)) != ctypes.c_size_t(-1).value
+
+
 def test_search_rejects_bad_struct_size_and_nulls(lib):
     prm = _params()
     prm.struct_size = 12

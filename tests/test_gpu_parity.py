@@ -268,6 +268,11 @@ TILE_CASES = _tile_cases() + [
     # multiply-add, on both sides
     (small_params(T=3, C=8, H=23, W=26, ws=9, wt=1, ps=5, k=10, stride1=0.3), "frac"),
     (small_params(T=2, C=6, H=19, W=22, ws=7, wt=1, ps=3, k=8, stride1=0.7, stride0=2), "smooth"),
+    # one query per tile 37 rows below its neighbours, one 5000 rows outside
+    # the frame: the shift union is clipped to rows a valid cell can read
+    (small_params(T=3, C=8, H=64, W=40, ws=9, wt=1, ps=7, k=10), "vspread"),
+    (small_params(T=2, C=8, H=61, W=33, ws=5, wt=1, ps=3, k=8, stride1=0.5), "vspread"),
+    (small_params(T=3, C=8, H=30, W=56, ws=9, wt=1, ps=5, k=10), "split"),
 ]
 TILE_IDS = ["t%d-ws%d-wt%d-ps%d-sk%g-k%d-%s" % (i, p["ws"], p["wt"], p["ps"], p["stride1"], p["k"], kd)
             for i, (p, kd) in enumerate(TILE_CASES)]
@@ -282,6 +287,16 @@ def _tile_flows(p, kind, r):
         return r.uniform(-7, 7, fshp).astype(np.float32)
     if kind == "far":  # +-60 px: the union exceeds the LDS layout
         return (r.choice([-1.0, 1.0], fshp) * 60.0 + r.uniform(-1, 1, fshp)).astype(np.float32)
+    if kind == "split":  # column offsets of +-12 px alternating along each row: a union wider than 30 shifts
+        fl = r.uniform(-0.5, 0.5, fshp)
+        sign = np.where(np.arange(p["W"]) % 2 == 0, -1.0, 1.0)
+        fl[:, :, :, 1] += 12.0 * sign
+        return fl.astype(np.float32)
+    if kind == "vspread":  # small offsets, but one query per tile far below and one far outside the frame
+        fl = r.uniform(-2, 2, fshp)
+        fl[:, :, :, 0, 0::10, 0::8] = 37.25
+        fl[:, :, :, 0, 5::10, 3::8] = -5000.5
+        return fl.astype(np.float32)
     if kind == "int":
         return r.integers(-3, 4, fshp).astype(np.float32)
     if kind == "edge":  # just below integers: adding a cell offset can round up to the next integer
@@ -361,6 +376,11 @@ L2_TILE_CASES = [
     (small_params(T=3, C=16, H=25, W=30, ws=9, wt=1, ps=7, k=10, dist_type=1), "far"),
     (small_params(T=3, C=16, H=33, W=35, ws=9, wt=1, ps=7, k=10, dist_type=1, stride0=2), "smooth"),
     (small_params(T=2, C=8, H=27, W=22, ws=5, wt=1, ps=3, k=20, dist_type=1, stride0=3), "frac"),
+    # in-frame candidates in tiles whose union is too wide for the LDS layout
+    # (+-12 px alternating column offsets): scored per candidate as inner
+    # products, ranked by the squared L2 distance
+    (small_params(T=3, C=8, H=26, W=56, ws=9, wt=1, ps=7, k=10, dist_type=1), "split"),
+    (small_params(T=3, C=8, H=64, W=40, ws=9, wt=1, ps=7, k=10, dist_type=1), "vspread"),
 ]
 
 
