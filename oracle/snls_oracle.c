@@ -43,6 +43,7 @@
  *    patches that cover it, pixels that no patch covers are 0.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -399,15 +400,95 @@ void oracle_search_fixed(const double* q, const double* k, const double* flows, 
  * Sec. 3.2), by the chain rule through aggregation, softmax, similarity and
  * the bilinear reads, for the selected candidates (the top-k set is held
  * constant).  grad_out: (B,T,C,H,W); grad_dists: (B,HD,T,nH,nW,k) or NULL.
- * Every gradient array is overwritten.  grad_flows: (B,T,2wt,2,H,W). */
+ * Every gradient array is overwritten.  grad_flows: (B,T,2wt,2,H,W).
+ *
+ * The query rows are split over OpenMP threads; each thread adds its rows'
+ * terms into gradient arrays of its own, which are summed in thread order at
+ * the end (the per-row arithmetic is the same as in a single pass). */
+static void backward_row(const double* q, const double* k, const double* v, const double* dists,
+                         const double* inds, const double* grad_out, const double* grad_dists,
+                         const oracle_params* p, double scale, const double* cnt, int64_t row, double* wts,
+                         double* G, double* grad_q, double* grad_k, double* grad_v, double* grad_flows) {
+  int Ch = p->C / p->HD, lo = patch_lo(p), kk = p->k;
+  double sign = p->dist_type == 0 ? 1.0 : -1.0;
+  int b, hd, t, h, w;
+  query_coords(p, row, &b, &hd, &t, &h, &w);
+  softmax_row(dists + row * kk, kk, p->dist_type, scale, wts);
+  /* aggregation: out = sum_l w_l vtilde_l / cnt */
+  for (int l = 0; l < kk; l++) {
+    G[l] = 0.0;
+    const double* ind = inds + 3 * (row * kk + l);
+    int tk = neighbour_frame(p, ind[0]);
+    if (tk < 0 || !isfinite(dists[row * kk + l])) continue;
+    double ddisp_h = 0.0, ddisp_w = 0.0;
+    for (int ph = lo; ph < lo + p->ps; ph++)
+      for (int pw = lo; pw < lo + p->ps; pw++) {
+        int y = h + ph, x = w + pw;
+        if (y < 0 || y >= p->H || x < 0 || x >= p->W) continue;
+        double n = cnt[(((int64_t)b * p->T + t) * p->H + y) * p->W + x];
+        double yv = (double)y + ind[1], xv = (double)x + ind[2];
+        for (int c = hd * Ch; c < (hd + 1) * Ch; c++) {
+          double g = grad_out[vid_index(p, b, t, c, y, x)] / n;
+          G[l] += g * bilinear(v, p, b, tk, c, yv, xv);
+          bilinear_scatter(grad_v, p, b, tk, c, yv, xv, wts[l] * g);
+          double gy, gx;
+          bilinear_grad(v, p, b, tk, c, yv, xv, &gy, &gx);
+          ddisp_h += wts[l] * g * gy;
+          ddisp_w += wts[l] * g * gx;
+        }
+      }
+    if (tk != t) {
+      int slot = flow_slot(p, tk - t);
+      grad_flows[flow_index(p, b, t, slot, 0, h, w)] += ddisp_h;
+      grad_flows[flow_index(p, b, t, slot, 1, h, w)] += ddisp_w;
+    }
+  }
+  /* softmax backward, then the similarity of each selected candidate */
+  double wg = 0.0;
+  for (int l = 0; l < kk; l++) wg += wts[l] * G[l];
+  for (int l = 0; l < kk; l++) {
+    const double* ind = inds + 3 * (row * kk + l);
+    int tk = neighbour_frame(p, ind[0]);
+    if (tk < 0 || !isfinite(dists[row * kk + l])) continue;
+    double dd = sign * scale * wts[l] * (G[l] - wg);
+    if (grad_dists) dd += grad_dists[row * kk + l];
+    if (dd == 0.0) continue;
+    double ddisp_h = 0.0, ddisp_w = 0.0;
+    for (int ph = lo; ph < lo + p->ps; ph++)
+      for (int pw = lo; pw < lo + p->ps; pw++) {
+        int y = h + ph, x = w + pw;
+        if (y < 0 || y >= p->H || x < 0 || x >= p->W) continue;
+        double yk = (double)y + ind[1], xk = (double)x + ind[2];
+        for (int c = hd * Ch; c < (hd + 1) * Ch; c++) {
+          double qv = q[vid_index(p, b, t, c, y, x)];
+          double kv = bilinear(k, p, b, tk, c, yk, xk);
+          double dq, dkv;
+          if (p->dist_type == 0) { dq = dd * kv; dkv = dd * qv; }
+          else { dq = 2.0 * dd * (qv - kv); dkv = -2.0 * dd * (qv - kv); }
+          grad_q[vid_index(p, b, t, c, y, x)] += dq;
+          bilinear_scatter(grad_k, p, b, tk, c, yk, xk, dkv);
+          double gy, gx;
+          bilinear_grad(k, p, b, tk, c, yk, xk, &gy, &gx);
+          ddisp_h += dkv * gy;
+          ddisp_w += dkv * gx;
+        }
+      }
+    if (tk != t) {
+      int slot = flow_slot(p, tk - t);
+      grad_flows[flow_index(p, b, t, slot, 0, h, w)] += ddisp_h;
+      grad_flows[flow_index(p, b, t, slot, 1, h, w)] += ddisp_w;
+    }
+  }
+}
+
 void oracle_backward(const double* q, const double* k, const double* v, const double* flows,
                      const double* dists, const double* inds, const double* grad_out, const double* grad_dists,
                      const oracle_params* p, double scale, double* grad_q, double* grad_k, double* grad_v,
                      double* grad_flows) {
-  int nH = grid_h(p), nW = grid_w(p), Ch = p->C / p->HD, lo = patch_lo(p), kk = p->k;
+  int nH = grid_h(p), nW = grid_w(p), lo = patch_lo(p), kk = p->k;
   int64_t nvid = (int64_t)p->B * p->T * p->C * p->H * p->W;
   int64_t nflow = (int64_t)p->B * p->T * 2 * p->wt * 2 * p->H * p->W;
-  double sign = p->dist_type == 0 ? 1.0 : -1.0;
+  int64_t rows = (int64_t)p->B * p->HD * p->T * nH * nW;
   (void)flows;
   memset(grad_q, 0, sizeof(double) * (size_t)nvid);
   memset(grad_k, 0, sizeof(double) * (size_t)nvid);
@@ -427,84 +508,46 @@ void oracle_backward(const double* q, const double* k, const double* v, const do
               cnt[(((int64_t)b * p->T + t) * p->H + y) * p->W + x] += 1.0;
             }
 
-  double* wts = (double*)malloc(sizeof(double) * (size_t)kk);
-  double* G = (double*)malloc(sizeof(double) * (size_t)kk);
-  for (int b = 0; b < p->B; b++)
-    for (int hd = 0; hd < p->HD; hd++)
-      for (int t = 0; t < p->T; t++)
-        for (int mh = 0; mh < nH; mh++)
-          for (int mw = 0; mw < nW; mw++) {
-            int h = mh * p->stride0, w = mw * p->stride0;
-            int64_t row = ((((int64_t)b * p->HD + hd) * p->T + t) * nH + mh) * nW + mw;
-            softmax_row(dists + row * kk, kk, p->dist_type, scale, wts);
-            /* aggregation: out = sum_l w_l vtilde_l / cnt */
-            for (int l = 0; l < kk; l++) {
-              G[l] = 0.0;
-              const double* ind = inds + 3 * (row * kk + l);
-              int tk = neighbour_frame(p, ind[0]);
-              if (tk < 0 || !isfinite(dists[row * kk + l])) continue;
-              double ddisp_h = 0.0, ddisp_w = 0.0;
-              for (int ph = lo; ph < lo + p->ps; ph++)
-                for (int pw = lo; pw < lo + p->ps; pw++) {
-                  int y = h + ph, x = w + pw;
-                  if (y < 0 || y >= p->H || x < 0 || x >= p->W) continue;
-                  double n = cnt[(((int64_t)b * p->T + t) * p->H + y) * p->W + x];
-                  double yv = (double)y + ind[1], xv = (double)x + ind[2];
-                  for (int c = hd * Ch; c < (hd + 1) * Ch; c++) {
-                    double g = grad_out[vid_index(p, b, t, c, y, x)] / n;
-                    G[l] += g * bilinear(v, p, b, tk, c, yv, xv);
-                    bilinear_scatter(grad_v, p, b, tk, c, yv, xv, wts[l] * g);
-                    double gy, gx;
-                    bilinear_grad(v, p, b, tk, c, yv, xv, &gy, &gx);
-                    ddisp_h += wts[l] * g * gy;
-                    ddisp_w += wts[l] * g * gx;
-                  }
-                }
-              if (tk != t) {
-                int slot = flow_slot(p, tk - t);
-                grad_flows[flow_index(p, b, t, slot, 0, h, w)] += ddisp_h;
-                grad_flows[flow_index(p, b, t, slot, 1, h, w)] += ddisp_w;
-              }
-            }
-            /* softmax backward, then the similarity of each selected candidate */
-            double wg = 0.0;
-            for (int l = 0; l < kk; l++) wg += wts[l] * G[l];
-            for (int l = 0; l < kk; l++) {
-              const double* ind = inds + 3 * (row * kk + l);
-              int tk = neighbour_frame(p, ind[0]);
-              if (tk < 0 || !isfinite(dists[row * kk + l])) continue;
-              double dd = sign * scale * wts[l] * (G[l] - wg);
-              if (grad_dists) dd += grad_dists[row * kk + l];
-              if (dd == 0.0) continue;
-              double ddisp_h = 0.0, ddisp_w = 0.0;
-              for (int ph = lo; ph < lo + p->ps; ph++)
-                for (int pw = lo; pw < lo + p->ps; pw++) {
-                  int y = h + ph, x = w + pw;
-                  if (y < 0 || y >= p->H || x < 0 || x >= p->W) continue;
-                  double yk = (double)y + ind[1], xk = (double)x + ind[2];
-                  for (int c = hd * Ch; c < (hd + 1) * Ch; c++) {
-                    double qv = q[vid_index(p, b, t, c, y, x)];
-                    double kv = bilinear(k, p, b, tk, c, yk, xk);
-                    double dq, dkv;
-                    if (p->dist_type == 0) { dq = dd * kv; dkv = dd * qv; }
-                    else { dq = 2.0 * dd * (qv - kv); dkv = -2.0 * dd * (qv - kv); }
-                    grad_q[vid_index(p, b, t, c, y, x)] += dq;
-                    bilinear_scatter(grad_k, p, b, tk, c, yk, xk, dkv);
-                    double gy, gx;
-                    bilinear_grad(k, p, b, tk, c, yk, xk, &gy, &gx);
-                    ddisp_h += dkv * gy;
-                    ddisp_w += dkv * gx;
-                  }
-                }
-              if (tk != t) {
-                int slot = flow_slot(p, tk - t);
-                grad_flows[flow_index(p, b, t, slot, 0, h, w)] += ddisp_h;
-                grad_flows[flow_index(p, b, t, slot, 1, h, w)] += ddisp_w;
-              }
-            }
-          }
-  free(G);
-  free(wts);
+  /* private gradient arrays: at most about 8 GB of them in total */
+  int64_t per_thread = (3 * nvid + nflow) * (int64_t)sizeof(double);
+  int nthr = omp_get_max_threads();
+  int64_t cap = per_thread > 0 ? (int64_t)8000000000LL / per_thread : nthr;
+  if (cap < 1) cap = 1;
+  if (nthr > cap) nthr = (int)cap;
+  if ((int64_t)nthr > rows) nthr = rows > 0 ? (int)rows : 1;
+  double** priv = (double**)calloc((size_t)nthr, sizeof(double*));
+  int used = 1;
+#pragma omp parallel num_threads(nthr)
+  {
+    int tid = omp_get_thread_num();
+#pragma omp single
+    used = omp_get_num_threads();
+    /* thread 0 adds straight into the outputs */
+    double* buf = tid == 0 ? NULL : (double*)calloc((size_t)(3 * nvid + nflow), sizeof(double));
+    double* gq = tid == 0 ? grad_q : buf;
+    double* gk = tid == 0 ? grad_k : buf + nvid;
+    double* gv = tid == 0 ? grad_v : buf + 2 * nvid;
+    double* gf = tid == 0 ? grad_flows : buf + 3 * nvid;
+    priv[tid] = buf;
+    double* wts = (double*)malloc(sizeof(double) * (size_t)(kk > 0 ? kk : 1));
+    double* G = (double*)malloc(sizeof(double) * (size_t)(kk > 0 ? kk : 1));
+#pragma omp for schedule(static)
+    for (int64_t row = 0; row < rows; row++)
+      backward_row(q, k, v, dists, inds, grad_out, grad_dists, p, scale, cnt, row, wts, G, gq, gk, gv, gf);
+    free(G);
+    free(wts);
+  }
+  for (int i = 1; i < used; i++) {
+    const double* buf = priv[i];
+    for (int64_t j = 0; j < nvid; j++) {
+      grad_q[j] += buf[j];
+      grad_k[j] += buf[nvid + j];
+      grad_v[j] += buf[2 * nvid + j];
+    }
+    for (int64_t j = 0; j < nflow; j++) grad_flows[j] += buf[3 * nvid + j];
+    free(priv[i]);
+  }
+  free(priv);
   free(cnt);
 }
 

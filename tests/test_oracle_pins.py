@@ -457,13 +457,17 @@ def test_aggregate_at_pixels_equals_full_scatter(oracle_lib):
 
 # ----------------------------------------------------------------- backward --
 
-def _fixed_problem(seed, dist_type, HD=1, ps=3, stride0=1):
+def _fixed_problem(seed, dist_type, HD=1, ps=3, stride0=1, stride1=1.0):
     r = _rng(100 + seed)
     C, H, W, T, wt, ws, kk = 4, 7, 8, 3, 1, 3, 3
-    p = small_params(T=T, C=C, H=H, W=W, HD=HD, ws=ws, wt=wt, ps=ps, stride0=stride0, k=kk, dist_type=dist_type)
+    p = small_params(T=T, C=C, H=H, W=W, HD=HD, ws=ws, wt=wt, ps=ps, stride0=stride0, stride1=stride1, k=kk,
+                     dist_type=dist_type)
     q, k, v = (r.standard_normal((1, T, C, H, W)) * 0.5 for _ in range(3))
     # offsets well away from integers so the bilinear weights stay smooth
-    flows = r.integers(-1, 2, size=(1, T, 2 * wt, 2, H, W)) + r.uniform(0.2, 0.8, size=(1, T, 2 * wt, 2, H, W))
+    # (with key stride 1/2 the cells add multiples of 0.5: fractions 0.1-0.4
+    # give positions 0.1-0.4 or 0.6-0.9 past an integer)
+    lo, hi = (0.2, 0.8) if stride1 == 1.0 else (0.1, 0.4)
+    flows = r.integers(-1, 2, size=(1, T, 2 * wt, 2, H, W)) + r.uniform(lo, hi, size=(1, T, 2 * wt, 2, H, W))
     nq = oracle.n_queries(p)
     sel = np.zeros((nq, kk, 3), np.int32)
     sel[:, :, 0] = r.integers(-wt, wt + 1, size=(nq, kk))
@@ -486,12 +490,20 @@ def _loss(p, q, k, v, flows, sel, g, gd, scale):
     return (g * out).sum() + (gd[fin] * d[fin]).sum(), d, ind
 
 
-@pytest.mark.parametrize("dist_type,HD", [(0, 1), (1, 1), (0, 2)])
-def test_backward_matches_finite_differences(oracle_lib, dist_type, HD):
+BWD_SHAPES = [  # dist_type, HD, P, S_Q, S_K
+    (0, 1, 3, 1, 1.0), (1, 1, 3, 1, 1.0), (0, 2, 3, 1, 1.0),
+    (0, 1, 1, 2, 1.0), (1, 1, 5, 2, 1.0), (0, 1, 5, 1, 0.5), (1, 2, 1, 1, 0.5), (0, 1, 3, 2, 0.5),
+]
+
+
+@pytest.mark.parametrize("dist_type,HD,ps,stride0,stride1", BWD_SHAPES)
+def test_backward_matches_finite_differences(oracle_lib, dist_type, HD, ps, stride0, stride1):
     """Sec. 1 / 3.2 differentiable search: the chain-rule gradients w.r.t. q,
     k, v and the offsets F_in match central finite differences of the
-    forward map (top-k set held fixed, positions in double precision)."""
-    p, q, k, v, flows, sel, g, gd = _fixed_problem(dist_type + 3 * HD, dist_type, HD=HD)
+    forward map (top-k set held fixed, positions in double precision), for
+    single-pixel and 5 x 5 patches, query stride 2 and key stride 1/2."""
+    p, q, k, v, flows, sel, g, gd = _fixed_problem(dist_type + 3 * HD + 7 * ps + 11 * stride0, dist_type, HD=HD,
+                                                   ps=ps, stride0=stride0, stride1=stride1)
     scale = 0.2
     L0, d, ind = _loss(p, q, k, v, flows, sel, g, gd, scale)
     gq, gk, gv, gf = oracle.backward(q, k, v, flows, d, ind, g, p, scale, grad_dists=gd)
@@ -514,11 +526,12 @@ def test_backward_matches_finite_differences(oracle_lib, dist_type, HD):
             assert grad.reshape(-1)[i] == pytest.approx(fd, rel=1e-6, abs=1e-7), (name, i)
 
 
-def test_backward_adjoint_identities(oracle_lib):
+@pytest.mark.parametrize("ps,stride0,stride1", [(3, 1, 1.0), (1, 2, 1.0), (5, 2, 1.0), (5, 1, 0.5)])
+def test_backward_adjoint_identities(oracle_lib, ps, stride0, stride1):
     """Adjoint checks of the linear pieces: v -> out is linear for fixed
     scores and positions, and q -> d, k -> d are linear for the inner product,
     so <J x, y> = <x, J^T y> with J^T y from the backward pass."""
-    p, q, k, v, flows, sel, g, gd = _fixed_problem(7, 0)
+    p, q, k, v, flows, sel, g, gd = _fixed_problem(7 + ps + stride0, 0, ps=ps, stride0=stride0, stride1=stride1)
     scale = 0.4
     d, ind = oracle.search_fixed(q, k, flows, p, sel)
     d = d.reshape(gd.shape)
