@@ -732,6 +732,27 @@ def test_backward_shapes(dev, kw):
         assert_close(_h(g_gpu), g_ref, name)
 
 
+def test_backward_full_size_matches_oracle(dev):
+    """train256 at its full size (256 x 256, T = 5, C = 64, P = 3, k = 10):
+    dq, dk, dv and the flow gradients of the GPU against the oracle's
+    gradients for the GPU's own neighbours, element by element.  q and k
+    are separate tensors (scaled copies of the video) so that every
+    gradient is checked on its own."""
+    c = _cfg(4)
+    p, scale = c["params"], c["scale"]
+    q = np.ascontiguousarray(c["q"] * np.float32(0.5))
+    k = np.ascontiguousarray(c["k"] * np.float32(0.4))
+    print("backward at full size %s" % p, flush=True)
+    qd, kd, vd, fd = (_d(a, dev) for a in (q, k, c["v"], c["flows"]))
+    gd, gi = B.snls_search(qd, kd, fd, p)
+    grads = B.snls_backward(qd, kd, vd, fd, gd, gi, _d(c["grad_out"], dev), p, scale)
+    torch.cuda.synchronize()
+    ref = oracle.backward(q, k, c["v"], c["flows"], _h(gd), _h(gi), c["grad_out"], p, scale)
+    for name, g_gpu, g_ref in zip(("dq", "dk", "dv", "dflows"), grads, ref):
+        assert_close(_h(g_gpu), g_ref, name)
+        print("  %s ok" % name, flush=True)
+
+
 def test_backward_adjoint_full_size(dev):
     """train256 at full size: v -> out is linear for fixed neighbours, so
     <out(x), y> = <x, grad_v(y)> with both sides from the GPU."""
