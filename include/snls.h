@@ -14,15 +14,18 @@
  *   snls_backward   Sec. 1 / 3.2, gradients of the differentiable search and
  *                   aggregation;
  *   snls_aggregate_stacked, snls_chain_flows  the code example's neighbour-
- *                   stacked gather and its forward/backward flow interface.
+ *                   stacked gather and its forward/backward flow interface;
+ *   snls_aggregate_static  snls_aggregate without a caller workspace, for
+ *                   callers that cannot allocate.
  *
  * Conventions shared by every call
  * --------------------------------
  *  - Pointers named as device buffers must point to device memory of the
  *    current HIP device; all are fp32, dense, C-contiguous, 4-byte aligned.
  *    The caller owns every buffer; the library keeps no pointer and no state
- *    between calls, so concurrent calls on different streams are safe when
- *    their output buffers do not overlap.
+ *    between calls (apart from the scratch array of snls_aggregate_static),
+ *    so concurrent calls on different streams are safe when their output
+ *    buffers do not overlap.
  *  - Every call is asynchronous on `stream` (a hipStream_t; NULL is the
  *    default stream).  Buffers must stay alive until the stream has
  *    completed the work.
@@ -68,14 +71,15 @@
 extern "C" {
 #endif
 
-#define SNLS_ABI_VERSION 2
+#define SNLS_ABI_VERSION 3
 
 typedef enum {
   SNLS_OK = 0,
   SNLS_ERR_INVALID_ARG = 1, /* a size, pointer or parameter is out of range */
   SNLS_ERR_UNSUPPORTED = 2, /* valid, but beyond this build's limits (e.g. k > 128) */
   SNLS_ERR_HIP = 3,         /* the HIP runtime reported an error (no device, launch failure) */
-  SNLS_ERR_WORKSPACE = 4    /* workspace missing or smaller than snls_workspace_size() */
+  SNLS_ERR_WORKSPACE = 4,   /* workspace missing or smaller than snls_workspace_size() */
+  SNLS_ERR_SCRATCH = 5      /* the call needs more than SNLS_STATIC_SCRATCH_BYTES (snls_aggregate_static) */
 } snls_status;
 
 typedef enum {
@@ -165,6 +169,26 @@ snls_status snls_topk(const float* dists_all, const float* inds_all, int64_t row
  * SNLS_ERR_WORKSPACE, SNLS_ERR_HIP. */
 snls_status snls_aggregate(const float* v, const float* dists, const float* inds, const snls_params* p,
                            float scale, float* out, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Size of the library's own device scratch array used by
+ * snls_aggregate_static (64 MiB on every GPU the library runs on). */
+#define SNLS_STATIC_SCRATCH_BYTES (64u << 20)
+
+/* snls_aggregate_static -- snls_aggregate for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same computation and kernels, with
+ * the workspace taken from a device array of SNLS_STATIC_SCRATCH_BYTES that
+ * the library holds on each GPU until the process ends.  The call allocates
+ * nothing (no hipMalloc / hipFree, no allocating library routine).
+ *   v, dists, inds, p, scale, out  as in snls_aggregate (caller-owned)
+ * The array is shared by every call on one GPU and keeps the last call's
+ * contents; calls that overlap in time on one GPU (several streams or host
+ * threads) race on it and must be serialised by the caller.
+ * Errors: as snls_aggregate; SNLS_ERR_SCRATCH (nothing launched) when
+ * snls_workspace_size(SNLS_OP_AGGREGATE, p) exceeds
+ * SNLS_STATIC_SCRATCH_BYTES. */
+snls_status snls_aggregate_static(const float* v, const float* dists, const float* inds, const snls_params* p,
+                                  float scale, float* out, void* stream);
 
 /* snls_backward -- gradients of search + aggregation (Sec. 1: the grid
  * search is differentiable; the top-k set is held fixed, Sec. 3.2).

@@ -41,6 +41,7 @@ const char* snls_status_string(snls_status s) {
     case SNLS_ERR_UNSUPPORTED: return "unsupported parameters";
     case SNLS_ERR_HIP: return "HIP runtime error";
     case SNLS_ERR_WORKSPACE: return "workspace missing or too small";
+    case SNLS_ERR_SCRATCH: return "problem larger than the library's static scratch array";
   }
   return "unknown status";
 }

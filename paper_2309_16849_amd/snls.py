@@ -6,8 +6,8 @@ There is no CPU fallback -- if libsnls.so is missing or fails to load, every
 call raises.
 
 Functions carry the C names: snls_search, snls_topk, snls_aggregate,
-snls_backward, snls_aggregate_stacked, snls_chain_flows, snls_workspace_size,
-snls_status_string, snls_abi_version.
+snls_backward, snls_aggregate_stacked, snls_chain_flows, snls_aggregate_static,
+snls_workspace_size, snls_status_string, snls_abi_version.
 Parameters are plain dicts with keys B, T, C, H, W, HD, ws, wt, ps, stride0,
 stride1, k, dist_type (see ``params_from_dict``).
 """
@@ -21,12 +21,14 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsnls.so")
 
-SNLS_OK, SNLS_ERR_INVALID_ARG, SNLS_ERR_UNSUPPORTED, SNLS_ERR_HIP, SNLS_ERR_WORKSPACE = range(5)
+SNLS_OK, SNLS_ERR_INVALID_ARG, SNLS_ERR_UNSUPPORTED, SNLS_ERR_HIP, SNLS_ERR_WORKSPACE, SNLS_ERR_SCRATCH = range(6)
 SNLS_DIST_PROD, SNLS_DIST_L2 = 0, 1
 SNLS_OP_SEARCH, SNLS_OP_AGGREGATE, SNLS_OP_BACKWARD, SNLS_OP_AGGREGATE_STACKED = 0, 1, 2, 3
 SNLS_MAX_K = 128
+SNLS_STATIC_SCRATCH_BYTES = 64 << 20
 SYMBOLS = ("snls_search", "snls_topk", "snls_aggregate", "snls_backward", "snls_workspace_size",
-           "snls_status_string", "snls_abi_version", "snls_aggregate_stacked", "snls_chain_flows")
+           "snls_status_string", "snls_abi_version", "snls_aggregate_stacked", "snls_chain_flows",
+           "snls_aggregate_static")
 
 
 class SnlsParams(ctypes.Structure):
@@ -60,13 +62,14 @@ def load_library():
         lib.snls_backward.argtypes = [P] * 8 + [PP, F32, P, P, P, P, P, SZ, P]
         lib.snls_aggregate_stacked.argtypes = [P, P, P, PP, F32, P, P, SZ, P]
         lib.snls_chain_flows.argtypes = [P, P, I32, I32, I32, I32, I32, P, P]
+        lib.snls_aggregate_static.argtypes = [P, P, P, PP, F32, P, P]
         lib.snls_workspace_size.argtypes = [ctypes.c_int, PP]
         lib.snls_workspace_size.restype = SZ
         lib.snls_status_string.argtypes = [ctypes.c_int]
         lib.snls_status_string.restype = ctypes.c_char_p
         lib.snls_abi_version.argtypes = []
         for f in ("snls_search", "snls_topk", "snls_aggregate", "snls_backward", "snls_abi_version",
-                  "snls_aggregate_stacked", "snls_chain_flows"):
+                  "snls_aggregate_stacked", "snls_chain_flows", "snls_aggregate_static"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -203,6 +206,23 @@ def snls_aggregate(v, dists, inds, p: dict, scale: float = 1.0, out=None, worksp
     prm = params_from_dict(p)
     _check(lib.snls_aggregate(_ptr(v), _ptr(dists), _ptr(inds), ctypes.byref(prm), float(scale), _ptr(out),
                               _ptr(workspace), workspace.numel() * 4, _stream(stream)), "snls_aggregate")
+    return out
+
+
+def snls_aggregate_static(v, dists, inds, p: dict, scale: float = 1.0, out=None, stream=None):
+    """snls_aggregate with the library's static scratch array as workspace
+    (nothing allocated on the device beyond ``out`` when it is not given)."""
+    lib = load_library()
+    _dev(v, "v", video_shape(p))
+    shp = out_shape(p)
+    _dev(dists, "dists", shp)
+    _dev(inds, "inds", shp + (3,))
+    if out is None:
+        out = torch.empty(video_shape(p), device=v.device, dtype=torch.float32)
+    _dev(out, "out", video_shape(p))
+    prm = params_from_dict(p)
+    _check(lib.snls_aggregate_static(_ptr(v), _ptr(dists), _ptr(inds), ctypes.byref(prm), float(scale), _ptr(out),
+                                     _stream(stream)), "snls_aggregate_static")
     return out
 
 

@@ -41,9 +41,9 @@ def test_exports_every_declared_function(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert B.snls_abi_version() == 2
+    assert B.snls_abi_version() == 3
     assert B.snls_status_string(0) == "ok"
-    for s in range(1, 5):
+    for s in range(1, 6):
         assert B.snls_status_string(s) not in ("ok", "unknown status")
     assert B.snls_status_string(99) == "unknown status"
     assert ctypes.sizeof(B.SnlsParams) == 4 * 14  # 14 four-byte fields, no padding
@@ -188,3 +188,21 @@ def test_stacked_and_chain_validation(lib):
         assert lib.snls_chain_flows(FAKE, FAKE, *args, FAKE, None) == B.SNLS_ERR_INVALID_ARG
     assert lib.snls_chain_flows(FAKE, None, 1, 3, 4, 4, 2, FAKE, None) == B.SNLS_ERR_INVALID_ARG
     assert lib.snls_chain_flows(FAKE, FAKE, 1, 3, 4, 4, 64, FAKE, None) == B.SNLS_ERR_UNSUPPORTED
+
+
+def test_aggregate_static_validation(lib):
+    """The allocation-free aggregation validates like snls_aggregate and
+    refuses, before touching the device, a problem whose workspace exceeds
+    the library's static scratch array."""
+    prm = _params(k=0)
+    assert lib.snls_aggregate_static(FAKE, FAKE, FAKE, ctypes.byref(prm), 1.0, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    prm = _params()
+    assert lib.snls_aggregate_static(FAKE, None, FAKE, ctypes.byref(prm), 1.0, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_aggregate_static(FAKE, FAKE, FAKE, ctypes.byref(prm), float("nan"), FAKE,
+                                     None) == B.SNLS_ERR_INVALID_ARG
+    # 1 x 5 x 64 x 256 x 256 video: 84 MB transposed copy + 13 MB weights > 64 MiB
+    big = _params(T=5, C=64, H=256, W=256, HD=1, ws=3, wt=1, k=10)
+    need = lib.snls_workspace_size(B.SNLS_OP_AGGREGATE, ctypes.byref(big))
+    assert need > B.SNLS_STATIC_SCRATCH_BYTES
+    assert lib.snls_aggregate_static(FAKE, FAKE, FAKE, ctypes.byref(big), 1.0, FAKE, None) == B.SNLS_ERR_SCRATCH
+    assert B.snls_status_string(B.SNLS_ERR_SCRATCH) != "unknown status"
