@@ -93,13 +93,6 @@ __global__ void __launch_bounds__(256) to_channels_last_kernel(const float* __re
   }
 }
 
-// Order this wave's earlier LDS accesses before its later ones (lanes of the
-// wave read what other lanes of the same wave wrote).
-SNLS_DEV void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
 
 // Merged gather.  One workgroup = 8 x 8 output pixels of one (b, t, head);
 // one wave per pixel at a time, lane = channel (CPL channels per lane).

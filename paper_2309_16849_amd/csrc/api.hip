@@ -25,7 +25,9 @@ snls_status device_ready() {
 
 // Only the scored top-k paths need scratch: the scores of every candidate.
 size_t search_ws_bytes(const Geo& g) {
-  return g.k >= 1 && (tile_supported(g) || p1_supported(g)) ? tile_ws_bytes(g) : 0;
+  if (g.k < 1) return 0;
+  const SearchRoute r = search_route(g);
+  return r == SearchRoute::Tile || r == SearchRoute::P1Scored ? tile_ws_bytes(g) : 0;
 }
 
 }  // namespace

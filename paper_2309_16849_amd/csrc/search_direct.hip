@@ -111,7 +111,7 @@ __global__ void __launch_bounds__(128) search_topk_direct_kernel(const float* __
   for (int e = 0; e < KMAX; ++e) {
     if (e >= first) {
       const int i = e - first;
-      int cid = min(lst.id[e], g.ncand - 1);  // every candidate was ranked: ids are real
+      int cid = min(max(lst.id[e], 0), g.ncand - 1);  // every candidate was ranked: ids are real
       int dw = cid % g.ws;
       int dh = (cid / g.ws) % g.ws;
       int dt = cid / (g.ws * g.ws) - g.wt;
@@ -149,15 +149,23 @@ snls_status launch_search_topk_direct(const float* q, const float* k, const floa
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
 }
 
+SearchRoute search_route(const Geo& g) {
+  // single-pixel patches at a query stride above 1: no patch overlap for
+  // the tiles to share, the per-query kernels are faster
+  if (g.ps == 1 && g.s0 > 1 && p1_supported(g)) return p1_fused(g) ? SearchRoute::P1Fused : SearchRoute::P1Scored;
+  if (tile_supported(g)) return SearchRoute::Tile;
+  if (p1_supported(g)) return p1_fused(g) ? SearchRoute::P1Fused : SearchRoute::P1Scored;
+  return SearchRoute::Direct;
+}
+
 snls_status launch_search_topk(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, void* ws, hipStream_t s) {
-  // single-pixel patches at a query stride above 1: no patch overlap for
-  // the tiles to share, the per-query kernel is faster
-  if (g.ps == 1 && g.s0 > 1 && p1_supported(g))
-    return launch_search_p1(q, k, flows, g, dists, inds, static_cast<float*>(ws), s);
-  if (tile_supported(g)) return launch_search_tile(q, k, flows, g, dists, inds, static_cast<float*>(ws), s);
-  if (p1_supported(g)) return launch_search_p1(q, k, flows, g, dists, inds, static_cast<float*>(ws), s);
-  return launch_search_topk_direct(q, k, flows, g, dists, inds, s);
+  switch (search_route(g)) {
+    case SearchRoute::P1Fused: return launch_search_p1_topk(q, k, flows, g, dists, inds, s);
+    case SearchRoute::P1Scored: return launch_search_p1(q, k, flows, g, dists, inds, static_cast<float*>(ws), s);
+    case SearchRoute::Tile: return launch_search_tile(q, k, flows, g, dists, inds, static_cast<float*>(ws), s);
+    default: return launch_search_topk_direct(q, k, flows, g, dists, inds, s);
+  }
 }
 
 }  // namespace snls

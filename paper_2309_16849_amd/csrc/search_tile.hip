@@ -731,7 +731,7 @@ __global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __rest
       const int i = e - first;
       // every candidate was ranked, so the k best are real candidates; the
       // clamp only keeps a placeholder id in bounds
-      const int cid = min(lst.id[e], g.ncand - 1);
+      const int cid = min(max(lst.id[e], 0), g.ncand - 1);
       const int dw = cid % g.ws, dh = (cid / g.ws) % g.ws, dt = cid / ncell - g.wt;
       float fh = 0.f, fw = 0.f;
       if (dt != 0) {
@@ -763,18 +763,6 @@ namespace wtk {
 constexpr int WAVES = 4;  // rows per workgroup
 }  // namespace wtk
 
-SNLS_DEV unsigned order_key(float f) {
-  const unsigned b = __float_as_uint(f);
-  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
-}
-SNLS_DEV float key_score(unsigned u) { return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u); }
-SNLS_DEV int lanes_below(unsigned long long m) {
-  return (int)__builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
-}
-SNLS_DEV unsigned long long shfl_xor64(unsigned long long x, int m) {
-  const unsigned lo = __shfl_xor((unsigned)x, m), hi = __shfl_xor((unsigned)(x >> 32), m);
-  return ((unsigned long long)hi << 32) | lo;
-}
 // Bitonic sort of one value per lane, descending across lanes 0..63.
 template <typename V, typename X>
 SNLS_DEV V sort64_desc(V x, int lane, X xchg) {
@@ -916,7 +904,7 @@ __global__ void __launch_bounds__(wtk::WAVES * 64) wave_topk_kernel(const float*
   if (lane >= g.k) return;
   // every candidate was ranked, so the k best are real candidates; the clamp
   // only keeps a placeholder id in bounds
-  const int cid = min((int)~(unsigned)best, g.ncand - 1);
+  const int cid = min(max((int)~(unsigned)best, 0), g.ncand - 1);
   const int dw = cid % g.ws, dh = (cid / g.ws) % g.ws, dt = cid / ncell - g.wt;
   float fh = 0.f, fw = 0.f;
   if (dt != 0) {

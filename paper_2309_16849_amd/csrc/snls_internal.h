@@ -57,8 +57,14 @@ size_t aggregate_stacked_ws_bytes(const Geo& g);
 bool tile_supported(const Geo& g);
 size_t tile_ws_bytes(const Geo& g);
 // Single-pixel patches (P = 1), any S_Q, S_K = 1, inner product, Ws <= 15:
-// same workspace layout (scores of every candidate).
+// same workspace layout (scores of every candidate) for k > 32; for k <= 32
+// (p1_fused) the selection runs inside the scoring kernel, no workspace.
 bool p1_supported(const Geo& g);
+bool p1_fused(const Geo& g);
+
+// Kernels a top-k search (k >= 1) runs on.
+enum class SearchRoute { Direct, Tile, P1Scored, P1Fused };
+SearchRoute search_route(const Geo& g);
 
 #ifdef __HIPCC__
 
@@ -75,6 +81,8 @@ snls_status launch_search_p1(const float* q, const float* k, const float* flows,
                              float* inds, float* scores, hipStream_t s);
 snls_status launch_search_p1_scores(const float* q, const float* k, const float* flows, const Geo& g, float* scores,
                                     int pitch, hipStream_t s);
+snls_status launch_search_p1_topk(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
+                                  float* inds, hipStream_t s);
 // L2 norm terms: key pair planes (workspace of l2_planes_bytes(g) bytes),
 // then the key-norm terms G (rows x pitch) and the query norms Qn (rows).
 size_t l2_planes_bytes(const Geo& g);
@@ -189,6 +197,30 @@ SNLS_DEV float score_candidate(const float* __restrict__ q, const float* __restr
   }
   // a NaN similarity (non-finite inputs) scores as an invalid candidate
   return acc != acc ? from_score(-INFINITY, g.dist) : acc;
+}
+
+// Order this wave's earlier LDS accesses before its later ones (lanes of the
+// wave read what other lanes of the same wave wrote).
+SNLS_DEV void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// 32-bit keys ordered like the scores they encode (unsigned comparison):
+// -inf maps to 0x007fffff, so 0 lies below every score.
+SNLS_DEV unsigned order_key(float f) {
+  const unsigned b = __float_as_uint(f);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+SNLS_DEV float key_score(unsigned u) { return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u); }
+// Number of lanes below this one whose bit is set in m.
+SNLS_DEV int lanes_below(unsigned long long m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+}
+SNLS_DEV unsigned long long shfl_xor64(unsigned long long x, int m) {
+  const unsigned lo = __shfl_xor((unsigned)x, m), hi = __shfl_xor((unsigned)(x >> 32), m);
+  return ((unsigned long long)hi << 32) | lo;
 }
 
 // Sorted top-k list in registers, best first, for 1 <= k <= KMAX.  The

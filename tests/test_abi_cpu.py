@@ -142,9 +142,11 @@ def test_search_workspace(lib):
                dict(ws=11, k=4)):
         assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(**kw))) == 0, kw
     # single-pixel patches at query stride 2: the scores of every candidate
-    p1 = _params(ps=1, stride0=2, ws=15, k=30)
+    # for k above 32; up to 32 the selection runs inside the scoring kernel
+    p1 = _params(ps=1, stride0=2, ws=15, k=33)
     rows1 = 1 * 2 * 3 * 8 * 9
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(p1)) == rows1 * 676 * 4  # 675 padded to 676
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, stride0=2, ws=15, k=32))) == 0
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, stride0=2, ws=17, k=30))) == 0
     # squared L2 (key stride 1): the scores, the key-norm terms, the query-norm
     # terms, five key pair planes and the query pixel-norm plane per frame and head

@@ -414,13 +414,17 @@ P1_CASES = [
 ]
 
 
-# The wave top-k's three selection paths on a smooth motion video (the
-# multi-head workload's settings at 40 x 56): about 94% of the rows have at
-# most 64 candidates at or above the first threshold, about 6% between 65
-# and 128 (two entries per lane, 128-entry sort) and 17 rows more than 128
-# (bisection for the exact k-th key); counts from the oracle's full rows.
-def test_wave_topk_paths(dev):
-    p = small_params(B=1, T=8, C=64, HD=4, H=40, W=56, ws=15, wt=3, ps=1, stride0=2, k=30)
+# The multi-head workload's settings at 40 x 56 on a smooth motion video:
+# with k = 30 the single-pixel search selects inside its scoring kernel
+# (query frame first: bisection of the first frame's cells, then merges of
+# few cells per frame); with k = 40 the scores go through the workspace to
+# the wave top-k, whose three selection paths this video reaches: about 94%
+# of the rows have at most 64 candidates at or above the first threshold,
+# about 6% between 65 and 128 (two entries per lane, 128-entry sort) and a
+# few rows more than 128 (bisection for the exact k-th key).
+@pytest.mark.parametrize("kk", [30, 40])
+def test_wave_topk_paths(dev, kk):
+    p = small_params(B=1, T=8, C=64, HD=4, H=40, W=56, ws=15, wt=3, ps=1, stride0=2, k=kk)
     x, flows = _motion_inputs(p, 3, 6.0)
     gd, gi = B.snls_search(_d(x, dev), _d(x, dev), _d(flows, dev), p)
     out = B.snls_aggregate(_d(x, dev), gd, gi, p, 1.0)
@@ -440,6 +444,12 @@ TIE_CASES = [
     small_params(T=3, C=3, H=17, W=19, ws=7, wt=1, ps=3, k=10),
     small_params(T=2, C=2, H=16, W=18, ws=5, wt=1, ps=3, k=30, dist_type=1),
     small_params(T=3, C=1, H=12, W=13, ws=9, wt=2, ps=1, k=64),
+    # single-pixel patches with k <= 32 (selection inside the scoring
+    # kernel): tied keys beyond 32 of a frame take the tie path of its
+    # bisection; frames outside the clip fill with invalid candidates
+    small_params(T=3, C=2, H=20, W=21, ws=9, wt=1, ps=1, stride0=2, k=20),
+    small_params(T=2, C=1, H=19, W=17, ws=15, wt=2, ps=1, stride0=2, k=32),
+    small_params(T=1, C=3, H=9, W=11, ws=3, wt=2, ps=1, stride0=2, k=25),
 ]
 
 
