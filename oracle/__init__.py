@@ -61,9 +61,11 @@ def _load():
         ci = ctypes.c_int
         lib.oracle_chain_flows.argtypes = [P, P, ci, ci, ci, ci, ci, P]
         lib.oracle_aggregate_stacked.argtypes = [P, P, P, P, ctypes.c_double, P]
+        lib.oracle_gather_stacked.argtypes = [P, P, P, P, P]
+        lib.oracle_stacked_reduce.argtypes = [P, P, P, ci, P]
         for f in ("oracle_search", "oracle_topk", "oracle_aggregate", "oracle_aggregate_at",
                   "oracle_search_fixed", "oracle_backward", "oracle_bilinear_image", "oracle_chain_flows",
-                  "oracle_aggregate_stacked"):
+                  "oracle_aggregate_stacked", "oracle_gather_stacked", "oracle_stacked_reduce"):
             getattr(lib, f).restype = None
         _lib = lib
     return _lib
@@ -222,4 +224,28 @@ def aggregate_stacked(v, dists, inds, p: dict, scale: float = 1.0):
     out = np.empty((p["B"], p["HD"], p["k"], p["T"], p["C"] // p["HD"], p["H"], p["W"]), np.float64)
     prm = _params(p)
     lib.oracle_aggregate_stacked(_ptr(vv), _ptr(dd), _ptr(ii), ctypes.byref(prm), float(scale), _ptr(out))
+    return out
+
+
+def gather_stacked(v, weights, inds, p: dict):
+    """The example's gather with the caller's weights (B,HD,T,nH,nW,k):
+    returns (B, HD, k, T, C/HD, H, W), float64."""
+    lib = _load()
+    vv, ww, ii = _f64(v), _f64(weights), _f64(inds)
+    out = np.empty((p["B"], p["HD"], p["k"], p["T"], p["C"] // p["HD"], p["H"], p["W"]), np.float64)
+    prm = _params(p)
+    lib.oracle_gather_stacked(_ptr(vv), _ptr(ww), _ptr(ii), ctypes.byref(prm), _ptr(out))
+    return out
+
+
+def stacked_reduce(stacked, proj, p: dict):
+    """The reduction over the k neighbours with kernel proj (Cout, C, k):
+    returns (B, T, Cout, H, W), float64."""
+    lib = _load()
+    ss, pp = _f64(stacked), _f64(proj)
+    cout = pp.shape[0]
+    assert pp.shape == (cout, p["C"], p["k"]), pp.shape
+    out = np.empty((p["B"], p["T"], cout, p["H"], p["W"]), np.float64)
+    prm = _params(p)
+    lib.oracle_stacked_reduce(_ptr(ss), _ptr(pp), ctypes.byref(prm), cout, _ptr(out))
     return out

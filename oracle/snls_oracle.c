@@ -668,3 +668,86 @@ void oracle_aggregate_stacked(const double* v, const double* dists, const double
   free(wts);
   free(cnt);
 }
+
+/* The stacked gather of the code example with the caller's weights (the
+ * example passes softmax(-10 * dists) computed outside the gather):
+ * stacked[b,hd,l,t,c,y,x] = (1/count(y,x)) * sum over the query patches
+ * covering (y,x) of weights_l * v~_l, the bilinear read of the l-th
+ * neighbour's frame at (y,x) + its displacement (head hd's channels).  A
+ * neighbour whose weight is 0, whose frame is not an integer in [0,T) or
+ * whose displacement is not finite contributes nothing.  weights:
+ * (B,HD,T,nH,nW,k); stacked: (B,HD,k,T,C/HD,H,W). */
+void oracle_gather_stacked(const double* v, const double* weights, const double* inds, const oracle_params* p,
+                           double* stacked) {
+  int nH = grid_h(p), nW = grid_w(p), Ch = p->C / p->HD, lo = patch_lo(p), kk = p->k;
+  int64_t HW = (int64_t)p->H * p->W;
+  int64_t nst = (int64_t)p->B * p->HD * kk * p->T * Ch * HW;
+  double* cnt = (double*)calloc((size_t)p->B * p->T * HW, sizeof(double));
+  memset(stacked, 0, sizeof(double) * (size_t)nst);
+  for (int b = 0; b < p->B; b++)
+    for (int t = 0; t < p->T; t++)
+      for (int mh = 0; mh < nH; mh++)
+        for (int mw = 0; mw < nW; mw++) {
+          int h = mh * p->stride0, w = mw * p->stride0;
+          for (int ph = lo; ph < lo + p->ps; ph++)
+            for (int pw = lo; pw < lo + p->ps; pw++) {
+              int y = h + ph, x = w + pw;
+              if (y < 0 || y >= p->H || x < 0 || x >= p->W) continue;
+              cnt[((int64_t)b * p->T + t) * HW + (int64_t)y * p->W + x] += 1.0;
+            }
+          for (int hd = 0; hd < p->HD; hd++) {
+            int64_t row = ((((int64_t)b * p->HD + hd) * p->T + t) * nH + mh) * nW + mw;
+            for (int l = 0; l < kk; l++) {
+              double wl = weights[row * kk + l];
+              const double* ind = inds + 3 * (row * kk + l);
+              int tk = neighbour_frame(p, ind[0]);
+              if (wl == 0.0 || tk < 0 || !isfinite(ind[1]) || !isfinite(ind[2])) continue;
+              for (int ph = lo; ph < lo + p->ps; ph++)
+                for (int pw = lo; pw < lo + p->ps; pw++) {
+                  int y = h + ph, x = w + pw;
+                  if (y < 0 || y >= p->H || x < 0 || x >= p->W) continue;
+                  for (int c = 0; c < Ch; c++) {
+                    int64_t o = (((((int64_t)b * p->HD + hd) * kk + l) * p->T + t) * Ch + c) * HW +
+                                (int64_t)y * p->W + x;
+                    stacked[o] += wl * bilinear(v, p, b, tk, hd * Ch + c, (double)y + ind[1], (double)x + ind[2]);
+                  }
+                }
+            }
+          }
+        }
+  for (int64_t o = 0; o < nst; o++) {
+    int64_t pix = o % HW;
+    int64_t r = o / HW / Ch;
+    int t = (int)(r % p->T);
+    int b = (int)(r / p->T / kk / p->HD);
+    double n = cnt[((int64_t)b * p->T + t) * HW + pix];
+    stacked[o] = n > 0.0 ? stacked[o] / n : 0.0;
+  }
+  free(cnt);
+}
+
+/* The reduction over the k neighbours that follows the gather in the code
+ * example: the stacked tensor is rearranged to ((b t), (hd f), k, h, w) and
+ * convolved with a (Cout, C, k, 1, 1) kernel at stride (k, 1, 1), so
+ * out[b,t,o,y,x] = sum over hd, f, l of proj[o, hd*C/HD + f, l] *
+ * stacked[b,hd,l,t,f,y,x].  proj: (Cout, C, k) row-major; out:
+ * (B,T,Cout,H,W). */
+void oracle_stacked_reduce(const double* stacked, const double* proj, const oracle_params* p, int cout,
+                           double* out) {
+  int Ch = p->C / p->HD, kk = p->k;
+  int64_t HW = (int64_t)p->H * p->W;
+#pragma omp parallel for schedule(static)
+  for (int64_t bt = 0; bt < (int64_t)p->B * p->T; bt++) {
+    int b = (int)(bt / p->T), t = (int)(bt % p->T);
+    for (int o = 0; o < cout; o++)
+      for (int64_t pix = 0; pix < HW; pix++) {
+        double s = 0.0;
+        for (int hd = 0; hd < p->HD; hd++)
+          for (int f = 0; f < Ch; f++)
+            for (int l = 0; l < kk; l++)
+              s += proj[((int64_t)o * p->C + hd * Ch + f) * kk + l] *
+                   stacked[(((((int64_t)b * p->HD + hd) * kk + l) * p->T + t) * Ch + f) * HW + pix];
+        out[(bt * cout + o) * HW + pix] = s;
+      }
+  }
+}

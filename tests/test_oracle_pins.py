@@ -695,3 +695,106 @@ def test_stacked_aggregation_keeps_neighbours_apart(oracle_lib, ps, stride0, HD)
                 folded = F.fold(torch.from_numpy(cols)[None], (H, W), ps, padding=ps // 2, stride=stride0)[0]
                 ref = torch.where(ones > 0, folded / ones.clamp(min=1), torch.zeros_like(folded)).numpy()
                 np.testing.assert_allclose(st[0, hd, l, t], ref, rtol=0, atol=1e-12)
+
+
+# ------------------------------------------- gather with caller weights --
+
+@pytest.mark.parametrize("ps,stride0,HD", [(3, 1, 1), (1, 2, 2), (5, 2, 1)])
+def test_gather_stacked_caller_weights_fold(oracle_lib, ps, stride0, HD):
+    """App. B example, gather with the caller's weights: with integer offsets
+    slice l is the fold of the queries' w_l-weighted l-th neighbour patches
+    divided by the cover count (torch fold), for arbitrary weights
+    (negative, zero, unnormalised) -- the weights are used as given."""
+    r = _rng(61 + ps + stride0 + HD)
+    Ch, H, W, T, kk = 2, 9, 10, 3, 3
+    C = Ch * HD
+    p = small_params(T=T, C=C, HD=HD, H=H, W=W, ps=ps, stride0=stride0, k=kk)
+    nH, nW = oracle.grid(p)
+    v = r.standard_normal((1, T, C, H, W))
+    wts = r.standard_normal((1, HD, T, nH, nW, kk))
+    wts[..., 1] = np.where(r.random(wts.shape[:-1]) < 0.3, 0.0, wts[..., 1])
+    inds = np.zeros((1, HD, T, nH, nW, kk, 3))
+    inds[..., 0] = r.integers(0, T, size=inds.shape[:-1])
+    inds[..., 1:] = r.integers(-2, 3, size=inds.shape[:-1] + (2,))
+    st = oracle.gather_stacked(v, wts, inds, p)
+    assert st.shape == (1, HD, kk, T, Ch, H, W)
+    m = ps + 4
+    pad = np.pad(v[0], ((0, 0), (0, 0), (m, m), (m, m)))
+    ones = F.fold(torch.ones(1, ps * ps, nH * nW, dtype=torch.float64), (H, W), ps, padding=ps // 2,
+                  stride=stride0)[0, 0]
+    for hd in range(HD):
+        for l in range(kk):
+            for t in range(T):
+                cols = np.zeros((Ch * ps * ps, nH * nW))
+                for mh in range(nH):
+                    for mw in range(nW):
+                        t2, dh, dw = inds[0, hd, t, mh, mw, l].astype(int)
+                        y0 = mh * stride0 + dh + m - ps // 2
+                        x0 = mw * stride0 + dw + m - ps // 2
+                        patch = pad[t2, hd * Ch:(hd + 1) * Ch, y0:y0 + ps, x0:x0 + ps].reshape(-1)
+                        cols[:, mh * nW + mw] = wts[0, hd, t, mh, mw, l] * patch
+                folded = F.fold(torch.from_numpy(cols)[None], (H, W), ps, padding=ps // 2, stride=stride0)[0]
+                ref = torch.where(ones > 0, folded / ones.clamp(min=1), torch.zeros_like(folded)).numpy()
+                np.testing.assert_allclose(st[0, hd, l, t], ref, rtol=0, atol=1e-12)
+
+
+def test_gather_stacked_softmax_weights_is_stacked_aggregation(oracle_lib):
+    """With the weights the aggregation forms itself (softmax of sign*scale*d,
+    0 for non-finite scores), the caller-weight gather is the stacked
+    aggregation at fractional offsets, including neighbours whose frame
+    lies outside the clip or whose offset is not finite."""
+    r = _rng(71)
+    p = small_params(T=3, C=6, HD=2, H=11, W=12, ps=3, stride0=1, k=4, dist_type=1)
+    nH, nW = oracle.grid(p)
+    v = r.standard_normal((1, 3, 6, 11, 12))
+    d = r.standard_normal((1, 2, 3, nH, nW, 4))
+    d[0, 0, 1, 2, 3, 2] = np.inf
+    inds = np.zeros((1, 2, 3, nH, nW, 4, 3))
+    inds[..., 0] = r.integers(0, 3, size=inds.shape[:-1])
+    inds[..., 1:] = r.uniform(-3, 3, size=inds.shape[:-1] + (2,))
+    inds[0, 1, 0, 1, 1, 0, 0] = 5.0            # frame outside the clip
+    inds[0, 1, 2, 3, 4, 1, 2] = np.nan         # offset not finite
+    scale = 0.7
+    s = -scale * d  # squared L2: smaller is better
+    fin = np.isfinite(s)
+    e = np.where(fin, np.exp(s - np.where(fin, s, -np.inf).max(-1, keepdims=True)), 0.0)
+    w = e / e.sum(-1, keepdims=True)
+    np.testing.assert_allclose(oracle.gather_stacked(v, w, inds, p), oracle.aggregate_stacked(v, d, inds, p, scale),
+                               rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("HD,cout", [(1, 5), (2, 6)])
+def test_stacked_reduce_is_strided_conv3d(oracle_lib, HD, cout):
+    """App. B example: the reduction over the k neighbours is torch's conv3d
+    with a (Cout, C, k, 1, 1) kernel at stride (k, 1, 1) after the example's
+    rearrangement (b hd k t f h w -> (b t) (hd f) k h w)."""
+    r = _rng(81 + HD)
+    B, T, Ch, H, W, kk = 2, 3, 3, 5, 4, 4
+    C = Ch * HD
+    p = small_params(B=B, T=T, C=C, HD=HD, H=H, W=W, k=kk)
+    st = r.standard_normal((B, HD, kk, T, Ch, H, W))
+    proj = r.standard_normal((cout, C, kk))
+    got = oracle.stacked_reduce(st, proj, p)
+    x = torch.from_numpy(st).permute(0, 3, 1, 4, 2, 5, 6).reshape(B * T, C, kk, H, W)
+    ref = F.conv3d(x, torch.from_numpy(proj)[..., None, None], stride=(kk, 1, 1))
+    ref = ref.reshape(B, T, cout, H, W).numpy()
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_reduce_of_gather_with_identity_kernel_is_aggregation(oracle_lib):
+    """Sum over the neighbours: with proj[o, i, l] = [o == i] for every l the
+    reduction of the gathered stack is the plain aggregation of Sec. 3.2
+    (softmax weights)."""
+    r = _rng(91)
+    p = small_params(T=3, C=4, HD=2, H=10, W=9, ps=3, stride0=2, k=3)
+    nH, nW = oracle.grid(p)
+    v = r.standard_normal((1, 3, 4, 10, 9))
+    d = r.standard_normal((1, 2, 3, nH, nW, 3))
+    inds = np.zeros((1, 2, 3, nH, nW, 3, 3))
+    inds[..., 0] = r.integers(0, 3, size=inds.shape[:-1])
+    inds[..., 1:] = r.uniform(-2, 2, size=inds.shape[:-1] + (2,))
+    w = np.exp(0.5 * d - (0.5 * d).max(-1, keepdims=True))
+    w /= w.sum(-1, keepdims=True)
+    proj = np.repeat(np.eye(4)[:, :, None], 3, axis=2)
+    out = oracle.stacked_reduce(oracle.gather_stacked(v, w, inds, p), proj, p)
+    np.testing.assert_allclose(out, oracle.aggregate(v, d, inds, p, 0.5), rtol=1e-12, atol=1e-12)
