@@ -45,7 +45,7 @@ PEAK_FP32_VALU = 157.3e12  # MI355X fp32 vector peak (packed FMA), FLOP/s
 PEAK_FP32_VALU_UNPACKED = 78.6e12  # 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz, unpacked FMA
 PEAK_HBM = 8.0e12          # MI355X HBM3E, B/s
 DEFAULT_WORKLOAD = "denoise480x854"
-BASELINE_METRIC = "queries/s (search+top-k+aggregate) and % fp32 VALU/HBM roofline, config 2"
+METRIC = "queries/s (search+top-k+aggregate) and % fp32 VALU/HBM roofline, config 2"
 
 # Kernels of each library call, by name (no kernel is shared between the
 # search call and the others).
@@ -161,11 +161,11 @@ def summarize_profiles(outdir, workload, copy_mib, extra_args=""):
     tag = "prof_%s" % workload
     args = "--workload %s --steps {s} --warmup {w} --no-cpu-baseline --copy-probe-mib %d%s" % (
         workload, copy_mib, extra_args)
-    cmd = ("cd /tmp && rocprofv3 {opts} --output-format csv -d $R/gpurun_out/{d} -o run -- "
+    cmd = ("cd /tmp && rocprofv3 {opts} --output-format csv -d $R/$OUT/{d} -o run -- "
            "python3 $R/bench.py " + args)
     lines = ["# rocprofv3 summary: workload %s (one step: %s)" % (
         workload, "search + top-k, aggregation, backward" if "train" in workload else "search + top-k, aggregation"),
-             "", "Commands (R = repository root on the GPU box):", ""]
+             "", "Commands (R = repository root, OUT = output folder under it):", ""]
     lines.append("    " + cmd.format(opts="--kernel-trace --stats", d=tag + "_trace", s=10, w=2))
     trace = _read_csv(_find(os.path.join(outdir, tag + "_trace"), "kernel_stats.csv"))
     lines += ["", "| kernel | calls | avg us | min us | max us | total % |", "|---|---|---|---|---|---|"]
@@ -291,6 +291,40 @@ def cpu_baseline(c, budget_s=12.0):
                       "pixels those queries cover alone; %.1f s wall, fp64" % (nrows, nW, nq, t_mid, npix, wall)}
 
 
+def time_stacked(B, torch, x, dists, inds, p, scale, dev, reps=5):
+    """The example's gather (weights = softmax over the row, computed by the
+    caller as in the example) and the reduction over the k neighbours with a
+    seeded (C, C, k) kernel: materialised stack, then the fused pass."""
+    sign = 1.0 if p["dist_type"] == 0 else -1.0
+    w = torch.softmax(sign * scale * dists, dim=-1).contiguous()
+    g = torch.Generator(device="cpu").manual_seed(17)
+    proj = (torch.randn((p["C"], p["C"], p["k"]), generator=g) / (p["C"] * p["k"]) ** 0.5).to(dev)
+    st = torch.empty(B.stacked_shape(p), device=dev)
+    gws = B.workspace_for(B.SNLS_OP_GATHER_STACKED, p, dev)
+    fws = B.workspace_for(B.SNLS_OP_GATHER_REDUCE, p, dev)
+    out = torch.empty((p["B"], p["T"], p["C"], p["H"], p["W"]), device=dev)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b_ in evs:
+            a.record()
+            fn()
+            b_.record()
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b_) for a, b_ in evs]))
+
+    t_gather = timed(lambda: B.snls_gather_stacked(x, w, inds, p, st, gws))
+    t_reduce = timed(lambda: B.snls_stacked_reduce(st, proj, p, out))
+    t_fused = timed(lambda: B.snls_gather_reduce(x, w, inds, proj, p, out, fws))
+    pix = p["B"] * p["T"] * p["H"] * p["W"]
+    red_flop = 2.0 * pix * p["C"] * p["k"] * p["C"]
+    return {"gather_stacked_ms": t_gather, "stacked_reduce_ms": t_reduce, "gather_reduce_ms": t_fused,
+            "stacked_gb": st.numel() * 4 / 1e9, "reduce_tflops_mfma": red_flop / (t_reduce * 1e-3) / 1e12,
+            "reduce_flop": red_flop}
+
+
 # ------------------------------------------------------------------ main --
 
 def main():
@@ -306,6 +340,10 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run one plain device copy of this size (calibrates the HBM byte counters)")
+    ap.add_argument("--stacked", action="store_true",
+                    help="also time the code example's gather with caller weights and its reduction over the k "
+                         "neighbours: snls_gather_stacked + snls_stacked_reduce, and the fused snls_gather_reduce "
+                         "(Cout = C), outside the timed step")
     ap.add_argument("--summarize-profiles", metavar="DIR", default=None,
                     help="write the profiles/ summary of --workload from the rocprofv3 outputs under DIR and exit")
     args = ap.parse_args()
@@ -315,8 +353,7 @@ def main():
         print(json.dumps(rec["search_call"], indent=1))
         return
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: the path has no multi-GPU mode in this build "
-              "(see DESIGN.md for how it would shard)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the path has no multi-GPU mode", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -404,8 +441,8 @@ def main():
         "alg_tflops": w["f_search"] / t_search / 1e12, "alg_frac": w["f_search"] / t_search / PEAK_FP32_VALU,
         "call_ms": t_search * 1e3, "profiled_call_ms": sc["avg_us"] / 1e3 if sc and sc.get("avg_us") else None,
     }
-    metric = BASELINE_METRIC if args.workload == DEFAULT_WORKLOAD else \
-        BASELINE_METRIC.replace("config 2", args.workload + (" (+backward)" if train else "")).replace(
+    metric = METRIC if args.workload == DEFAULT_WORKLOAD else \
+        METRIC.replace("config 2", args.workload + (" (+backward)" if train else "")).replace(
             "search+top-k+aggregate", "search+top-k+aggregate" + ("+backward" if train else ""))
     line = {
         "metric": metric, "value": value, "unit": "queries/s", "n_gpus": 1, "steps": args.steps,
@@ -428,6 +465,8 @@ def main():
         line["backward_ms"] = t_bwd * 1e3
         line["backward_alg_tflops"] = w["f_bwd"] / t_bwd / 1e12
         line["backward_alg_frac_hbm"] = w["bwd_bytes"] / t_bwd / PEAK_HBM
+    if args.stacked:
+        line["stacked"] = time_stacked(B, torch, x, dists, inds, p, scale, dev)
     if not args.no_cpu_baseline and args.workload == DEFAULT_WORKLOAD:
         line["cpu_baseline"] = cpu_baseline(c, args.cpu_budget)
     print(json.dumps(line), flush=True)

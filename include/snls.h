@@ -15,6 +15,9 @@
  *                   aggregation;
  *   snls_aggregate_stacked, snls_chain_flows  the code example's neighbour-
  *                   stacked gather and its forward/backward flow interface;
+ *   snls_gather_stacked, snls_stacked_reduce, snls_gather_reduce  the
+ *                   example's gather with caller weights and its reduction
+ *                   over the k neighbours (App. B);
  *   snls_aggregate_static  snls_aggregate without a caller workspace, for
  *                   callers that cannot allocate.
  *
@@ -71,7 +74,7 @@
 extern "C" {
 #endif
 
-#define SNLS_ABI_VERSION 3
+#define SNLS_ABI_VERSION 4
 
 typedef enum {
   SNLS_OK = 0,
@@ -245,10 +248,62 @@ snls_status snls_aggregate_stacked(const float* v, const float* dists, const flo
 snls_status snls_chain_flows(const float* fflow, const float* bflow, int32_t B, int32_t T, int32_t H, int32_t W,
                              int32_t wt, float* flows, void* stream);
 
+/* snls_gather_stacked -- the gather of the paper's code example, with the
+ * caller's weights (the example passes softmax(-10 * dists) computed outside
+ * the gather): stacked[b,hd,l,t,f,y,x] = (1/cnt(y,x)) * sum over the query
+ * patches covering (y,x) of weights_l * v~(frame_l, f, (y,x) + disp_l),
+ * the aggregation of Sec. 3.2 restricted to the l-th neighbours (cnt: the
+ * number of query patches covering the pixel; pixels no patch covers are
+ * 0).  A neighbour whose weight is 0, whose frame entry is not an integer in
+ * [0,T) or whose displacement is not finite contributes nothing; weights are
+ * otherwise used as given (finite values expected).
+ *   v          device, (B, T, C, H, W)
+ *   weights    device, (B, HD, T, nH, nW, k) with k = p->k >= 1
+ *   inds       device, (B, HD, T, nH, nW, k, 3), as snls_search returns
+ *   stacked    device out, (B, HD, k, T, C/HD, H, W), fully overwritten
+ *   workspace  device scratch of at least
+ *              snls_workspace_size(SNLS_OP_GATHER_STACKED, p) bytes, 256-byte
+ *              aligned (a channels-last copy of v; 0 bytes when a head has
+ *              more than 64 channels, a channel count not a multiple of 4, or
+ *              an 8 x 8 pixel tile more than 256 covering queries)
+ * Errors: SNLS_ERR_INVALID_ARG, SNLS_ERR_UNSUPPORTED (outputs beyond 2^40
+ * elements), SNLS_ERR_WORKSPACE, SNLS_ERR_HIP. */
+snls_status snls_gather_stacked(const float* v, const float* weights, const float* inds, const snls_params* p,
+                                float* stacked, void* workspace, size_t workspace_bytes, void* stream);
+
+/* snls_stacked_reduce -- the reduction over the k neighbours that follows
+ * the gather in the code example: the stacked tensor rearranged to
+ * ((b t), (hd f), k, h, w) and convolved with a (Cout, C, k, 1, 1) kernel at
+ * stride (k, 1, 1):
+ *   out[b,t,o,y,x] = sum over hd, f, l of proj[o, hd*C/HD + f, l] * stacked[b,hd,l,t,f,y,x]
+ * computed in fp32 on the matrix cores.
+ *   stacked  device, (B, HD, k, T, C/HD, H, W)
+ *   proj     device, (Cout, C, k) (the conv3d kernel without its 1 x 1 tail)
+ *   cout     output channels, 1 <= cout <= 128
+ *   out      device out, (B, T, Cout, H, W), fully overwritten
+ * Errors: SNLS_ERR_INVALID_ARG; SNLS_ERR_UNSUPPORTED when C/HD is not a
+ * multiple of 4 or exceeds 64, or cout > 128; SNLS_ERR_HIP. */
+snls_status snls_stacked_reduce(const float* stacked, const float* proj, const snls_params* p, int32_t cout,
+                                float* out, void* stream);
+
+/* snls_gather_reduce -- snls_stacked_reduce(snls_gather_stacked(...)) in one
+ * pass: the stacked tensor (k times the size of v) is formed per 8 x 8 pixel
+ * tile on chip and never written.  Arguments as in the two calls; workspace:
+ * at least snls_workspace_size(SNLS_OP_GATHER_REDUCE, p) bytes, 256-byte
+ * aligned (a channels-last copy of v).
+ * Errors: SNLS_ERR_INVALID_ARG; SNLS_ERR_UNSUPPORTED beyond the limits of
+ * snls_stacked_reduce or when an 8 x 8 tile has more than 256 covering
+ * queries; SNLS_ERR_WORKSPACE; SNLS_ERR_HIP. */
+snls_status snls_gather_reduce(const float* v, const float* weights, const float* inds, const float* proj,
+                               const snls_params* p, int32_t cout, float* out, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
 #define SNLS_OP_SEARCH 0
 #define SNLS_OP_AGGREGATE 1
 #define SNLS_OP_BACKWARD 2
 #define SNLS_OP_AGGREGATE_STACKED 3
+#define SNLS_OP_GATHER_STACKED 4
+#define SNLS_OP_GATHER_REDUCE 5
 
 /* Device workspace in bytes that operation op needs for parameters p
  * (0 when none is needed; (size_t)-1 for invalid arguments). */

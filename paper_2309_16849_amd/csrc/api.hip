@@ -55,7 +55,50 @@ size_t snls_workspace_size(int op, const snls_params* p) {
   if (op == SNLS_OP_BACKWARD) return check_params(p, true, &g) == SNLS_OK ? backward_ws_bytes(g) : (size_t)-1;
   if (op == SNLS_OP_AGGREGATE_STACKED)
     return check_params(p, true, &g) == SNLS_OK ? aggregate_stacked_ws_bytes(g) : (size_t)-1;
+  if (op == SNLS_OP_GATHER_STACKED) return check_params(p, true, &g) == SNLS_OK ? gather_ws_bytes(g) : (size_t)-1;
+  if (op == SNLS_OP_GATHER_REDUCE)
+    return check_params(p, true, &g) == SNLS_OK ? (size_t)g.B * g.T * g.C * g.HW * sizeof(float) : (size_t)-1;
   return (size_t)-1;
+}
+
+snls_status snls_gather_stacked(const float* v, const float* weights, const float* inds, const snls_params* p,
+                                float* stacked, void* workspace, size_t workspace_bytes, void* stream) {
+  Geo g;
+  snls_status st = check_params(p, true, &g);
+  if (st != SNLS_OK) return st;
+  if (!v || !weights || !inds || !stacked) return SNLS_ERR_INVALID_ARG;
+  if ((long long)g.B * g.HD * g.k * g.T * ((g.Ch + 15) / 16) * g.HW > 0xffffffffLL * 256) return SNLS_ERR_UNSUPPORTED;
+  const size_t need = gather_ws_bytes(g);
+  if (need > 0 && (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)))
+    return SNLS_ERR_WORKSPACE;
+  if ((st = device_ready()) != SNLS_OK) return st;
+  return launch_gather_stacked(v, weights, inds, g, stacked, workspace, as_stream(stream));
+}
+
+snls_status snls_stacked_reduce(const float* stacked, const float* proj, const snls_params* p, int32_t cout,
+                                float* out, void* stream) {
+  Geo g;
+  snls_status st = check_params(p, true, &g);
+  if (st != SNLS_OK) return st;
+  if (!stacked || !proj || !out || cout < 1) return SNLS_ERR_INVALID_ARG;
+  if (!reduce_supported(g, cout)) return SNLS_ERR_UNSUPPORTED;
+  if ((st = device_ready()) != SNLS_OK) return st;
+  return launch_stacked_reduce(stacked, proj, g, cout, out, as_stream(stream));
+}
+
+snls_status snls_gather_reduce(const float* v, const float* weights, const float* inds, const float* proj,
+                               const snls_params* p, int32_t cout, float* out, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  Geo g;
+  snls_status st = check_params(p, true, &g);
+  if (st != SNLS_OK) return st;
+  if (!v || !weights || !inds || !proj || !out || cout < 1) return SNLS_ERR_INVALID_ARG;
+  if (!reduce_supported(g, cout) || !gather_tile_supported(g)) return SNLS_ERR_UNSUPPORTED;
+  const size_t need = (size_t)g.B * g.T * g.C * g.HW * sizeof(float);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255))
+    return SNLS_ERR_WORKSPACE;
+  if ((st = device_ready()) != SNLS_OK) return st;
+  return launch_gather_reduce(v, weights, inds, proj, g, cout, out, workspace, as_stream(stream));
 }
 
 snls_status snls_search(const float* q, const float* k, const float* flows, const snls_params* p, float* dists,

@@ -102,8 +102,12 @@ __global__ void __launch_bounds__(256) aggregate_stacked_kernel(const float* __r
       if (w < 0 || w % g.s0 || w / g.s0 >= g.nW) continue;
       const long long row = ((((long long)b * g.HD + hd) * g.T + t) * g.nH + h / g.s0) * g.nW + w / g.s0;
       const float wl = wts[row * g.k + l];
-      if (wl == 0.f) continue;
       const float* ind = inds + (row * g.k + l) * 3;
+      // a neighbour adds nothing when its weight is 0, its frame is not an
+      // integer in [0, T) or its offset is not finite
+      if (wl == 0.f || !(ind[0] >= 0.f && ind[0] < (float)g.T) || ind[0] != floorf(ind[0]) ||
+          !(fabsf(ind[1]) < kFarDisp) || !(fabsf(ind[2]) < kFarDisp))
+        continue;
       int ny, nx;
       float ay, ax;
       split_disp(ind[1], &ny, &ay);
@@ -124,6 +128,17 @@ __global__ void __launch_bounds__(256) aggregate_stacked_kernel(const float* __r
 }
 
 size_t aggregate_stacked_ws_bytes(const Geo& g) { return (size_t)g.rows * (size_t)g.k * sizeof(float); }
+
+// The stacked gather with the caller's weights, one thread per output.
+snls_status launch_gather_stacked_plain(const float* v, const float* weights, const float* inds, const Geo& g,
+                                        float* stacked, hipStream_t s) {
+  if (g.rows == 0) return SNLS_OK;
+  const int nchunk = (g.Ch + kStChunk - 1) / kStChunk;
+  const long long n = (long long)g.B * g.HD * g.k * g.T * nchunk * g.HW;
+  hipLaunchKernelGGL(aggregate_stacked_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, v, weights, inds,
+                     g, stacked);
+  return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+}
 
 snls_status launch_aggregate_stacked(const float* v, const float* dists, const float* inds, const Geo& g,
                                      float scale, float* stacked, void* ws, hipStream_t s) {

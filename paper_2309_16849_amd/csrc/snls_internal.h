@@ -49,6 +49,13 @@ size_t aggregate_ws_bytes(const Geo& g);
 size_t backward_ws_bytes(const Geo& g);
 // Device workspace of snls_aggregate_stacked: softmax weights (rows x k).
 size_t aggregate_stacked_ws_bytes(const Geo& g);
+// The code example's gather with caller weights and its reduction over the
+// neighbours: tiled kernels when a head has at most 64 channels (a multiple
+// of 4) and a tile at most 256 covering queries; their workspace is a
+// channels-last copy of v (0 bytes when the plain gather runs instead).
+bool gather_tile_supported(const Geo& g);
+bool reduce_supported(const Geo& g, int cout);
+size_t gather_ws_bytes(const Geo& g);
 
 // The tiled search path (S_Q = 1, P <= 7, Ws <= 9; inner product with
 // S_K <= 1, squared L2 with S_K = 1) and its workspace: the inner-product
@@ -99,6 +106,14 @@ snls_status launch_chain_flows(const float* fflow, const float* bflow, int B, in
                                float* flows, hipStream_t s);
 snls_status launch_aggregate_stacked(const float* v, const float* dists, const float* inds, const Geo& g,
                                      float scale, float* stacked, void* ws, hipStream_t s);
+snls_status launch_gather_stacked_plain(const float* v, const float* weights, const float* inds, const Geo& g,
+                                        float* stacked, hipStream_t s);
+snls_status launch_gather_stacked(const float* v, const float* weights, const float* inds, const Geo& g,
+                                  float* stacked, void* ws, hipStream_t s);
+snls_status launch_stacked_reduce(const float* stacked, const float* proj, const Geo& g, int cout, float* out,
+                                  hipStream_t s);
+snls_status launch_gather_reduce(const float* v, const float* weights, const float* inds, const float* proj,
+                                 const Geo& g, int cout, float* out, void* ws, hipStream_t s);
 snls_status launch_backward(const float* q, const float* k, const float* v, const float* dists, const float* inds,
                             const float* grad_out, const float* grad_dists, const Geo& g, float scale,
                             float* grad_q, float* grad_k, float* grad_v, float* grad_flows, float* Gws,

@@ -7,7 +7,8 @@ call raises.
 
 Functions carry the C names: snls_search, snls_topk, snls_aggregate,
 snls_backward, snls_aggregate_stacked, snls_chain_flows, snls_aggregate_static,
-snls_workspace_size, snls_status_string, snls_abi_version.
+snls_gather_stacked, snls_stacked_reduce, snls_gather_reduce, snls_workspace_size,
+snls_status_string, snls_abi_version.
 Parameters are plain dicts with keys B, T, C, H, W, HD, ws, wt, ps, stride0,
 stride1, k, dist_type (see ``params_from_dict``).
 """
@@ -24,11 +25,12 @@ LIB_PATH = os.path.join(_HERE, "libsnls.so")
 SNLS_OK, SNLS_ERR_INVALID_ARG, SNLS_ERR_UNSUPPORTED, SNLS_ERR_HIP, SNLS_ERR_WORKSPACE, SNLS_ERR_SCRATCH = range(6)
 SNLS_DIST_PROD, SNLS_DIST_L2 = 0, 1
 SNLS_OP_SEARCH, SNLS_OP_AGGREGATE, SNLS_OP_BACKWARD, SNLS_OP_AGGREGATE_STACKED = 0, 1, 2, 3
+SNLS_OP_GATHER_STACKED, SNLS_OP_GATHER_REDUCE = 4, 5
 SNLS_MAX_K = 128
 SNLS_STATIC_SCRATCH_BYTES = 64 << 20
 SYMBOLS = ("snls_search", "snls_topk", "snls_aggregate", "snls_backward", "snls_workspace_size",
            "snls_status_string", "snls_abi_version", "snls_aggregate_stacked", "snls_chain_flows",
-           "snls_aggregate_static")
+           "snls_aggregate_static", "snls_gather_stacked", "snls_stacked_reduce", "snls_gather_reduce")
 
 
 class SnlsParams(ctypes.Structure):
@@ -63,13 +65,17 @@ def load_library():
         lib.snls_aggregate_stacked.argtypes = [P, P, P, PP, F32, P, P, SZ, P]
         lib.snls_chain_flows.argtypes = [P, P, I32, I32, I32, I32, I32, P, P]
         lib.snls_aggregate_static.argtypes = [P, P, P, PP, F32, P, P]
+        lib.snls_gather_stacked.argtypes = [P, P, P, PP, P, P, SZ, P]
+        lib.snls_stacked_reduce.argtypes = [P, P, PP, I32, P, P]
+        lib.snls_gather_reduce.argtypes = [P, P, P, P, PP, I32, P, P, SZ, P]
         lib.snls_workspace_size.argtypes = [ctypes.c_int, PP]
         lib.snls_workspace_size.restype = SZ
         lib.snls_status_string.argtypes = [ctypes.c_int]
         lib.snls_status_string.restype = ctypes.c_char_p
         lib.snls_abi_version.argtypes = []
         for f in ("snls_search", "snls_topk", "snls_aggregate", "snls_backward", "snls_abi_version",
-                  "snls_aggregate_stacked", "snls_chain_flows", "snls_aggregate_static"):
+                  "snls_aggregate_stacked", "snls_chain_flows", "snls_aggregate_static", "snls_gather_stacked",
+                  "snls_stacked_reduce", "snls_gather_reduce"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -284,3 +290,64 @@ def snls_chain_flows(fflow, bflow, wt: int, flows=None, stream=None):
     _check(lib.snls_chain_flows(_ptr(fflow), _ptr(bflow), B, T, H, W, int(wt), _ptr(flows), _stream(stream)),
            "snls_chain_flows")
     return flows
+
+
+def stacked_shape(p: dict):
+    return (p["B"], p["HD"], p["k"], p["T"], p["C"] // p["HD"], p["H"], p["W"])
+
+
+def snls_gather_stacked(v, weights, inds, p: dict, stacked=None, workspace=None, stream=None):
+    """The example's gather with caller weights; returns (B, HD, k, T, C/HD, H, W)."""
+    lib = load_library()
+    _dev(v, "v", video_shape(p))
+    shp = out_shape(p)
+    _dev(weights, "weights", shp)
+    _dev(inds, "inds", shp + (3,))
+    if stacked is None:
+        stacked = torch.empty(stacked_shape(p), device=v.device, dtype=torch.float32)
+    _dev(stacked, "stacked", stacked_shape(p))
+    if workspace is None:
+        workspace = workspace_for(SNLS_OP_GATHER_STACKED, p, v.device)
+    prm = params_from_dict(p)
+    _check(lib.snls_gather_stacked(_ptr(v), _ptr(weights), _ptr(inds), ctypes.byref(prm), _ptr(stacked),
+                                   _ptr(workspace), workspace.numel() * 4, _stream(stream)), "snls_gather_stacked")
+    return stacked
+
+
+def snls_stacked_reduce(stacked, proj, p: dict, out=None, stream=None):
+    """Reduction over the k neighbours with kernel proj (Cout, C, k); returns (B, T, Cout, H, W)."""
+    lib = load_library()
+    _dev(stacked, "stacked", stacked_shape(p))
+    _dev(proj, "proj")
+    cout = proj.shape[0]
+    if tuple(proj.shape) != (cout, p["C"], p["k"]):
+        raise ValueError("proj must be (Cout, C, k)")
+    if out is None:
+        out = torch.empty((p["B"], p["T"], cout, p["H"], p["W"]), device=stacked.device, dtype=torch.float32)
+    _dev(out, "out", (p["B"], p["T"], cout, p["H"], p["W"]))
+    prm = params_from_dict(p)
+    _check(lib.snls_stacked_reduce(_ptr(stacked), _ptr(proj), ctypes.byref(prm), cout, _ptr(out), _stream(stream)),
+           "snls_stacked_reduce")
+    return out
+
+
+def snls_gather_reduce(v, weights, inds, proj, p: dict, out=None, workspace=None, stream=None):
+    """Gather with caller weights and reduction over the k neighbours in one pass; returns (B, T, Cout, H, W)."""
+    lib = load_library()
+    _dev(v, "v", video_shape(p))
+    shp = out_shape(p)
+    _dev(weights, "weights", shp)
+    _dev(inds, "inds", shp + (3,))
+    _dev(proj, "proj")
+    cout = proj.shape[0]
+    if tuple(proj.shape) != (cout, p["C"], p["k"]):
+        raise ValueError("proj must be (Cout, C, k)")
+    if out is None:
+        out = torch.empty((p["B"], p["T"], cout, p["H"], p["W"]), device=v.device, dtype=torch.float32)
+    _dev(out, "out", (p["B"], p["T"], cout, p["H"], p["W"]))
+    if workspace is None:
+        workspace = workspace_for(SNLS_OP_GATHER_REDUCE, p, v.device)
+    prm = params_from_dict(p)
+    _check(lib.snls_gather_reduce(_ptr(v), _ptr(weights), _ptr(inds), _ptr(proj), ctypes.byref(prm), cout, _ptr(out),
+                                  _ptr(workspace), workspace.numel() * 4, _stream(stream)), "snls_gather_reduce")
+    return out

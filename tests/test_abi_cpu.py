@@ -41,7 +41,7 @@ def test_exports_every_declared_function(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert B.snls_abi_version() == 3
+    assert B.snls_abi_version() == 4
     assert B.snls_status_string(0) == "ok"
     for s in range(1, 6):
         assert B.snls_status_string(s) not in ("ok", "unknown status")
@@ -208,3 +208,31 @@ def test_aggregate_static_validation(lib):
     assert need > B.SNLS_STATIC_SCRATCH_BYTES
     assert lib.snls_aggregate_static(FAKE, FAKE, FAKE, ctypes.byref(big), 1.0, FAKE, None) == B.SNLS_ERR_SCRATCH
     assert B.snls_status_string(B.SNLS_ERR_SCRATCH) != "unknown status"
+
+
+def test_gather_and_reduce_validation(lib):
+    """The example's gather with caller weights and the reduction over the k
+    neighbours validate their arguments and workspaces before any device
+    work; unsupported head widths and output channel counts are refused."""
+    prm = _params()  # C = 8, HD = 2: 4 channels per head
+    ws_g = lib.snls_workspace_size(B.SNLS_OP_GATHER_STACKED, ctypes.byref(prm))
+    ws_r = lib.snls_workspace_size(B.SNLS_OP_GATHER_REDUCE, ctypes.byref(prm))
+    assert ws_g == ws_r == 1 * 3 * 8 * 16 * 17 * 4  # channels-last copy of v
+    # 3 channels per head: the plain gather needs no workspace, the fused pass is refused
+    odd = _params(C=6, HD=2)
+    assert lib.snls_workspace_size(B.SNLS_OP_GATHER_STACKED, ctypes.byref(odd)) == 0
+    assert lib.snls_gather_reduce(FAKE, FAKE, FAKE, FAKE, ctypes.byref(odd), 8, FAKE, FAKE, BIG,
+                                  None) == B.SNLS_ERR_UNSUPPORTED
+    assert lib.snls_gather_stacked(FAKE, None, FAKE, ctypes.byref(prm), FAKE, FAKE, BIG, None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_gather_stacked(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, ws_g - 1,
+                                   None) == B.SNLS_ERR_WORKSPACE
+    assert lib.snls_gather_stacked(FAKE, FAKE, FAKE, ctypes.byref(_params(k=0)), FAKE, FAKE, BIG,
+                                   None) == B.SNLS_ERR_INVALID_ARG
+    for cout, st in ((0, B.SNLS_ERR_INVALID_ARG), (129, B.SNLS_ERR_UNSUPPORTED)):
+        assert lib.snls_stacked_reduce(FAKE, FAKE, ctypes.byref(prm), cout, FAKE, None) == st
+        assert lib.snls_gather_reduce(FAKE, FAKE, FAKE, FAKE, ctypes.byref(prm), cout, FAKE, FAKE, BIG, None) == st
+    assert lib.snls_stacked_reduce(FAKE, None, ctypes.byref(prm), 8, FAKE, None) == B.SNLS_ERR_INVALID_ARG
+    assert lib.snls_gather_reduce(FAKE, FAKE, FAKE, FAKE, ctypes.byref(prm), 8, FAKE, None, BIG,
+                                  None) == B.SNLS_ERR_WORKSPACE
+    wide = _params(C=160, HD=2)  # 80 channels per head
+    assert lib.snls_stacked_reduce(FAKE, FAKE, ctypes.byref(wide), 8, FAKE, None) == B.SNLS_ERR_UNSUPPORTED

@@ -645,13 +645,14 @@ def _covering_rows(p, pix):
     return np.array(sorted(rows), np.int64)
 
 
-@pytest.mark.parametrize("idx", [0, 1, 2, 3, 4, 5, 6, 7, 8, 9])
+@pytest.mark.parametrize("idx", [0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10])
 def test_workload_parity(dev, idx):
     """Search + top-k + aggregation of each workload at its full size (the
     launch configuration bench.py times), on sampled rows and pixels: the five
     workloads, then the paper's own benchmark shapes (320 x 320 at query
-    strides 1 and 2, the 152 x 152 x 192 memory shape) and the 480 x 854
-    workload at key stride 1/2 and at query stride 2."""
+    strides 1 and 2, the 152 x 152 x 192 memory shape), the 480 x 854
+    workload at key stride 1/2 and at query stride 2, and the settings of
+    the paper's code example."""
     c = _cfg(idx)
     p, scale = c["params"], c["scale"]
     print("workload %d (%s) %s" % (idx, c["name"], p), flush=True)
@@ -779,3 +780,74 @@ def test_backward_adjoint_full_size(dev):
     lhs = float((out.double() * y.double()).sum())
     rhs = float((x.double() * gv.double()).sum())
     assert abs(lhs - rhs) <= REL * max(abs(lhs), 1.0)
+
+
+# ------------------------------------- the example's gather and reduction --
+
+@pytest.mark.parametrize("ps,stride0,HD,C,k,stride1", [(3, 1, 2, 16, 10, 0.5), (7, 1, 1, 64, 6, 1.0),
+                                                       (1, 2, 4, 64, 12, 1.0), (5, 2, 1, 8, 5, 1.0),
+                                                       (3, 3, 2, 12, 4, 1.0), (3, 1, 1, 70, 4, 1.0),
+                                                       (2, 1, 2, 6, 3, 1.0)],
+                         ids=["example", "p7", "p1-heads", "p5-s2", "p3-s3", "c70-plain", "c3-plain"])
+def test_gather_stacked_and_reduce(dev, ps, stride0, HD, C, k, stride1):
+    """The example's gather with caller weights (weights with zeros, negative
+    values, neighbours outside the clip or with non-finite offsets), the
+    reduction over the k neighbours (MFMA) from the gathered stack, and the
+    fused gather + reduction, against the oracle."""
+    p = small_params(T=5, C=C, HD=HD, H=21, W=19, ws=5, wt=2, ps=ps, stride0=stride0, stride1=stride1, k=k)
+    q, kk_, v, flows = _inputs(p, 7100 + ps * 10 + C)
+    r = np.random.default_rng(7200 + C + ps)
+    gd, gi = B.snls_search(_d(q, dev), _d(kk_, dev), _d(flows, dev), p)
+    torch.cuda.synchronize()
+    inds = _h(gi).copy()
+    shp = _h(gd).shape
+    wts = r.standard_normal(shp).astype(np.float32)
+    wts[r.random(shp) < 0.2] = 0.0
+    flat = inds.reshape(-1, 3)
+    sel = r.choice(flat.shape[0], 7, replace=False)
+    flat[sel[:3], 0] = np.array([5.0, -1.0, 2.5], np.float32)  # outside the clip / not an integer
+    flat[sel[3:5], 1] = np.nan
+    flat[sel[5:], 2] = np.inf
+    vd, wd, idd = _d(v, dev), _d(wts, dev), _d(inds, dev)
+    st = B.snls_gather_stacked(vd, wd, idd, p)
+    torch.cuda.synchronize()
+    ref = oracle.gather_stacked(v, wts, inds, p)
+    assert_close(_h(st), ref, "stacked gather")
+    if C // HD % 4 == 0 and C // HD <= 64:
+        for cout in (C, 20, 128):
+            proj = r.standard_normal((cout, C, k)).astype(np.float32) / np.sqrt(C * k)
+            pd = _d(proj, dev)
+            red = B.snls_stacked_reduce(st, pd, p)
+            fused = B.snls_gather_reduce(vd, wd, idd, pd, p)
+            torch.cuda.synchronize()
+            ref_red = oracle.stacked_reduce(ref, proj, p)
+            assert_close(_h(red), oracle.stacked_reduce(_h(st), proj, p), "reduction of the GPU stack (cout %d)" % cout)
+            assert_close(_h(fused), ref_red, "fused gather + reduction (cout %d)" % cout)
+    else:
+        proj = _d(np.zeros((8, C, k), np.float32), dev)
+        with pytest.raises(B.SnlsError):
+            B.snls_gather_reduce(vd, wd, idd, proj, p)
+
+
+def test_gather_reduce_example_full_size(dev):
+    """The code example's pipeline at its own size (5 x 128 x 128, 16
+    features in 2 heads, k = 10, key stride 1/2): search, weights = a softmax
+    over the row with temperature 10 computed by the caller as in the example
+    (+10 for the inner product, larger is better; invalid neighbours, -inf,
+    get weight 0), the gather that keeps the neighbours apart, and the fused
+    gather + reduction with a (16, 16, 10) kernel, element by element against
+    the oracle."""
+    from workloads import config_index
+    c = _cfg(config_index("example_appb"))
+    p = c["params"]
+    qd, fd = _d(c["q"], dev), _d(c["flows"], dev)
+    gd, gi = B.snls_search(qd, qd, fd, p)
+    w = torch.softmax(10.0 * gd, dim=-1).contiguous()
+    assert torch.isfinite(w).all()
+    proj = torch.from_numpy(np.random.default_rng(31).standard_normal((16, 16, 10)).astype(np.float32) / 12.0).to(dev)
+    st = B.snls_gather_stacked(qd, w, gi, p)
+    out = B.snls_gather_reduce(qd, w, gi, proj, p)
+    torch.cuda.synchronize()
+    ref = oracle.gather_stacked(c["v"], _h(w), _h(gi), p)
+    assert_close(_h(st), ref, "stacked gather (example size)")
+    assert_close(_h(out), oracle.stacked_reduce(ref, _h(proj), p), "gather + reduction (example size)")

@@ -60,6 +60,11 @@ CONFIGS = [
     # patches overlapping by 5 of 7 pixels).
     dict(name="denoise480x854_s2", B=1, T=5, C=64, H=480, W=854, HD=1, ws=9, wt=2, ps=7, stride0=2, stride1=1.0,
          k=10, dist_type=0, scale=1.0, video="motion", amp=16.0, backward=False, data_of="denoise480x854"),
+    # The settings of the paper's code example (App. B): 5 frames of
+    # 128 x 128, 16 features in 2 heads, ws = 5, wt = 2, ps = 3, k = 10, key
+    # stride 1/2 (its gather and reduction over the k neighbours follow).
+    dict(name="example_appb", B=1, T=5, C=16, H=128, W=128, HD=2, ws=5, wt=2, ps=3, stride0=1, stride1=0.5,
+         k=10, dist_type=0, scale=1.0, video="motion", amp=4.0, backward=False),
 ]
 
 # The five workloads every parity test covers; the paper's benchmark shapes
