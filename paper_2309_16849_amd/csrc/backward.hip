@@ -4,17 +4,23 @@
 //
 // Two passes over query rows, one wave per row (lanes = channels of the
 // head, 64 at a time), on channels-last copies of q, k, v and grad_out so
-// that every read and every scatter of one (row, neighbour, patch pixel, tap)
-// touches 64 consecutive floats:
+// that every read of one (row, neighbour, patch pixel, tap) touches 64
+// consecutive floats:
 //  1. aggregation: G_l = sum_{p,c} g~(p,c) v~_l(p,c) with g~ = grad_out/count,
-//     dV += w_l g~ scattered through the bilinear taps, and the position
-//     gradient w_l * g~ . dv~_l/dpos into the row's flow slot;
+//     the softmax weight w_l, and the position gradient w_l * g~ . dv~_l/dpos
+//     into the row's flow slot;
 //  2. softmax + similarity: dd_l = sign*scale*w_l*(G_l - sum_m w_m G_m)
-//     (+ grad_dists), then dQ, dK (through the taps) and the position
-//     gradient dd_l * dscore/dpos into the flow slot.
-// Scatters are float atomics into channels-last accumulators (the order of
-// the additions, hence the last bits, may vary between runs), transposed into
-// the caller's gradients at the end.
+//     (+ grad_dists), dQ, and the position gradient dd_l * dscore/dpos.
+// The terms on the key frames -- dV = w_l g~ and dK = dd_l q (L2: 2 dd_l
+// (k~ - q)) spread through the bilinear taps -- are then summed per 8 x 8
+// key tile: the (row, neighbour) pairs are sorted by the tiles their tap
+// blocks touch and one wave per tile adds their terms in LDS and writes the
+// tile once.  dQ and the flow gradients are float atomics, and the order of
+// a tile's entries follows the atomics of the sort, so the last bits may
+// vary between runs.
+// Heads wider than 64 channels (and P > 7) scatter every term with float
+// atomics instead.  All accumulators are channels-last, transposed into the
+// caller's gradients at the end.
 #include "snls_internal.h"
 
 namespace snls {
@@ -52,6 +58,14 @@ SNLS_DEV float wave_max(float v) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
   return v;
+}
+
+// p[off] when ok, else 0, with the load itself unconditional (address 0
+// when !ok, which the caller keeps valid), so that a run of such reads is
+// issued back to back instead of one per branch.
+SNLS_DEV float load_or_zero(const float* __restrict__ p, long long off, bool ok) {
+  const float v = p[ok ? off : 0];
+  return ok ? v : 0.f;
 }
 
 // Softmax statistics of a row (lanes over the k entries): max and sum of
@@ -290,24 +304,46 @@ __global__ void __launch_bounds__(256) backward_search_kernel(const float* __res
   }
 }
 
-// ---- merged scatters (P <= 7, at most 64 channels per head) ----
+// 32-bit buffer view of a channels-last video (below 2^30 bytes on the
+// paths that use it): a read sums the byte offsets of a row, a pixel column
+// and the lane's channel, each kOOB when outside the frame (or, for the
+// channel, past the head's channels); any sum with a kOOB term lies in
+// [2^30, 3 * 2^30], past the buffer and without wrapping, so it reads 0.
+constexpr unsigned kOOB = 1u << 30, kOOB2 = kOOB;
+struct ClView {
+  __amdgpu_buffer_rsrc_t rs;
+  unsigned rowb, colb;
+  SNLS_DEV float ld(unsigned off) const {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+  }
+};
+SNLS_DEV ClView cl_view(const float* x, const Geo& g) {
+  ClView v;
+  v.rs = __builtin_amdgcn_make_buffer_rsrc((void*)x, (short)0, (int)(unsigned)((long long)g.B * g.T * g.HW * g.C * 4),
+                                           0x00020000);
+  v.rowb = (unsigned)(g.W * g.C) * 4u;
+  v.colb = (unsigned)g.C * 4u;
+  return v;
+}
+
+// ---- per-row terms (P <= 7, at most 64 channels per head) ----
 //
 // For one neighbour l of a row, the taps of the P x P patch pixels cover a
-// (P+1) x (P+1) block of key positions at the neighbour's integer offset;
-// each lane (channel) sums the block in registers and adds it with (P+1)^2
-// atomics instead of 4 P^2.  dQ of a patch pixel sums over all k neighbours
-// of the row and is added once per pixel.
+// (P+1) x (P+1) block of key positions at the neighbour's integer offset,
+// read once into registers.  These kernels form the per-row terms -- G_l,
+// the flow gradients, dQ (summed over all k neighbours of the row and added
+// once per patch pixel) -- and store the pair scalars w_l and dd_l; the dK and
+// dV terms on the key blocks are summed per key tile further below.
 template <int P>
 __global__ void __launch_bounds__(256) backward_agg_block_kernel(const float* __restrict__ vcl,
                                                                  const float* __restrict__ dists,
                                                                  const float* __restrict__ inds,
-                                                                 const float* __restrict__ gocl, Geo g,
-                                                                 float scale, float* __restrict__ dvcl,
-                                                                 float* __restrict__ grad_flows,
-                                                                 float* __restrict__ Gws) {
+                                                                 const float* __restrict__ gs, Geo g,
+                                                                 float scale, float* __restrict__ grad_flows,
+                                                                 float* __restrict__ Gws, float* __restrict__ wl_out) {
   constexpr int PB = P + 1;
   const int lane = threadIdx.x & 63;
-  const long long row = (long long)blockIdx.x * bwd::WAVES + (threadIdx.x >> 6);
+  const long long row = (long long)blockIdx.x * bwd::WAVES + __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   if (row >= g.rows) return;  // whole wave
   const RowPos rp = row_pos(row, g);
   const float* drow = dists + row * g.k;
@@ -315,49 +351,55 @@ __global__ void __launch_bounds__(256) backward_agg_block_kernel(const float* __
   const float sscale = (g.dist == SNLS_DIST_PROD ? 1.f : -1.f) * scale;
   float m, z;
   softmax_stats(drow, g.k, sscale, lane, &m, &z);
-  const long long qbase = ((long long)rp.b * g.T + rp.t) * g.HW;
-  const int cc = rp.hd * g.Ch + lane;
   const bool act = lane < g.Ch;
+  const unsigned ch4 = act ? (unsigned)(rp.hd * g.Ch + lane) * 4u : kOOB2;
   const int lo = -(P / 2);
-  // g~ = grad_out / count of the patch pixels (0 outside the frame)
+  const ClView gv_ = cl_view(gs, g), vv = cl_view(vcl, g);
+  // g~ = grad_out / count of the patch pixels (gs holds it; 0 outside the frame)
   float gg[P * P];
+  {
+    unsigned ro[P], co[P];
 #pragma unroll
-  for (int ph = 0; ph < P; ++ph)
-#pragma unroll
-    for (int pw = 0; pw < P; ++pw) {
-      const int y = rp.h + lo + ph, x = rp.w + lo + pw;
-      float v = 0.f;
-      if (act && y >= 0 && y < g.H && x >= 0 && x < g.W) {
-        const float inv =
-            1.f / (float)(cover_count_1d(y, g.s0, g.nH, lo, P) * cover_count_1d(x, g.s0, g.nW, lo, P));
-        v = gocl[(qbase + (long long)y * g.W + x) * g.C + cc] * inv;
-      }
-      gg[ph * P + pw] = v;
+    for (int i = 0; i < P; ++i) {
+      const int y = rp.h + lo + i, x = rp.w + lo + i;
+      ro[i] = y >= 0 && y < g.H ? (unsigned)((rp.b * g.T + rp.t) * g.H + y) * gv_.rowb : kOOB;
+      co[i] = x >= 0 && x < g.W ? (unsigned)x * gv_.colb : kOOB;
     }
+#pragma unroll
+    for (int ph = 0; ph < P; ++ph)
+#pragma unroll
+      for (int pw = 0; pw < P; ++pw) gg[ph * P + pw] = gv_.ld(ro[ph] + co[pw] + ch4);
+  }
   for (int l = 0; l < g.k; ++l) {
     int t2, ny, nx;
     float ay, ax;
     if (!isfinite(drow[l]) || !(z > 0.f) || !neighbour(irow, l, g, &t2, &ny, &nx, &ay, &ax)) {
-      if (lane == 0) Gws[row * g.k + l] = 0.f;
+      if (lane == 0) {
+        Gws[row * g.k + l] = 0.f;
+        wl_out[row * g.k + l] = 0.f;
+      }
       continue;
     }
     const float wl = expf(sscale * drow[l] - m) / z;
-    const float* vf = vcl + ((long long)rp.b * g.T + t2) * g.HW * g.C + cc;
+    if (lane == 0) wl_out[row * g.k + l] = wl;
     const int Y0 = rp.h + lo + ny, X0 = rp.w + lo + nx;  // block origin
     // the block of V values (0 outside the frame)
     float vb[PB * PB];
+    {
+      unsigned kr[PB], kc[PB];
 #pragma unroll
-    for (int a = 0; a < PB; ++a)
-#pragma unroll
-      for (int c = 0; c < PB; ++c) {
-        const int Y = Y0 + a, X = X0 + c;
-        vb[a * PB + c] = act && Y >= 0 && Y < g.H && X >= 0 && X < g.W ? vf[((long long)Y * g.W + X) * g.C] : 0.f;
+      for (int i = 0; i < PB; ++i) {
+        const int Y = Y0 + i, X = X0 + i;
+        kr[i] = Y >= 0 && Y < g.H ? (unsigned)((rp.b * g.T + t2) * g.H + Y) * vv.rowb : kOOB;
+        kc[i] = X >= 0 && X < g.W ? (unsigned)X * vv.colb : kOOB;
       }
+#pragma unroll
+      for (int a = 0; a < PB; ++a)
+#pragma unroll
+        for (int c = 0; c < PB; ++c) vb[a * PB + c] = vv.ld(kr[a] + kc[c] + ch4);
+    }
     const float w00 = (1.f - ay) * (1.f - ax), w01 = (1.f - ay) * ax, w10 = ay * (1.f - ax), w11 = ay * ax;
     float Gl = 0.f, fh = 0.f, fw = 0.f;
-    float blk[PB * PB];
-#pragma unroll
-    for (int i = 0; i < PB * PB; ++i) blk[i] = 0.f;
 #pragma unroll
     for (int ph = 0; ph < P; ++ph)
 #pragma unroll
@@ -369,20 +411,6 @@ __global__ void __launch_bounds__(256) backward_agg_block_kernel(const float* __
         Gl = fmaf(gv, val, Gl);
         fh = fmaf(gv, (1.f - ax) * (v10 - v00) + ax * (v11 - v01), fh);
         fw = fmaf(gv, (1.f - ay) * (v01 - v00) + ay * (v11 - v10), fw);
-        const float sv = wl * gv;
-        blk[ph * PB + pw] = fmaf(w00, sv, blk[ph * PB + pw]);
-        blk[ph * PB + pw + 1] = fmaf(w01, sv, blk[ph * PB + pw + 1]);
-        blk[(ph + 1) * PB + pw] = fmaf(w10, sv, blk[(ph + 1) * PB + pw]);
-        blk[(ph + 1) * PB + pw + 1] = fmaf(w11, sv, blk[(ph + 1) * PB + pw + 1]);
-      }
-    float* dvf = dvcl + ((long long)rp.b * g.T + t2) * g.HW * g.C + cc;
-#pragma unroll
-    for (int a = 0; a < PB; ++a)
-#pragma unroll
-      for (int c = 0; c < PB; ++c) {
-        const int Y = Y0 + a, X = X0 + c;
-        if (act && Y >= 0 && Y < g.H && X >= 0 && X < g.W && blk[a * PB + c] != 0.f)
-          atomicAdd(dvf + ((long long)Y * g.W + X) * g.C, blk[a * PB + c]);
       }
     Gl = wave_sum(Gl);
     fh = wave_sum(fh);
@@ -402,11 +430,11 @@ __global__ void __launch_bounds__(256) backward_search_block_kernel(const float*
                                                                     const float* __restrict__ grad_dists, Geo g,
                                                                     float scale, const float* __restrict__ Gws,
                                                                     float* __restrict__ dqcl,
-                                                                    float* __restrict__ dkcl,
-                                                                    float* __restrict__ grad_flows) {
+                                                                    float* __restrict__ grad_flows,
+                                                                    float* __restrict__ dd_out) {
   constexpr int PB = P + 1;
   const int lane = threadIdx.x & 63;
-  const long long row = (long long)blockIdx.x * bwd::WAVES + (threadIdx.x >> 6);
+  const long long row = (long long)blockIdx.x * bwd::WAVES + __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   if (row >= g.rows) return;  // whole wave
   const RowPos rp = row_pos(row, g);
   const float* drow = dists + row * g.k;
@@ -422,42 +450,56 @@ __global__ void __launch_bounds__(256) backward_search_block_kernel(const float*
       if (isfinite(drow[l])) wg += expf(sscale * drow[l] - m) / z * Grow[l];
   wg = wave_sum(wg);
   const long long qbase = ((long long)rp.b * g.T + rp.t) * g.HW;
-  const int cc = rp.hd * g.Ch + lane;
   const bool act = lane < g.Ch;
+  const int cc = rp.hd * g.Ch + (act ? lane : 0);  // a channel of the head for every lane
+  const unsigned ch4 = act ? (unsigned)cc * 4u : kOOB2;
   const int lo = -(P / 2);
+  const ClView qv_ = cl_view(qcl, g), kv_ = cl_view(kcl, g);
   float qv[P * P], dq[P * P];
+  {
+    unsigned ro[P], co[P];
 #pragma unroll
-  for (int ph = 0; ph < P; ++ph)
-#pragma unroll
-    for (int pw = 0; pw < P; ++pw) {
-      const int y = rp.h + lo + ph, x = rp.w + lo + pw;
-      const bool in = act && y >= 0 && y < g.H && x >= 0 && x < g.W;
-      qv[ph * P + pw] = in ? qcl[(qbase + (long long)y * g.W + x) * g.C + cc] : 0.f;
-      dq[ph * P + pw] = 0.f;
+    for (int i = 0; i < P; ++i) {
+      const int y = rp.h + lo + i, x = rp.w + lo + i;
+      ro[i] = y >= 0 && y < g.H ? (unsigned)((rp.b * g.T + rp.t) * g.H + y) * qv_.rowb : kOOB;
+      co[i] = x >= 0 && x < g.W ? (unsigned)x * qv_.colb : kOOB;
     }
+#pragma unroll
+    for (int ph = 0; ph < P; ++ph)
+#pragma unroll
+      for (int pw = 0; pw < P; ++pw) {
+        qv[ph * P + pw] = qv_.ld(ro[ph] + co[pw] + ch4);
+        dq[ph * P + pw] = 0.f;
+      }
+  }
   for (int l = 0; l < g.k; ++l) {
     int t2, ny, nx;
     float ay, ax;
-    if (!isfinite(drow[l]) || !neighbour(irow, l, g, &t2, &ny, &nx, &ay, &ax)) continue;
+    const bool ok = isfinite(drow[l]) && neighbour(irow, l, g, &t2, &ny, &nx, &ay, &ax);
     float dd = 0.f;
-    if (z > 0.f) dd = sscale * (expf(sscale * drow[l] - m) / z) * (Grow[l] - wg);
-    if (grad_dists) dd += grad_dists[row * g.k + l];
-    if (dd == 0.f) continue;
-    const float* kf = kcl + ((long long)rp.b * g.T + t2) * g.HW * g.C + cc;
+    if (ok) {
+      if (z > 0.f) dd = sscale * (expf(sscale * drow[l] - m) / z) * (Grow[l] - wg);
+      if (grad_dists) dd += grad_dists[row * g.k + l];
+    }
+    if (lane == 0) dd_out[row * g.k + l] = dd;
+    if (!ok || dd == 0.f) continue;
     const int Y0 = rp.h + lo + ny, X0 = rp.w + lo + nx;
     float kb[PB * PB];
+    {
+      unsigned kr[PB], kc[PB];
 #pragma unroll
-    for (int a = 0; a < PB; ++a)
-#pragma unroll
-      for (int c = 0; c < PB; ++c) {
-        const int Y = Y0 + a, X = X0 + c;
-        kb[a * PB + c] = act && Y >= 0 && Y < g.H && X >= 0 && X < g.W ? kf[((long long)Y * g.W + X) * g.C] : 0.f;
+      for (int i = 0; i < PB; ++i) {
+        const int Y = Y0 + i, X = X0 + i;
+        kr[i] = Y >= 0 && Y < g.H ? (unsigned)((rp.b * g.T + t2) * g.H + Y) * kv_.rowb : kOOB;
+        kc[i] = X >= 0 && X < g.W ? (unsigned)X * kv_.colb : kOOB;
       }
+#pragma unroll
+      for (int a = 0; a < PB; ++a)
+#pragma unroll
+        for (int c = 0; c < PB; ++c) kb[a * PB + c] = kv_.ld(kr[a] + kc[c] + ch4);
+    }
     const float w00 = (1.f - ay) * (1.f - ax), w01 = (1.f - ay) * ax, w10 = ay * (1.f - ax), w11 = ay * ax;
     float fh = 0.f, fw = 0.f;
-    float blk[PB * PB];
-#pragma unroll
-    for (int i = 0; i < PB * PB; ++i) blk[i] = 0.f;
 #pragma unroll
     for (int ph = 0; ph < P; ++ph) {
       const int y = rp.h + lo + ph;
@@ -478,23 +520,10 @@ __global__ void __launch_bounds__(256) backward_search_block_kernel(const float*
           dk = -dqv;
         }
         dq[ph * P + pw] += dqv;
-        blk[ph * PB + pw] = fmaf(w00, dk, blk[ph * PB + pw]);
-        blk[ph * PB + pw + 1] = fmaf(w01, dk, blk[ph * PB + pw + 1]);
-        blk[(ph + 1) * PB + pw] = fmaf(w10, dk, blk[(ph + 1) * PB + pw]);
-        blk[(ph + 1) * PB + pw + 1] = fmaf(w11, dk, blk[(ph + 1) * PB + pw + 1]);
         fh = fmaf(dk, (1.f - ax) * (k10 - k00) + ax * (k11 - k01), fh);
         fw = fmaf(dk, (1.f - ay) * (k01 - k00) + ay * (k11 - k10), fw);
       }
     }
-    float* dkf = dkcl + ((long long)rp.b * g.T + t2) * g.HW * g.C + cc;
-#pragma unroll
-    for (int a = 0; a < PB; ++a)
-#pragma unroll
-      for (int c = 0; c < PB; ++c) {
-        const int Y = Y0 + a, X = X0 + c;
-        if (act && Y >= 0 && Y < g.H && X >= 0 && X < g.W && blk[a * PB + c] != 0.f)
-          atomicAdd(dkf + ((long long)Y * g.W + X) * g.C, blk[a * PB + c]);
-      }
     fh = wave_sum(fh);
     fw = wave_sum(fw);
     if (lane == 0) add_flow_grad(grad_flows, g, rp, t2, fh, fw);
@@ -509,13 +538,471 @@ __global__ void __launch_bounds__(256) backward_search_block_kernel(const float*
     }
 }
 
+// ---- dK and dV gathered per key tile (P <= 7, at most 64 channels per head) ----
+//
+// The dK and dV terms of one (row, neighbour) pair fall on the (P+1) x (P+1)
+// block of key pixels its taps read.  Instead of adding them to global memory
+// with float atomics, the pairs are sorted by the 8 x 8 key tiles their
+// block touches (a counting sort: counts per tile, exclusive scan, fill), and
+// one workgroup per tile sums the terms of its pairs in LDS and writes the
+// tile once.  The row kernels above provide the per-pair scalars: the softmax
+// weight w_l (dV = w_l g~ through the taps) and dd_l (dK = dd_l q, or
+// 2 dd_l (k~ - q) for L2, through the taps).
+namespace bin {
+constexpr int TS = 8;            // key tile side (pixels): a tap block (P+1 <= 8) spans at most 2 x 2 tiles
+constexpr int NPIX = TS * TS;
+constexpr int SORT_THREADS = 256;
+}  // namespace bin
+
+// Tiles [ty0, ty1] x [tx0, tx1] of the key frame that the tap block with
+// origin (Y0, X0) touches inside the frame; false when it misses the frame.
+SNLS_DEV bool block_tiles(int Y0, int X0, int P, const Geo& g, int* ty0, int* ty1, int* tx0, int* tx1) {
+  const int ylo = max(Y0, 0), yhi = min(Y0 + P, g.H - 1);
+  const int xlo = max(X0, 0), xhi = min(X0 + P, g.W - 1);
+  if (ylo > yhi || xlo > xhi) return false;
+  *ty0 = ylo / bin::TS;
+  *ty1 = yhi / bin::TS;
+  *tx0 = xlo / bin::TS;
+  *tx1 = xhi / bin::TS;
+  return true;
+}
+
+// What the tile pass needs of one pair, decoded once: query frame and pixel,
+// tap-block origin and fractions, dd_l.  32 bytes, one scalar load.
+struct alignas(32) PairRec {
+  int t, h, w, Y0, X0;
+  float ay, ax, dd;
+};
+constexpr unsigned kNoBin = 0xffffffffu;
+
+// Per pair (one thread each, pair indices below 2^29): decode the row and the
+// neighbour, write its record and its first tile -- bin | (second tile row)
+// << 30 | (second tile column) << 31, kNoBin when the block misses every
+// frame or the pair contributes nothing -- and count its tiles.
+__global__ void __launch_bounds__(bin::SORT_THREADS) bin_count_kernel(const float* __restrict__ dists,
+                                                                      const float* __restrict__ inds,
+                                                                      const float* __restrict__ dd, Geo g, int nty,
+                                                                      int ntx, PairRec* __restrict__ recs,
+                                                                      unsigned* __restrict__ binfo,
+                                                                      unsigned* __restrict__ counts);
+
+// Adds, for every lane with `has`, one to cnt[key] -- one atomic per distinct
+// key of the wave -- and returns the lane's slot: the counter's previous value
+// plus the number of lower lanes with the same key.
+SNLS_DEV unsigned wave_count_add(unsigned* cnt, bool has, unsigned key) {
+  const int lane = (int)__lane_id();
+  unsigned long long pend = __ballot(has);
+  unsigned slot = 0;
+  while (pend) {
+    const int leader = (int)__builtin_ctzll(pend);
+    const unsigned lk = (unsigned)__builtin_amdgcn_readlane((int)key, leader);
+    const bool mine = ((pend >> lane) & 1ull) && key == lk;
+    const unsigned long long same = __ballot(mine);
+    unsigned base = 0;
+    if (lane == leader) base = atomicAdd(cnt + lk, (unsigned)__popcll(same));
+    base = (unsigned)__builtin_amdgcn_readlane((int)base, leader);
+    if (mine) slot = base + (unsigned)lanes_below(same);
+    pend &= ~same;
+  }
+  return slot;
+}
+
+// The (up to 4) tiles of a pair from its first-tile word.
+SNLS_DEV int expand_bins(unsigned bi, int ntx, unsigned (&bins)[4]) {
+  if (bi == kNoBin) return 0;
+  const unsigned b0 = bi & 0x3fffffffu;
+  const bool dy = (bi >> 30) & 1u, dx = (bi >> 31) & 1u;
+  int n = 0;
+  bins[n++] = b0;
+  if (dx) bins[n++] = b0 + 1;
+  if (dy) bins[n++] = b0 + (unsigned)ntx;
+  if (dy && dx) bins[n++] = b0 + (unsigned)ntx + 1;
+  return n;
+}
+
+__global__ void __launch_bounds__(bin::SORT_THREADS) bin_count_kernel(const float* __restrict__ dists,
+                                                                      const float* __restrict__ inds,
+                                                                      const float* __restrict__ dd, Geo g, int nty,
+                                                                      int ntx, PairRec* __restrict__ recs,
+                                                                      unsigned* __restrict__ binfo,
+                                                                      unsigned* __restrict__ counts) {
+  const unsigned pair = blockIdx.x * bin::SORT_THREADS + threadIdx.x;
+  const unsigned npair = (unsigned)(g.rows * g.k);
+  unsigned bi = kNoBin;
+  if (pair < npair) {
+    const unsigned k = (unsigned)g.k;
+    unsigned row = pair / k;
+    const int l = (int)(pair - row * k);
+    const float* irow = inds + (size_t)row * k * 3;
+    const float dist = dists[pair];
+    // row -> (b, hd, t, mh, mw), 32-bit (rows below 2^29)
+    const int mw = (int)(row % (unsigned)g.nW);
+    row /= (unsigned)g.nW;
+    const int mh = (int)(row % (unsigned)g.nH);
+    row /= (unsigned)g.nH;
+    const int t = (int)(row % (unsigned)g.T);
+    row /= (unsigned)g.T;
+    const int hd = (int)(row % (unsigned)g.HD);
+    const int b = (int)(row / (unsigned)g.HD);
+    const int h = mh * g.s0, w = mw * g.s0;
+    int t2, ny, nx, ty0, ty1, tx0, tx1;
+    float ay, ax;
+    if (isfinite(dist) && neighbour(irow, l, g, &t2, &ny, &nx, &ay, &ax)) {
+      const int Y0 = h + g.lo + ny, X0 = w + g.lo + nx;
+      if (block_tiles(Y0, X0, g.ps, g, &ty0, &ty1, &tx0, &tx1)) {
+        const unsigned b0 = ((unsigned)(((b * g.HD + hd) * g.T + t2) * nty + ty0)) * (unsigned)ntx + (unsigned)tx0;
+        bi = b0 | ((unsigned)(ty1 > ty0) << 30) | ((unsigned)(tx1 > tx0) << 31);
+        PairRec r;
+        r.t = t;
+        r.h = h;
+        r.w = w;
+        r.Y0 = Y0;
+        r.X0 = X0;
+        r.ay = ay;
+        r.ax = ax;
+        r.dd = dd[pair];
+        recs[pair] = r;
+      }
+    }
+    binfo[pair] = bi;
+  }
+  unsigned bins[4];
+  const int n = expand_bins(bi, ntx, bins);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) (void)wave_count_add(counts, i < n, i < n ? bins[i] : 0u);
+}
+
+// Exclusive scan of the counts (one workgroup): offsets[i] = sum of counts
+// below i, offsets[nbins] = total.
+__global__ void __launch_bounds__(1024) bin_scan_kernel(const unsigned* __restrict__ counts, int nbins,
+                                                        unsigned* __restrict__ offsets) {
+  __shared__ unsigned part[1024];
+  const int tid = threadIdx.x;
+  const int per = (nbins + 1023) / 1024;
+  const int i0 = min(tid * per, nbins), i1 = min(i0 + per, nbins);
+  unsigned sum = 0;
+  for (int i = i0; i < i1; ++i) sum += counts[i];
+  part[tid] = sum;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const unsigned v = tid >= off ? part[tid - off] : 0u;
+    __syncthreads();
+    part[tid] += v;
+    __syncthreads();
+  }
+  unsigned run = part[tid] - sum;  // exclusive prefix of this thread's segment
+  for (int i = i0; i < i1; ++i) {
+    offsets[i] = run;
+    run += counts[i];
+  }
+  if (tid == 1023) offsets[nbins] = part[1023];
+}
+
+__global__ void __launch_bounds__(bin::SORT_THREADS) bin_fill_kernel(const unsigned* __restrict__ binfo, Geo g,
+                                                                     int ntx, const unsigned* __restrict__ offsets,
+                                                                     unsigned* __restrict__ cursor,
+                                                                     unsigned* __restrict__ entries) {
+  const unsigned pair = blockIdx.x * bin::SORT_THREADS + threadIdx.x;
+  const unsigned bi = pair < (unsigned)(g.rows * g.k) ? binfo[pair] : kNoBin;
+  unsigned bins[4];
+  const int n = expand_bins(bi, ntx, bins);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const unsigned slot = wave_count_add(cursor, i < n, i < n ? bins[i] : 0u);
+    if (i < n) entries[offsets[bins[i]] + slot] = pair;
+  }
+}
+
+// One wave per (key tile, term): blockIdx.y + term0 = 0 sums dK, 1 sums dV.  The
+// wave owns its 8 x 8 x 64 tile in LDS, so every addition is a plain
+// read-add-write (float atomics in LDS are far slower here), in the order of
+// the tile's entry list; lanes are the head's channels.  Entries go in
+// batches of 64: lane i decodes entry i of the batch (read offsets of its
+// patch rows and columns, LDS rows and columns of its tap block, its tap
+// weights times its scalar), and the wave then takes the
+// entries from the lanes one at a time, two per step, the reads of a step
+// issued a few steps before its additions.
+// Reads are 32-bit buffer loads whose offset is pushed past the buffer
+// (reads 0) for pixels outside the frame.  The tile is written to the
+// channels-last accumulator (every pixel of every tile, so the accumulator
+// needs no clearing).  gs is grad_out already divided by the cover count of
+// its pixel.
+template <int P, bool L2K>
+__global__ void __launch_bounds__(64) bin_accumulate_kernel(const float* __restrict__ qcl,
+                                                            const float* __restrict__ kcl,
+                                                            const float* __restrict__ gs,
+                                                            const PairRec* __restrict__ recs,
+                                                            const float* __restrict__ wl,
+                                                            const unsigned* __restrict__ offsets,
+                                                            const unsigned* __restrict__ entries, Geo g, int nty,
+                                                            int ntx, int term0, float* __restrict__ dkcl,
+                                                            float* __restrict__ dvcl) {
+  using namespace bin;
+  constexpr int PB = P + 1;
+  constexpr int lo = -(P / 2);
+  constexpr unsigned OOB = 1u << 30;  // tensors are below 2^30 bytes: OOB + any in-frame offset reads 0
+  // 9 x 9 pixels: the 8 x 8 tile plus a spare row and column that take the
+  // block pixels outside the tile (written, never read back)
+  constexpr int LP = TS + 1;
+  __shared__ float acc[LP * LP * 64];
+  const int lane = threadIdx.x;
+  const bool is_v = (int)blockIdx.y + term0 == 1;
+  // Tile order: consecutive workgroups land on different XCDs (8 per
+  // device), so XCD x takes a contiguous run of a list in which the tile
+  // rows are cut into 8 bands and each band lists its rows of every frame:
+  // tiles that read the same query patches share an L2, and every XCD gets
+  // the same share of every frame.
+  int f, ty, tx;
+  {
+    const int nwg = (int)gridDim.x, nfr = nwg / (nty * ntx);
+    const int xcd = (int)blockIdx.x % 8, xq = nwg / 8, xrem = nwg % 8;
+    int j = xcd * xq + min(xcd, xrem) + (int)blockIdx.x / 8;  // position in the band-major list
+    int band = 0, r0 = 0, r1 = (nty + 7) / 8;
+    while (j >= nfr * (r1 - r0) * ntx) {  // bands of rows [ceil(i nty / 8), ceil((i+1) nty / 8))
+      j -= nfr * (r1 - r0) * ntx;
+      ++band;
+      r0 = r1;
+      r1 = ((band + 1) * nty + 7) / 8;
+    }
+    const int per = (r1 - r0) * ntx;
+    f = j / per;
+    ty = r0 + (j % per) / ntx;
+    tx = j % ntx;
+  }
+  const int bn = (f * nty + ty) * ntx + tx;
+  const int t2 = f % g.T, hd = (f / g.T) % g.HD, b = f / (g.T * g.HD);
+  const int ty0 = ty * TS, tx0 = tx * TS;
+  const int ch = hd * g.Ch + (lane < g.Ch ? lane : 0);  // a channel of the head for every lane
+  const unsigned ch4 = (unsigned)ch * 4u;
+  constexpr bool l2k = L2K;  // the dK pass of the L2 distance (reads the key block too)
+  const int H = g.H, W = g.W;
+  const unsigned rowb = (unsigned)(W * g.C) * 4u, colb = (unsigned)g.C * 4u;  // bytes per row / pixel
+  const unsigned tbytes = (unsigned)((long long)g.B * g.T * g.HW * g.C * 4);
+  const __amdgpu_buffer_rsrc_t src_rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(is_v ? gs : qcl), (short)0, (int)tbytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t k_rs = __builtin_amdgcn_make_buffer_rsrc((void*)kcl, (short)0, (int)tbytes, 0x00020000);
+  const unsigned kframe = (unsigned)((b * g.T + t2) * H) * rowb;  // byte offset of key frame (b, t2)
+#pragma unroll
+  for (int i = 0; i < LP * LP; ++i) acc[i * 64 + lane] = 0.f;
+
+  // What the wave needs of one entry (per lane: the entry of that lane).
+  struct Ent {
+    unsigned ro[P], co[P];     // byte offsets of the patch rows / columns (OOB outside the frame)
+    unsigned kr[PB], kc[PB];   // the same for the key block (L2 only)
+    int lr[PB], lc[PB];        // LDS index of each block row / column (spare row / column outside the tile)
+    int pin;                   // patch rows | columns << 8 inside the frame (L2 only)
+    float w00, w01, w10, w11;  // tap weights (times the scalar unless L2)
+    float sc;                  // the scalar (0: nothing to add)
+  };
+  auto decode = [&](const PairRec& r, float s) {
+    Ent en;
+    const unsigned qrow0 = (unsigned)((b * g.T + r.t) * H) * rowb;
+    int pr = 0, pc = 0;
+#pragma unroll
+    for (int i = 0; i < P; ++i) {
+      const int y = r.h + lo + i, x = r.w + lo + i;
+      const bool yin = y >= 0 && y < H, xin = x >= 0 && x < W;
+      en.ro[i] = yin ? qrow0 + (unsigned)y * rowb : OOB;
+      en.co[i] = xin ? (unsigned)x * colb : OOB;
+      pr |= (int)yin << i;
+      pc |= (int)xin << i;
+    }
+    en.pin = pr | (pc << 8);
+    bool anyr = false, anyc = false;
+#pragma unroll
+    for (int i = 0; i < PB; ++i) {
+      const int Y = r.Y0 + i, X = r.X0 + i;
+      en.kr[i] = Y >= 0 && Y < H ? kframe + (unsigned)Y * rowb : OOB;
+      en.kc[i] = X >= 0 && X < W ? (unsigned)X * colb : OOB;
+      const bool rin = Y >= ty0 && Y < ty0 + TS, cin = X >= tx0 && X < tx0 + TS;
+      en.lr[i] = (rin ? Y - ty0 : TS) * LP * 64;
+      en.lc[i] = (cin ? X - tx0 : TS) * 64;
+      anyr |= rin;
+      anyc |= cin;
+    }
+    const float m = l2k ? 1.f : s;
+    en.w00 = (1.f - r.ay) * (1.f - r.ax) * m;
+    en.w01 = (1.f - r.ay) * r.ax * m;
+    en.w10 = r.ay * (1.f - r.ax) * m;
+    en.w11 = r.ay * r.ax * m;
+    en.sc = (anyr && anyc) ? s : 0.f;
+    return en;
+  };
+  // entry i of the batch, from lane i
+  auto get = [&](const Ent& v, int i) {
+    Ent en;
+    auto rd = [&](unsigned x) { return (unsigned)__builtin_amdgcn_readlane((int)x, i); };
+    auto rdf = [&](float x) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), i)); };
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      en.ro[j] = rd(v.ro[j]);
+      en.co[j] = rd(v.co[j]);
+    }
+    if (l2k) {
+#pragma unroll
+      for (int j = 0; j < PB; ++j) {
+        en.kr[j] = rd(v.kr[j]);
+        en.kc[j] = rd(v.kc[j]);
+      }
+      en.pin = (int)rd((unsigned)v.pin);
+    }
+#pragma unroll
+    for (int j = 0; j < PB; ++j) {
+      en.lr[j] = (int)rd((unsigned)v.lr[j]);
+      en.lc[j] = (int)rd((unsigned)v.lc[j]);
+    }
+    en.w00 = rdf(v.w00);
+    en.w01 = rdf(v.w01);
+    en.w10 = rdf(v.w10);
+    en.w11 = rdf(v.w11);
+    en.sc = rdf(v.sc);
+    return en;
+  };
+  // patch values (and for L2 the key block) of one entry
+  auto load = [&](const Ent& en, float (&tp)[P * P], float (&kb)[PB * PB]) {
+#pragma unroll
+    for (int ph = 0; ph < P; ++ph)
+#pragma unroll
+      for (int pw = 0; pw < P; ++pw)
+        tp[ph * P + pw] = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(src_rs, en.ro[ph] + en.co[pw] + ch4, 0, 0));
+    if (l2k) {
+#pragma unroll
+      for (int a = 0; a < PB; ++a)
+#pragma unroll
+        for (int c = 0; c < PB; ++c)
+          kb[a * PB + c] =
+              __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(k_rs, en.kr[a] + en.kc[c] + ch4, 0, 0));
+    }
+  };
+  // term of each patch pixel, spread through the taps into the tile:
+  // block pixel (a, c) collects w00, w01, w10, w11 of patch pixels (a, c),
+  // (a, c-1), (a-1, c), (a-1, c-1)
+  auto spread = [&](const Ent& en, float (&tp)[P * P], const float (&kb)[PB * PB]) {
+    if (l2k) {
+      // dK of patch pixel p: 2 dd (k~ - q); patch pixels outside the frame
+      // add nothing (their q and taps read 0, but the k~ term would not vanish)
+      const float u00 = en.w00, u01 = en.w01, u10 = en.w10, u11 = en.w11;
+#pragma unroll
+      for (int ph = 0; ph < P; ++ph)
+#pragma unroll
+        for (int pw = 0; pw < P; ++pw) {
+          const float kv = u00 * kb[ph * PB + pw] + u01 * kb[ph * PB + pw + 1] + u10 * kb[(ph + 1) * PB + pw] +
+                           u11 * kb[(ph + 1) * PB + pw + 1];
+          const bool in = ((en.pin >> ph) & (en.pin >> (8 + pw)) & 1) != 0;
+          tp[ph * P + pw] = in ? -(2.f * en.sc * (tp[ph * P + pw] - kv)) : 0.f;
+        }
+    }
+    // no branches: every block pixel reads and writes (outside the tile the
+    // spare row / column), so the reads of the block go out together
+    float cur[PB * PB];
+#pragma unroll
+    for (int a = 0; a < PB; ++a)
+#pragma unroll
+      for (int c = 0; c < PB; ++c) cur[a * PB + c] = acc[en.lr[a] + en.lc[c] + lane];
+#pragma unroll
+    for (int a = 0; a < PB; ++a)
+#pragma unroll
+      for (int c = 0; c < PB; ++c) {
+        float v = cur[a * PB + c];
+        if (a > 0 && c > 0) v = fmaf(en.w11, tp[(a - 1) * P + c - 1], v);
+        if (a > 0 && c < P) v = fmaf(en.w10, tp[(a - 1) * P + c], v);
+        if (a < P && c > 0) v = fmaf(en.w01, tp[a * P + c - 1], v);
+        if (a < P && c < P) v = fmaf(en.w00, tp[a * P + c], v);
+        acc[en.lr[a] + en.lc[c] + lane] = v;
+      }
+  };
+
+  const int e0 = (int)offsets[bn], e1 = (int)offsets[bn + 1];
+  for (int eb = e0; eb < e1; eb += 64) {
+    const int n = min(64, e1 - eb);
+    const bool mine = lane < n;
+    const unsigned pr = entries[eb + (mine ? lane : 0)];
+    const PairRec rv = recs[pr];
+    const float s = is_v ? wl[pr] : rv.dd;
+    const Ent vb = decode(rv, mine ? s : 0.f);
+    // Two entries per step, pipelined D steps deep: the reads of step
+    // i + D - 1 are issued before the additions of step i (D = 2 for P <= 3
+    // without the key block, else 1: what the registers hold).
+    constexpr int D = P <= 3 && !L2K ? 2 : 1;
+    Ent es[D][2];
+    float ts[D][2][P * P];
+    float ks[D][2][PB * PB];
+    auto fetch = [&](int step, Ent (&e)[2], float (&t)[2][P * P], float (&kk)[2][PB * PB]) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int idx = 2 * step + u;
+        e[u] = get(vb, idx & 63);
+        if (idx >= n) e[u].sc = 0.f;
+        if (e[u].sc != 0.f) load(e[u], t[u], kk[u]);
+      }
+    };
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d) fetch(d, es[d], ts[d], ks[d]);
+    for (int st = 0; 2 * st < n; st += D) {
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        const int nd = (d + D - 1) % D;
+        fetch(st + d + D - 1, es[nd], ts[nd], ks[nd]);
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+          if (es[d][u].sc != 0.f) spread(es[d][u], ts[d][u], ks[d][u]);
+      }
+    }
+  }
+  float* dst = (is_v ? dvcl : dkcl) + ((long long)b * g.T + t2) * g.HW * g.C + ch;
+  const bool act = lane < g.Ch;
+#pragma unroll
+  for (int px = 0; px < NPIX; ++px) {
+    const int Y = ty0 + px / TS, X = tx0 + px % TS;
+    if (act && Y < H && X < W) dst[((long long)Y * W + X) * g.C] = acc[((px / TS) * LP + px % TS) * 64 + lane];
+  }
+}
+
+// grad_out (channels-last) divided in place by the number of query patches
+// covering each pixel: 4 pixels per workgroup, lanes over the channels.
+__global__ void __launch_bounds__(256) scale_by_cover_kernel(float* __restrict__ gcl, Geo g, int lo, int P) {
+  const long long pix = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (pix >= (long long)g.B * g.T * g.HW) return;
+  const long long p = pix % g.HW;
+  const int y = (int)(p / g.W), x = (int)(p % g.W);
+  const int n = cover_count_1d(y, g.s0, g.nH, lo, P) * cover_count_1d(x, g.s0, g.nW, lo, P);
+  const float inv = n > 0 ? 1.f / (float)n : 0.f;
+  float* row = gcl + pix * g.C;
+  for (int c = threadIdx.x & 63; c < g.C; c += 64) row[c] = row[c] * inv;
+}
+
+// The binned path: P <= 7, at most 64 channels per head, bin entries (up
+// to 4 per pair) counted in 31 bits, videos below 2^30 bytes.
+static bool bin_supported(const Geo& g) {
+  if (g.ps > 7 || g.Ch > 64) return false;
+  if (g.rows * (long long)g.k >= (1LL << 29)) return false;
+  if ((long long)g.B * g.T * g.HW * g.C * 4 >= (1LL << 30)) return false;  // 32-bit buffer offsets
+  const long long nbins = (long long)g.B * g.HD * g.T * ((g.H + bin::TS - 1) / bin::TS) * ((g.W + bin::TS - 1) / bin::TS);
+  return nbins < (1LL << 30);
+}
+static long long bin_count(const Geo& g) {
+  return (long long)g.B * g.HD * g.T * ((g.H + bin::TS - 1) / bin::TS) * ((g.W + bin::TS - 1) / bin::TS);
+}
+
 // Workspace: G (rows x k), channels-last copies of q, k, v and grad_out, and
-// channels-last accumulators of dq, dk and dv (256-byte aligned pieces).
+// channels-last accumulators of dq, dk and dv (256-byte aligned pieces); on
+// the binned path also the pair scalars dd and w (rows x k each), the pair
+// records and first-tile words, the tile counts, cursors and offsets, and the
+// sorted entries (up to 4 per pair).
 static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 size_t backward_ws_bytes(const Geo& g) {
   const size_t nvid = (size_t)g.B * g.T * g.C * g.HW * sizeof(float);
-  return align256((size_t)g.rows * (size_t)g.k * sizeof(float)) + 7 * align256(nvid);
+  const size_t pairs = (size_t)g.rows * (size_t)g.k;
+  size_t b = align256(pairs * sizeof(float)) + 7 * align256(nvid);
+  if (bin_supported(g)) {
+    const size_t nb = (size_t)bin_count(g);
+    b += 2 * align256(pairs * sizeof(float)) + align256(pairs * sizeof(PairRec)) + align256(pairs * sizeof(unsigned)) +
+         2 * align256(nb * sizeof(unsigned)) + align256((nb + 1) * sizeof(unsigned)) +
+         align256(4 * pairs * sizeof(unsigned));
+  }
+  return b;
 }
 
 static void zero(float* p, long long n, hipStream_t s) {
@@ -531,10 +1018,12 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
                             hipStream_t s) {
   const long long nvid = (long long)g.B * g.T * g.C * g.HW;
   const long long nflow = (long long)g.B * g.T * g.nslot * 2 * g.HW;
+  const long long pairs = g.rows * (long long)g.k;
   const size_t vb = align256((size_t)nvid * sizeof(float));
+  const size_t pb = align256((size_t)pairs * sizeof(float));
   char* base = reinterpret_cast<char*>(ws);
   float* Gws = reinterpret_cast<float*>(base);
-  base += align256((size_t)g.rows * (size_t)g.k * sizeof(float));
+  base += pb;
   float* qcl = reinterpret_cast<float*>(base);
   float* kcl = reinterpret_cast<float*>(base + vb);
   float* vcl = reinterpret_cast<float*>(base + 2 * vb);
@@ -542,9 +1031,33 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
   float* dqcl = reinterpret_cast<float*>(base + 4 * vb);
   float* dkcl = reinterpret_cast<float*>(base + 5 * vb);
   float* dvcl = reinterpret_cast<float*>(base + 6 * vb);
+  base += 7 * vb;
+  const bool binned = bin_supported(g) && g.rows > 0;
+  const int nty = (g.H + bin::TS - 1) / bin::TS, ntx = (g.W + bin::TS - 1) / bin::TS;
+  const long long nbins = bin_count(g);
+  float *ddws = nullptr, *wlws = nullptr;
+  PairRec* recs = nullptr;
+  unsigned *binfo = nullptr, *counts = nullptr, *cursor = nullptr, *offsets = nullptr, *entries = nullptr;
+  if (binned) {
+    const size_t nbb = align256((size_t)nbins * sizeof(unsigned));
+    ddws = reinterpret_cast<float*>(base);
+    base += pb;
+    wlws = reinterpret_cast<float*>(base);
+    base += pb;
+    recs = reinterpret_cast<PairRec*>(base);
+    base += align256((size_t)pairs * sizeof(PairRec));
+    binfo = reinterpret_cast<unsigned*>(base);
+    base += align256((size_t)pairs * sizeof(unsigned));
+    counts = reinterpret_cast<unsigned*>(base);
+    cursor = reinterpret_cast<unsigned*>(base + nbb);
+    offsets = reinterpret_cast<unsigned*>(base + 2 * nbb);
+    entries = reinterpret_cast<unsigned*>(base + 2 * nbb + align256((size_t)(nbins + 1) * sizeof(unsigned)));
+    zero(reinterpret_cast<float*>(counts), 2 * (long long)(nbb / sizeof(unsigned)), s);  // counts and cursors
+  } else {
+    zero(dkcl, nvid, s);
+    zero(dvcl, nvid, s);
+  }
   zero(dqcl, nvid, s);
-  zero(dkcl, nvid, s);
-  zero(dvcl, nvid, s);
   zero(grad_flows, nflow, s);
   if (nvid > 0) {
     launch_to_channels_last(q, g, qcl, s);
@@ -555,23 +1068,57 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
   if (g.rows > 0) {
     const unsigned blocks = (unsigned)((g.rows + bwd::WAVES - 1) / bwd::WAVES);
     const dim3 grid(blocks), block(64 * bwd::WAVES);
-    if (g.ps <= 7 && g.Ch <= 64) {
+    if (binned) {
+      const unsigned pix = (unsigned)((g.B * g.T * g.HW + 3) / 4);
+      hipLaunchKernelGGL(scale_by_cover_kernel, dim3(pix), dim3(256), 0, s, gocl, g, g.lo, g.ps);
       switch (g.ps) {
-#define SNLS_BWD_CASE(P)                                                                                        \
-  case P:                                                                                                       \
-    hipLaunchKernelGGL(backward_agg_block_kernel<P>, grid, block, 0, s, vcl, dists, inds, gocl, g, scale, dvcl, \
-                       grad_flows, Gws);                                                                        \
-    hipLaunchKernelGGL(backward_search_block_kernel<P>, grid, block, 0, s, qcl, kcl, dists, inds, grad_dists, g, \
-                       scale, Gws, dqcl, dkcl, grad_flows);                                                     \
+#define SNLS_BWD_ROWS_CASE(P)                                                                                     \
+  case P:                                                                                                         \
+    hipLaunchKernelGGL(backward_agg_block_kernel<P>, grid, block, 0, s, vcl, dists, inds, gocl, g, scale,          \
+                       grad_flows, Gws, wlws);                                                                    \
+    hipLaunchKernelGGL(backward_search_block_kernel<P>, grid, block, 0, s, qcl, kcl, dists, inds, grad_dists, g,   \
+                       scale, Gws, dqcl, grad_flows, ddws);                                                       \
     break;
-        SNLS_BWD_CASE(1)
-        SNLS_BWD_CASE(2)
-        SNLS_BWD_CASE(3)
-        SNLS_BWD_CASE(4)
-        SNLS_BWD_CASE(5)
-        SNLS_BWD_CASE(6)
-        SNLS_BWD_CASE(7)
-#undef SNLS_BWD_CASE
+        SNLS_BWD_ROWS_CASE(1)
+        SNLS_BWD_ROWS_CASE(2)
+        SNLS_BWD_ROWS_CASE(3)
+        SNLS_BWD_ROWS_CASE(4)
+        SNLS_BWD_ROWS_CASE(5)
+        SNLS_BWD_ROWS_CASE(6)
+        SNLS_BWD_ROWS_CASE(7)
+#undef SNLS_BWD_ROWS_CASE
+      }
+      const unsigned sblocks = (unsigned)((pairs + bin::SORT_THREADS - 1) / bin::SORT_THREADS);
+      hipLaunchKernelGGL(bin_count_kernel, dim3(sblocks), dim3(bin::SORT_THREADS), 0, s, dists, inds, ddws, g, nty,
+                         ntx, recs, binfo, counts);
+      hipLaunchKernelGGL(bin_scan_kernel, dim3(1), dim3(1024), 0, s, counts, (int)nbins, offsets);
+      hipLaunchKernelGGL(bin_fill_kernel, dim3(sblocks), dim3(bin::SORT_THREADS), 0, s, binfo, g, ntx, offsets,
+                         cursor, entries);
+      // one wave per (tile, term); the L2 dK pass is a kernel of its own (it
+      // also reads the key block)
+      const bool l2 = g.dist != SNLS_DIST_PROD;
+      const dim3 agrid((unsigned)nbins, l2 ? 1 : 2), ablock(64);
+      switch (g.ps) {
+#define SNLS_BWD_ACC_CASE(P)                                                                                        \
+  case P:                                                                                                           \
+    if (l2) {                                                                                                       \
+      hipLaunchKernelGGL((bin_accumulate_kernel<P, true>), agrid, ablock, 0, s, qcl, kcl, gocl, recs, wlws, offsets, \
+                         entries, g, nty, ntx, 0, dkcl, dvcl);                                                      \
+      hipLaunchKernelGGL((bin_accumulate_kernel<P, false>), agrid, ablock, 0, s, qcl, kcl, gocl, recs, wlws,        \
+                         offsets, entries, g, nty, ntx, 1, dkcl, dvcl);                                             \
+    } else {                                                                                                        \
+      hipLaunchKernelGGL((bin_accumulate_kernel<P, false>), agrid, ablock, 0, s, qcl, kcl, gocl, recs, wlws,        \
+                         offsets, entries, g, nty, ntx, 0, dkcl, dvcl);                                             \
+    }                                                                                                               \
+    break;
+        SNLS_BWD_ACC_CASE(1)
+        SNLS_BWD_ACC_CASE(2)
+        SNLS_BWD_ACC_CASE(3)
+        SNLS_BWD_ACC_CASE(4)
+        SNLS_BWD_ACC_CASE(5)
+        SNLS_BWD_ACC_CASE(6)
+        SNLS_BWD_ACC_CASE(7)
+#undef SNLS_BWD_ACC_CASE
       }
     } else {
       hipLaunchKernelGGL(backward_agg_kernel, grid, block, 0, s, vcl, dists, inds, gocl, g, scale, dvcl, grad_flows,

@@ -114,7 +114,18 @@ def test_aggregate_and_backward_validation(lib):
                               None) == B.SNLS_ERR_WORKSPACE
     need = lib.snls_workspace_size(B.SNLS_OP_BACKWARD, ctypes.byref(prm))
     al = lambda b: (b + 255) // 256 * 256
-    assert need == al(nq * 4 * 4) + 7 * al(1 * 3 * 8 * 16 * 17 * 4)  # G, 4 channels-last inputs, 3 accumulators
+    pairs = nq * 4
+    nbins = 1 * 2 * 3 * 2 * 3  # (B, heads, frames) x 8 x 8 key tiles of a 16 x 17 frame
+    # G, 4 channels-last inputs, 3 accumulators; the binned dK/dV pass adds the
+    # pair scalars, 32-byte pair records, first-tile words, tile counts,
+    # cursors, offsets and up to 4 entries a pair
+    assert need == (al(pairs * 4) + 7 * al(1 * 3 * 8 * 16 * 17 * 4) + 2 * al(pairs * 4) + al(pairs * 32)
+                    + al(pairs * 4) + 2 * al(nbins * 4) + al((nbins + 1) * 4) + al(4 * pairs * 4))
+    # heads wider than 64 channels take the atomic scatter path: no bin section
+    wide = _params(C=130, HD=1)
+    nqw = 1 * 1 * 3 * 16 * 17
+    assert lib.snls_workspace_size(B.SNLS_OP_BACKWARD, ctypes.byref(wide)) == \
+        al(nqw * 4 * 4) + 7 * al(1 * 3 * 130 * 16 * 17 * 4)
     args = [FAKE] * 8
     st = lib.snls_backward(*args, ctypes.byref(prm), 1.0, FAKE, FAKE, FAKE, FAKE, None, 0, None)
     assert st == B.SNLS_ERR_WORKSPACE
