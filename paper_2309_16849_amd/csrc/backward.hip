@@ -542,49 +542,28 @@ __global__ void __launch_bounds__(256) backward_search_block_kernel(const float*
 //
 // The dK and dV terms of one (row, neighbour) pair fall on the (P+1) x (P+1)
 // block of key pixels its taps read.  Instead of adding them to global memory
-// with float atomics, the pairs are sorted by the 8 x 8 key tiles their
-// block touches (a counting sort: counts per tile, exclusive scan, fill), and
-// one workgroup per tile sums the terms of its pairs in LDS and writes the
-// tile once.  The row kernels above provide the per-pair scalars: the softmax
-// weight w_l (dV = w_l g~ through the taps) and dd_l (dK = dd_l q, or
+// with float atomics, the pairs are sorted by the tile of the key frame that
+// holds their block origin (4 x 8 tiles of origins; a counting sort: counts
+// per tile, exclusive scan, fill).  One wave per tile sums the terms of its
+// pairs in a private LDS region -- the tile's pixels plus the P rows above
+// and P columns left of it, so that every block of the tile lies inside --
+// and writes the region to a scratch buffer; a merge pass then adds, for
+// every key pixel, the copies of the (up to 3 x 2) regions that hold it, in
+// a fixed order.  The row kernels above provide the per-pair scalars: the
+// softmax weight w_l (dV = w_l g~ through the taps) and dd_l (dK = dd_l q, or
 // 2 dd_l (k~ - q) for L2, through the taps).
 namespace bin {
-constexpr int TS = 8;            // key tile side (pixels): a tap block (P+1 <= 8) spans at most 2 x 2 tiles
-constexpr int NPIX = TS * TS;
+constexpr int TH = 4, TW = 8;    // tile of block origins (rows, columns)
 constexpr int SORT_THREADS = 256;
 }  // namespace bin
 
-// Tiles [ty0, ty1] x [tx0, tx1] of the key frame that the tap block with
-// origin (Y0, X0) touches inside the frame; false when it misses the frame.
-SNLS_DEV bool block_tiles(int Y0, int X0, int P, const Geo& g, int* ty0, int* ty1, int* tx0, int* tx1) {
-  const int ylo = max(Y0, 0), yhi = min(Y0 + P, g.H - 1);
-  const int xlo = max(X0, 0), xhi = min(X0 + P, g.W - 1);
-  if (ylo > yhi || xlo > xhi) return false;
-  *ty0 = ylo / bin::TS;
-  *ty1 = yhi / bin::TS;
-  *tx0 = xlo / bin::TS;
-  *tx1 = xhi / bin::TS;
-  return true;
-}
-
 // What the tile pass needs of one pair, decoded once: query frame and pixel,
-// tap-block origin and fractions, dd_l.  32 bytes, one scalar load.
+// tap-block origin and fractions, dd_l.
 struct alignas(32) PairRec {
   int t, h, w, Y0, X0;
   float ay, ax, dd;
 };
 constexpr unsigned kNoBin = 0xffffffffu;
-
-// Per pair (one thread each, pair indices below 2^29): decode the row and the
-// neighbour, write its record and its first tile -- bin | (second tile row)
-// << 30 | (second tile column) << 31, kNoBin when the block misses every
-// frame or the pair contributes nothing -- and count its tiles.
-__global__ void __launch_bounds__(bin::SORT_THREADS) bin_count_kernel(const float* __restrict__ dists,
-                                                                      const float* __restrict__ inds,
-                                                                      const float* __restrict__ dd, Geo g, int nty,
-                                                                      int ntx, PairRec* __restrict__ recs,
-                                                                      unsigned* __restrict__ binfo,
-                                                                      unsigned* __restrict__ counts);
 
 // Adds, for every lane with `has`, one to cnt[key] -- one atomic per distinct
 // key of the wave -- and returns the lane's slot: the counter's previous value
@@ -607,19 +586,11 @@ SNLS_DEV unsigned wave_count_add(unsigned* cnt, bool has, unsigned key) {
   return slot;
 }
 
-// The (up to 4) tiles of a pair from its first-tile word.
-SNLS_DEV int expand_bins(unsigned bi, int ntx, unsigned (&bins)[4]) {
-  if (bi == kNoBin) return 0;
-  const unsigned b0 = bi & 0x3fffffffu;
-  const bool dy = (bi >> 30) & 1u, dx = (bi >> 31) & 1u;
-  int n = 0;
-  bins[n++] = b0;
-  if (dx) bins[n++] = b0 + 1;
-  if (dy) bins[n++] = b0 + (unsigned)ntx;
-  if (dy && dx) bins[n++] = b0 + (unsigned)ntx + 1;
-  return n;
-}
-
+// Per pair (one thread each, pair indices below 2^29): decode the row and the
+// neighbour, write its record and its tile (kNoBin when its block misses the
+// frame or the pair contributes nothing) and count it.  Block origins lie in
+// [-P, H-1] x [-P, W-1]: tile (ty, tx) holds the origins with
+// (Y0 + P) / TH == ty and (X0 + P) / TW == tx.
 __global__ void __launch_bounds__(bin::SORT_THREADS) bin_count_kernel(const float* __restrict__ dists,
                                                                       const float* __restrict__ inds,
                                                                       const float* __restrict__ dd, Geo g, int nty,
@@ -645,13 +616,13 @@ __global__ void __launch_bounds__(bin::SORT_THREADS) bin_count_kernel(const floa
     const int hd = (int)(row % (unsigned)g.HD);
     const int b = (int)(row / (unsigned)g.HD);
     const int h = mh * g.s0, w = mw * g.s0;
-    int t2, ny, nx, ty0, ty1, tx0, tx1;
+    int t2, ny, nx;
     float ay, ax;
     if (isfinite(dist) && neighbour(irow, l, g, &t2, &ny, &nx, &ay, &ax)) {
       const int Y0 = h + g.lo + ny, X0 = w + g.lo + nx;
-      if (block_tiles(Y0, X0, g.ps, g, &ty0, &ty1, &tx0, &tx1)) {
-        const unsigned b0 = ((unsigned)(((b * g.HD + hd) * g.T + t2) * nty + ty0)) * (unsigned)ntx + (unsigned)tx0;
-        bi = b0 | ((unsigned)(ty1 > ty0) << 30) | ((unsigned)(tx1 > tx0) << 31);
+      if (Y0 + g.ps >= 0 && Y0 < g.H && X0 + g.ps >= 0 && X0 < g.W) {
+        const int ty = (Y0 + g.ps) / bin::TH, tx = (X0 + g.ps) / bin::TW;
+        bi = ((unsigned)(((b * g.HD + hd) * g.T + t2) * nty + ty)) * (unsigned)ntx + (unsigned)tx;
         PairRec r;
         r.t = t;
         r.h = h;
@@ -666,10 +637,7 @@ __global__ void __launch_bounds__(bin::SORT_THREADS) bin_count_kernel(const floa
     }
     binfo[pair] = bi;
   }
-  unsigned bins[4];
-  const int n = expand_bins(bi, ntx, bins);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) (void)wave_count_add(counts, i < n, i < n ? bins[i] : 0u);
+  (void)wave_count_add(counts, bi != kNoBin, bi != kNoBin ? bi : 0u);
 }
 
 // Exclusive scan of the counts (one workgroup): offsets[i] = sum of counts
@@ -699,34 +667,30 @@ __global__ void __launch_bounds__(1024) bin_scan_kernel(const unsigned* __restri
 }
 
 __global__ void __launch_bounds__(bin::SORT_THREADS) bin_fill_kernel(const unsigned* __restrict__ binfo, Geo g,
-                                                                     int ntx, const unsigned* __restrict__ offsets,
+                                                                     const unsigned* __restrict__ offsets,
                                                                      unsigned* __restrict__ cursor,
                                                                      unsigned* __restrict__ entries) {
   const unsigned pair = blockIdx.x * bin::SORT_THREADS + threadIdx.x;
   const unsigned bi = pair < (unsigned)(g.rows * g.k) ? binfo[pair] : kNoBin;
-  unsigned bins[4];
-  const int n = expand_bins(bi, ntx, bins);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const unsigned slot = wave_count_add(cursor, i < n, i < n ? bins[i] : 0u);
-    if (i < n) entries[offsets[bins[i]] + slot] = pair;
-  }
+  const bool has = bi != kNoBin;
+  const unsigned slot = wave_count_add(cursor, has, has ? bi : 0u);
+  if (has) entries[offsets[bi] + slot] = pair;
 }
 
-// One wave per (key tile, term): blockIdx.y + term0 = 0 sums dK, 1 sums dV.  The
-// wave owns its 8 x 8 x 64 tile in LDS, so every addition is a plain
-// read-add-write (float atomics in LDS are far slower here), in the order of
-// the tile's entry list; lanes are the head's channels.  Entries go in
-// batches of 64: lane i decodes entry i of the batch (read offsets of its
-// patch rows and columns, LDS rows and columns of its tap block, its tap
-// weights times its scalar), and the wave then takes the
-// entries from the lanes one at a time, two per step, the reads of a step
-// issued a few steps before its additions.
-// Reads are 32-bit buffer loads whose offset is pushed past the buffer
-// (reads 0) for pixels outside the frame.  The tile is written to the
-// channels-last accumulator (every pixel of every tile, so the accumulator
-// needs no clearing).  gs is grad_out already divided by the cover count of
-// its pixel.
+// One wave per (tile, term): blockIdx.y + term0 = 0 sums dK, 1 sums dV.  The
+// wave owns its region -- key rows [TH ty - P, TH ty + TH), columns
+// [TW tx - P, TW tx + TW) -- in LDS, so every addition is a plain
+// read-add-write (float atomics in LDS are far slower here) at a fixed
+// offset from the block origin, in the order of the tile's entry list; lanes
+// are the head's channels.  Entries go in batches of 64: lane i decodes
+// entry i of the batch (read offsets of its patch rows and columns, LDS index
+// of its block origin, its tap weights times its scalar), and the wave then
+// takes the entries from the lanes one at a time, two per step, the reads of
+// a step issued a step before its additions.  Reads are 32-bit buffer loads
+// whose offset is pushed past the buffer (reads 0) for pixels outside the
+// frame.  The region goes to scratch (all of it, every tile: the merge reads
+// no stale value).  gs is grad_out already divided by the cover count of its
+// pixel.
 template <int P, bool L2K>
 __global__ void __launch_bounds__(64) bin_accumulate_kernel(const float* __restrict__ qcl,
                                                             const float* __restrict__ kcl,
@@ -735,97 +699,66 @@ __global__ void __launch_bounds__(64) bin_accumulate_kernel(const float* __restr
                                                             const float* __restrict__ wl,
                                                             const unsigned* __restrict__ offsets,
                                                             const unsigned* __restrict__ entries, Geo g, int nty,
-                                                            int ntx, int term0, float* __restrict__ dkcl,
-                                                            float* __restrict__ dvcl) {
+                                                            int ntx, int term0, float* __restrict__ scratch) {
   using namespace bin;
   constexpr int PB = P + 1;
   constexpr int lo = -(P / 2);
-  constexpr unsigned OOB = 1u << 30;  // tensors are below 2^30 bytes: OOB + any in-frame offset reads 0
-  // 9 x 9 pixels: the 8 x 8 tile plus a spare row and column that take the
-  // block pixels outside the tile (written, never read back)
-  constexpr int LP = TS + 1;
-  __shared__ float acc[LP * LP * 64];
+  constexpr int RH = TH + P, RW = TW + P, RPIX = RH * RW;
+  __shared__ float acc[RPIX * 64];
   const int lane = threadIdx.x;
-  const bool is_v = (int)blockIdx.y + term0 == 1;
-  // Tile order: consecutive workgroups land on different XCDs (8 per
-  // device), so XCD x takes a contiguous run of a list in which the tile
-  // rows are cut into 8 bands and each band lists its rows of every frame:
-  // tiles that read the same query patches share an L2, and every XCD gets
-  // the same share of every frame.
-  int f, ty, tx;
-  {
-    const int nwg = (int)gridDim.x, nfr = nwg / (nty * ntx);
-    const int xcd = (int)blockIdx.x % 8, xq = nwg / 8, xrem = nwg % 8;
-    int j = xcd * xq + min(xcd, xrem) + (int)blockIdx.x / 8;  // position in the band-major list
-    int band = 0, r0 = 0, r1 = (nty + 7) / 8;
-    while (j >= nfr * (r1 - r0) * ntx) {  // bands of rows [ceil(i nty / 8), ceil((i+1) nty / 8))
-      j -= nfr * (r1 - r0) * ntx;
-      ++band;
-      r0 = r1;
-      r1 = ((band + 1) * nty + 7) / 8;
-    }
-    const int per = (r1 - r0) * ntx;
-    f = j / per;
-    ty = r0 + (j % per) / ntx;
-    tx = j % ntx;
-  }
-  const int bn = (f * nty + ty) * ntx + tx;
+  const int term = (int)blockIdx.y + term0;
+  const bool is_v = term == 1;
+  const int nbins = (int)gridDim.x;
+  const int bn = (int)blockIdx.x;
+  const int tx = bn % ntx, ty = (bn / ntx) % nty;
+  const int f = bn / (ntx * nty);
   const int t2 = f % g.T, hd = (f / g.T) % g.HD, b = f / (g.T * g.HD);
-  const int ty0 = ty * TS, tx0 = tx * TS;
+  const int ry0 = ty * TH - P, rx0 = tx * TW - P;  // region origin
   const int ch = hd * g.Ch + (lane < g.Ch ? lane : 0);  // a channel of the head for every lane
   const unsigned ch4 = (unsigned)ch * 4u;
   constexpr bool l2k = L2K;  // the dK pass of the L2 distance (reads the key block too)
   const int H = g.H, W = g.W;
-  const unsigned rowb = (unsigned)(W * g.C) * 4u, colb = (unsigned)g.C * 4u;  // bytes per row / pixel
-  const unsigned tbytes = (unsigned)((long long)g.B * g.T * g.HW * g.C * 4);
-  const __amdgpu_buffer_rsrc_t src_rs =
-      __builtin_amdgcn_make_buffer_rsrc((void*)(is_v ? gs : qcl), (short)0, (int)tbytes, 0x00020000);
-  const __amdgpu_buffer_rsrc_t k_rs = __builtin_amdgcn_make_buffer_rsrc((void*)kcl, (short)0, (int)tbytes, 0x00020000);
-  const unsigned kframe = (unsigned)((b * g.T + t2) * H) * rowb;  // byte offset of key frame (b, t2)
+  const ClView sv = cl_view(is_v ? gs : qcl, g), kv = cl_view(kcl, g);
+  const unsigned kframe = (unsigned)((b * g.T + t2) * H) * kv.rowb;  // byte offset of key frame (b, t2)
 #pragma unroll
-  for (int i = 0; i < LP * LP; ++i) acc[i * 64 + lane] = 0.f;
+  for (int i = 0; i < RPIX; ++i) acc[i * 64 + lane] = 0.f;
 
   // What the wave needs of one entry (per lane: the entry of that lane).
   struct Ent {
-    unsigned ro[P], co[P];     // byte offsets of the patch rows / columns (OOB outside the frame)
+    unsigned ro[P], co[P];     // byte offsets of the patch rows / columns (kOOB outside the frame)
     unsigned kr[PB], kc[PB];   // the same for the key block (L2 only)
-    int lr[PB], lc[PB];        // LDS index of each block row / column (spare row / column outside the tile)
     int pin;                   // patch rows | columns << 8 inside the frame (L2 only)
+    int base;                  // LDS index of the block origin
     float w00, w01, w10, w11;  // tap weights (times the scalar unless L2)
     float sc;                  // the scalar (0: nothing to add)
   };
   auto decode = [&](const PairRec& r, float s) {
     Ent en;
-    const unsigned qrow0 = (unsigned)((b * g.T + r.t) * H) * rowb;
+    const unsigned qrow0 = (unsigned)((b * g.T + r.t) * H) * sv.rowb;
     int pr = 0, pc = 0;
 #pragma unroll
     for (int i = 0; i < P; ++i) {
       const int y = r.h + lo + i, x = r.w + lo + i;
       const bool yin = y >= 0 && y < H, xin = x >= 0 && x < W;
-      en.ro[i] = yin ? qrow0 + (unsigned)y * rowb : OOB;
-      en.co[i] = xin ? (unsigned)x * colb : OOB;
+      en.ro[i] = yin ? qrow0 + (unsigned)y * sv.rowb : kOOB;
+      en.co[i] = xin ? (unsigned)x * sv.colb : kOOB;
       pr |= (int)yin << i;
       pc |= (int)xin << i;
     }
     en.pin = pr | (pc << 8);
-    bool anyr = false, anyc = false;
 #pragma unroll
     for (int i = 0; i < PB; ++i) {
       const int Y = r.Y0 + i, X = r.X0 + i;
-      en.kr[i] = Y >= 0 && Y < H ? kframe + (unsigned)Y * rowb : OOB;
-      en.kc[i] = X >= 0 && X < W ? (unsigned)X * colb : OOB;
-      const bool rin = Y >= ty0 && Y < ty0 + TS, cin = X >= tx0 && X < tx0 + TS;
-      en.lr[i] = (rin ? Y - ty0 : TS) * LP * 64;
-      en.lc[i] = (cin ? X - tx0 : TS) * 64;
-      anyr |= rin;
-      anyc |= cin;
+      en.kr[i] = Y >= 0 && Y < H ? kframe + (unsigned)Y * kv.rowb : kOOB;
+      en.kc[i] = X >= 0 && X < W ? (unsigned)X * kv.colb : kOOB;
     }
+    en.base = ((r.Y0 - ry0) * RW + (r.X0 - rx0)) * 64;
     const float m = l2k ? 1.f : s;
     en.w00 = (1.f - r.ay) * (1.f - r.ax) * m;
     en.w01 = (1.f - r.ay) * r.ax * m;
     en.w10 = r.ay * (1.f - r.ax) * m;
     en.w11 = r.ay * r.ax * m;
-    en.sc = (anyr && anyc) ? s : 0.f;
+    en.sc = s;
     return en;
   };
   // entry i of the batch, from lane i
@@ -846,11 +779,7 @@ __global__ void __launch_bounds__(64) bin_accumulate_kernel(const float* __restr
       }
       en.pin = (int)rd((unsigned)v.pin);
     }
-#pragma unroll
-    for (int j = 0; j < PB; ++j) {
-      en.lr[j] = (int)rd((unsigned)v.lr[j]);
-      en.lc[j] = (int)rd((unsigned)v.lc[j]);
-    }
+    en.base = (int)rd((unsigned)v.base) + lane;
     en.w00 = rdf(v.w00);
     en.w01 = rdf(v.w01);
     en.w10 = rdf(v.w10);
@@ -863,43 +792,36 @@ __global__ void __launch_bounds__(64) bin_accumulate_kernel(const float* __restr
 #pragma unroll
     for (int ph = 0; ph < P; ++ph)
 #pragma unroll
-      for (int pw = 0; pw < P; ++pw)
-        tp[ph * P + pw] = __builtin_bit_cast(
-            float, __builtin_amdgcn_raw_buffer_load_b32(src_rs, en.ro[ph] + en.co[pw] + ch4, 0, 0));
+      for (int pw = 0; pw < P; ++pw) tp[ph * P + pw] = sv.ld(en.ro[ph] + en.co[pw] + ch4);
     if (l2k) {
 #pragma unroll
       for (int a = 0; a < PB; ++a)
 #pragma unroll
-        for (int c = 0; c < PB; ++c)
-          kb[a * PB + c] =
-              __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(k_rs, en.kr[a] + en.kc[c] + ch4, 0, 0));
+        for (int c = 0; c < PB; ++c) kb[a * PB + c] = kv.ld(en.kr[a] + en.kc[c] + ch4);
     }
   };
-  // term of each patch pixel, spread through the taps into the tile:
+  // term of each patch pixel, spread through the taps into the region:
   // block pixel (a, c) collects w00, w01, w10, w11 of patch pixels (a, c),
   // (a, c-1), (a-1, c), (a-1, c-1)
   auto spread = [&](const Ent& en, float (&tp)[P * P], const float (&kb)[PB * PB]) {
     if (l2k) {
       // dK of patch pixel p: 2 dd (k~ - q); patch pixels outside the frame
       // add nothing (their q and taps read 0, but the k~ term would not vanish)
-      const float u00 = en.w00, u01 = en.w01, u10 = en.w10, u11 = en.w11;
 #pragma unroll
       for (int ph = 0; ph < P; ++ph)
 #pragma unroll
         for (int pw = 0; pw < P; ++pw) {
-          const float kv = u00 * kb[ph * PB + pw] + u01 * kb[ph * PB + pw + 1] + u10 * kb[(ph + 1) * PB + pw] +
-                           u11 * kb[(ph + 1) * PB + pw + 1];
+          const float kvv = en.w00 * kb[ph * PB + pw] + en.w01 * kb[ph * PB + pw + 1] +
+                            en.w10 * kb[(ph + 1) * PB + pw] + en.w11 * kb[(ph + 1) * PB + pw + 1];
           const bool in = ((en.pin >> ph) & (en.pin >> (8 + pw)) & 1) != 0;
-          tp[ph * P + pw] = in ? -(2.f * en.sc * (tp[ph * P + pw] - kv)) : 0.f;
+          tp[ph * P + pw] = in ? -(2.f * en.sc * (tp[ph * P + pw] - kvv)) : 0.f;
         }
     }
-    // no branches: every block pixel reads and writes (outside the tile the
-    // spare row / column), so the reads of the block go out together
     float cur[PB * PB];
 #pragma unroll
     for (int a = 0; a < PB; ++a)
 #pragma unroll
-      for (int c = 0; c < PB; ++c) cur[a * PB + c] = acc[en.lr[a] + en.lc[c] + lane];
+      for (int c = 0; c < PB; ++c) cur[a * PB + c] = acc[en.base + (a * RW + c) * 64];
 #pragma unroll
     for (int a = 0; a < PB; ++a)
 #pragma unroll
@@ -909,7 +831,7 @@ __global__ void __launch_bounds__(64) bin_accumulate_kernel(const float* __restr
         if (a > 0 && c < P) v = fmaf(en.w10, tp[(a - 1) * P + c], v);
         if (a < P && c > 0) v = fmaf(en.w01, tp[a * P + c - 1], v);
         if (a < P && c < P) v = fmaf(en.w00, tp[a * P + c], v);
-        acc[en.lr[a] + en.lc[c] + lane] = v;
+        acc[en.base + (a * RW + c) * 64] = v;
       }
   };
 
@@ -950,13 +872,39 @@ __global__ void __launch_bounds__(64) bin_accumulate_kernel(const float* __restr
       }
     }
   }
-  float* dst = (is_v ? dvcl : dkcl) + ((long long)b * g.T + t2) * g.HW * g.C + ch;
-  const bool act = lane < g.Ch;
+  float* dst = scratch + ((long long)term * nbins + bn) * (RPIX * 64) + lane;
 #pragma unroll
-  for (int px = 0; px < NPIX; ++px) {
-    const int Y = ty0 + px / TS, X = tx0 + px % TS;
-    if (act && Y < H && X < W) dst[((long long)Y * W + X) * g.C] = acc[((px / TS) * LP + px % TS) * 64 + lane];
-  }
+  for (int px = 0; px < RPIX; ++px) dst[px * 64] = acc[px * 64 + lane];
+}
+
+// Key pixel (Y, X) of frame (b, hd, t2) sums the copies of the regions of
+// tiles ty in [Y / TH, (Y + P) / TH], tx in [X / TW, (X + P) / TW] (those
+// that exist), in that order, into the channels-last accumulator.  One wave
+// per pixel, lanes over the head's channels; blockIdx.y + term0 picks dK / dV.
+__global__ void __launch_bounds__(256) bin_merge_kernel(const float* __restrict__ scratch, Geo g, int nty, int ntx,
+                                                        int term0, float* __restrict__ dkcl,
+                                                        float* __restrict__ dvcl) {
+  using namespace bin;
+  const long long pid = (long long)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const long long npix = (long long)g.B * g.HD * g.T * g.HW;
+  if (pid >= npix) return;  // whole wave
+  const int lane = threadIdx.x & 63;
+  const int term = (int)blockIdx.y + term0;
+  const int P = g.ps, RH = TH + P, RW = TW + P;
+  const long long nbins = (long long)g.B * g.HD * g.T * nty * ntx;
+  const int X = (int)(pid % g.W), Y = (int)((pid / g.W) % g.H);
+  const int f = (int)(pid / g.HW);
+  const int t2 = f % g.T, hd = (f / g.T) % g.HD, b = f / (g.T * g.HD);
+  float v = 0.f;
+  const int ty1 = min((Y + P) / TH, nty - 1), tx1 = min((X + P) / TW, ntx - 1);
+  for (int ty = Y / TH; ty <= ty1; ++ty)
+    for (int tx = X / TW; tx <= tx1; ++tx) {
+      const long long bn = ((long long)f * nty + ty) * ntx + tx;
+      const int px = (Y - (ty * TH - P)) * RW + (X - (tx * TW - P));
+      v += scratch[((term * nbins + bn) * (RH * RW) + px) * 64 + lane];
+    }
+  if (lane < g.Ch)
+    (term == 1 ? dvcl : dkcl)[(((long long)b * g.T + t2) * g.HW + (long long)Y * g.W + X) * g.C + hd * g.Ch + lane] = v;
 }
 
 // grad_out (channels-last) divided in place by the number of query patches
@@ -972,24 +920,29 @@ __global__ void __launch_bounds__(256) scale_by_cover_kernel(float* __restrict__
   for (int c = threadIdx.x & 63; c < g.C; c += 64) row[c] = row[c] * inv;
 }
 
-// The binned path: P <= 7, at most 64 channels per head, bin entries (up
-// to 4 per pair) counted in 31 bits, videos below 2^30 bytes.
+// Tiles of block origins per frame: origins lie in [-P, H-1] x [-P, W-1].
+static int bin_nty(const Geo& g) { return (g.H - 1 + g.ps) / bin::TH + 1; }
+static int bin_ntx(const Geo& g) { return (g.W - 1 + g.ps) / bin::TW + 1; }
+static long long bin_count(const Geo& g) { return (long long)g.B * g.HD * g.T * bin_nty(g) * bin_ntx(g); }
+// floats of the scratch regions of both terms
+static long long bin_scratch_floats(const Geo& g) {
+  return 2 * bin_count(g) * (bin::TH + g.ps) * (bin::TW + g.ps) * 64;
+}
+
+// The binned path: P <= 7, at most 64 channels per head, pair indices in 29
+// bits, videos below 2^30 bytes (32-bit buffer offsets).
 static bool bin_supported(const Geo& g) {
   if (g.ps > 7 || g.Ch > 64) return false;
   if (g.rows * (long long)g.k >= (1LL << 29)) return false;
-  if ((long long)g.B * g.T * g.HW * g.C * 4 >= (1LL << 30)) return false;  // 32-bit buffer offsets
-  const long long nbins = (long long)g.B * g.HD * g.T * ((g.H + bin::TS - 1) / bin::TS) * ((g.W + bin::TS - 1) / bin::TS);
-  return nbins < (1LL << 30);
-}
-static long long bin_count(const Geo& g) {
-  return (long long)g.B * g.HD * g.T * ((g.H + bin::TS - 1) / bin::TS) * ((g.W + bin::TS - 1) / bin::TS);
+  if ((long long)g.B * g.T * g.HW * g.C * 4 >= (1LL << 30)) return false;
+  return bin_count(g) < (1LL << 30);
 }
 
 // Workspace: G (rows x k), channels-last copies of q, k, v and grad_out, and
 // channels-last accumulators of dq, dk and dv (256-byte aligned pieces); on
 // the binned path also the pair scalars dd and w (rows x k each), the pair
-// records and first-tile words, the tile counts, cursors and offsets, and the
-// sorted entries (up to 4 per pair).
+// records and tiles, the tile counts, cursors and offsets, the sorted
+// entries (one per pair) and the scratch regions of both terms.
 static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 size_t backward_ws_bytes(const Geo& g) {
@@ -1000,7 +953,7 @@ size_t backward_ws_bytes(const Geo& g) {
     const size_t nb = (size_t)bin_count(g);
     b += 2 * align256(pairs * sizeof(float)) + align256(pairs * sizeof(PairRec)) + align256(pairs * sizeof(unsigned)) +
          2 * align256(nb * sizeof(unsigned)) + align256((nb + 1) * sizeof(unsigned)) +
-         align256(4 * pairs * sizeof(unsigned));
+         align256(pairs * sizeof(unsigned)) + align256((size_t)bin_scratch_floats(g) * sizeof(float));
   }
   return b;
 }
@@ -1033,11 +986,12 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
   float* dvcl = reinterpret_cast<float*>(base + 6 * vb);
   base += 7 * vb;
   const bool binned = bin_supported(g) && g.rows > 0;
-  const int nty = (g.H + bin::TS - 1) / bin::TS, ntx = (g.W + bin::TS - 1) / bin::TS;
+  const int nty = bin_nty(g), ntx = bin_ntx(g);
   const long long nbins = bin_count(g);
   float *ddws = nullptr, *wlws = nullptr;
   PairRec* recs = nullptr;
   unsigned *binfo = nullptr, *counts = nullptr, *cursor = nullptr, *offsets = nullptr, *entries = nullptr;
+  float* scratch = nullptr;
   if (binned) {
     const size_t nbb = align256((size_t)nbins * sizeof(unsigned));
     ddws = reinterpret_cast<float*>(base);
@@ -1051,7 +1005,10 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
     counts = reinterpret_cast<unsigned*>(base);
     cursor = reinterpret_cast<unsigned*>(base + nbb);
     offsets = reinterpret_cast<unsigned*>(base + 2 * nbb);
-    entries = reinterpret_cast<unsigned*>(base + 2 * nbb + align256((size_t)(nbins + 1) * sizeof(unsigned)));
+    base += 2 * nbb + align256((size_t)(nbins + 1) * sizeof(unsigned));
+    entries = reinterpret_cast<unsigned*>(base);
+    base += align256((size_t)pairs * sizeof(unsigned));
+    scratch = reinterpret_cast<float*>(base);
     zero(reinterpret_cast<float*>(counts), 2 * (long long)(nbb / sizeof(unsigned)), s);  // counts and cursors
   } else {
     zero(dkcl, nvid, s);
@@ -1092,8 +1049,8 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
       hipLaunchKernelGGL(bin_count_kernel, dim3(sblocks), dim3(bin::SORT_THREADS), 0, s, dists, inds, ddws, g, nty,
                          ntx, recs, binfo, counts);
       hipLaunchKernelGGL(bin_scan_kernel, dim3(1), dim3(1024), 0, s, counts, (int)nbins, offsets);
-      hipLaunchKernelGGL(bin_fill_kernel, dim3(sblocks), dim3(bin::SORT_THREADS), 0, s, binfo, g, ntx, offsets,
-                         cursor, entries);
+      hipLaunchKernelGGL(bin_fill_kernel, dim3(sblocks), dim3(bin::SORT_THREADS), 0, s, binfo, g, offsets, cursor,
+                         entries);
       // one wave per (tile, term); the L2 dK pass is a kernel of its own (it
       // also reads the key block)
       const bool l2 = g.dist != SNLS_DIST_PROD;
@@ -1103,12 +1060,12 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
   case P:                                                                                                           \
     if (l2) {                                                                                                       \
       hipLaunchKernelGGL((bin_accumulate_kernel<P, true>), agrid, ablock, 0, s, qcl, kcl, gocl, recs, wlws, offsets, \
-                         entries, g, nty, ntx, 0, dkcl, dvcl);                                                      \
+                         entries, g, nty, ntx, 0, scratch);                                                         \
       hipLaunchKernelGGL((bin_accumulate_kernel<P, false>), agrid, ablock, 0, s, qcl, kcl, gocl, recs, wlws,        \
-                         offsets, entries, g, nty, ntx, 1, dkcl, dvcl);                                             \
+                         offsets, entries, g, nty, ntx, 1, scratch);                                                \
     } else {                                                                                                        \
       hipLaunchKernelGGL((bin_accumulate_kernel<P, false>), agrid, ablock, 0, s, qcl, kcl, gocl, recs, wlws,        \
-                         offsets, entries, g, nty, ntx, 0, dkcl, dvcl);                                             \
+                         offsets, entries, g, nty, ntx, 0, scratch);                                                \
     }                                                                                                               \
     break;
         SNLS_BWD_ACC_CASE(1)
@@ -1120,6 +1077,9 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
         SNLS_BWD_ACC_CASE(7)
 #undef SNLS_BWD_ACC_CASE
       }
+      const long long npix = (long long)g.B * g.HD * g.T * g.HW;
+      hipLaunchKernelGGL(bin_merge_kernel, dim3((unsigned)((npix + 3) / 4), 2), dim3(256), 0, s, scratch, g, nty, ntx,
+                         0, dkcl, dvcl);
     } else {
       hipLaunchKernelGGL(backward_agg_kernel, grid, block, 0, s, vcl, dists, inds, gocl, g, scale, dvcl, grad_flows,
                          Gws);

@@ -115,12 +115,14 @@ def test_aggregate_and_backward_validation(lib):
     need = lib.snls_workspace_size(B.SNLS_OP_BACKWARD, ctypes.byref(prm))
     al = lambda b: (b + 255) // 256 * 256
     pairs = nq * 4
-    nbins = 1 * 2 * 3 * 2 * 3  # (B, heads, frames) x 8 x 8 key tiles of a 16 x 17 frame
+    # tiles of 4 x 8 block origins, origins in [-P, H-1] x [-P, W-1]: 5 x 3 per (B, head, frame)
+    nbins = 1 * 2 * 3 * ((16 - 1 + 3) // 4 + 1) * ((17 - 1 + 3) // 8 + 1)
     # G, 4 channels-last inputs, 3 accumulators; the binned dK/dV pass adds the
-    # pair scalars, 32-byte pair records, first-tile words, tile counts,
-    # cursors, offsets and up to 4 entries a pair
+    # pair scalars, 32-byte pair records, pair tiles, tile counts, cursors,
+    # offsets, one entry a pair and the (4+P) x (8+P) x 64 regions of both terms
     assert need == (al(pairs * 4) + 7 * al(1 * 3 * 8 * 16 * 17 * 4) + 2 * al(pairs * 4) + al(pairs * 32)
-                    + al(pairs * 4) + 2 * al(nbins * 4) + al((nbins + 1) * 4) + al(4 * pairs * 4))
+                    + al(pairs * 4) + 2 * al(nbins * 4) + al((nbins + 1) * 4) + al(pairs * 4)
+                    + al(2 * nbins * 7 * 11 * 64 * 4))
     # heads wider than 64 channels take the atomic scatter path: no bin section
     wide = _params(C=130, HD=1)
     nqw = 1 * 1 * 3 * 16 * 17
