@@ -684,7 +684,13 @@ __global__ void __launch_bounds__(256) aggregate_p1_kernel(const float* __restri
   float* wl_s = lds_p1;              // scores, then weights (0: neighbour skipped)
   float* ind_s = lds_p1 + NQ * KP;   // (frame, disp_h, disp_w) per neighbour
   const int tid = threadIdx.x;
-  const long long row0 = (long long)blockIdx.x * NQ;
+  // Consecutive workgroups land on different XCDs (8 per device): give each
+  // XCD a contiguous run of query rows, whose neighbours' taps overlap in
+  // its L2.
+  const long long nwg = (long long)gridDim.x;
+  const long long xcd = blockIdx.x % 8, xq = nwg / 8, xrem = nwg % 8;
+  const long long wg = xcd * xq + (xcd < xrem ? xcd : xrem) + blockIdx.x / 8;
+  const long long row0 = wg * NQ;
   const int nq = (int)min((long long)NQ, g.rows - row0);
   for (int e = tid; e < nq * k; e += 256) wl_s[(e / k) * KP + e % k] = dists[row0 * k + e];
   for (int e = tid; e < nq * 3 * k; e += 256) ind_s[e] = inds[row0 * 3 * k + e];

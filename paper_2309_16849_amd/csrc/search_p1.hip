@@ -506,7 +506,12 @@ __global__ void __launch_bounds__(p1::NT) search_p1_topk_kernel(const float* __r
   const int tid = threadIdx.x, j = tid / NR, dh = tid % NR;
   const int img = (int)blockIdx.y;  // (b, hd, t)
   const int t = img % g.T, hd = (img / g.T) % g.HD, b = img / (g.T * g.HD);
-  const int ty = (int)blockIdx.x / tiles_x, tx = (int)blockIdx.x % tiles_x;
+  // Consecutive workgroups land on different XCDs (8 per device): give each
+  // XCD a contiguous run of tiles, whose key regions overlap in its L2.
+  const int ntile = (int)gridDim.x;
+  const int xcd = (int)blockIdx.x % 8, xq = ntile / 8, xrem = ntile % 8;
+  const int tile = xcd * xq + min(xcd, xrem) + (int)blockIdx.x / 8;
+  const int ty = tile / tiles_x, tx = tile % tiles_x;
   const int mh = ty * TQ + j / TQ, mw = tx * TQ + j % TQ;
   const bool inside = mh < g.nH && mw < g.nW;  // the same for the query's 16 lanes
   const int gb = (tid & 63) & ~15;             // the group's first lane in the wave
