@@ -181,7 +181,12 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
                               const float* __restrict__ flows, const Geo& g, int b, int hd, int t, int dt, int ty,
                               int tx, float (&sc)[p1::WSM]) {
   using namespace p1;
-  const int tid = threadIdx.x, j = tid / NR, dh = tid % NR;
+  // The thread index is made opaque here so that what derives from it is
+  // recomputed per frame rather than hoisted out of a caller's frame loop
+  // and kept live (spilled) across the selection.
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  const int j = tid / NR, dh = tid % NR;
   const int t2 = t + dt;
   const int mh = ty * TQ + j / TQ, mw = tx * TQ + j % TQ;  // query-grid position
   const bool inside = mh < g.nH && mw < g.nW;
