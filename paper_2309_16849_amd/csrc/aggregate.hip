@@ -738,8 +738,9 @@ __global__ void __launch_bounds__(256) aggregate_p1_kernel(const float* __restri
     for (int l = 0; l < k; ++l) {
       const float wl = wrow[l];
       const bool use = wl != 0.f;
-      const float tf = use ? ind[3 * l] : 0.f;
-      const float dh = use ? ind[3 * l + 1] : 0.f, dw = use ? ind[3 * l + 2] : 0.f;
+      const float tf0 = ind[3 * l], dh0 = ind[3 * l + 1], dw0 = ind[3 * l + 2];
+      const float tf = use ? tf0 : 0.f;
+      const float dh = use ? dh0 : 0.f, dw = use ? dw0 : 0.f;
       int ny, nx;
       float ay, ax;
       split_disp(dh, &ny, &ay);
@@ -750,11 +751,18 @@ __global__ void __launch_bounds__(256) aggregate_p1_kernel(const float* __restri
       const bool x0in = x0 >= 0 && x0 < g.W, x1in = x0 + 1 >= 0 && x0 + 1 < g.W;
       const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
       const long long o = ((long long)y0 * g.W + x0) * g.Ch;
-      const float4 v00 = (y0in && x0in) ? *reinterpret_cast<const float4*>(vb + o) : zero;
-      const float4 v01 = (y0in && x1in) ? *reinterpret_cast<const float4*>(vb + o + g.Ch) : zero;
-      const float4 v10 = (y1in && x0in) ? *reinterpret_cast<const float4*>(vb + o + (long long)g.W * g.Ch) : zero;
-      const float4 v11 =
-          (y1in && x1in) ? *reinterpret_cast<const float4*>(vb + o + (long long)(g.W + 1) * g.Ch) : zero;
+      // unconditional 16-byte reads (taps outside the frame read the head
+      // plane's first record and are replaced by 0), so the compiler issues
+      // four vector loads per neighbour instead of branching per component
+      typedef float f32x4 __attribute__((ext_vector_type(4)));
+      auto tap4 = [&](bool ok, long long off) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(ok ? vb + off : vh);
+        return ok ? make_float4(v.x, v.y, v.z, v.w) : zero;
+      };
+      const float4 v00 = tap4(y0in && x0in, o);
+      const float4 v01 = tap4(y0in && x1in, o + g.Ch);
+      const float4 v10 = tap4(y1in && x0in, o + (long long)g.W * g.Ch);
+      const float4 v11 = tap4(y1in && x1in, o + (long long)(g.W + 1) * g.Ch);
       auto tap = [&](float a00, float a01, float a10, float a11) {
         const float top = (1.f - ax) * a00 + ax * a01;
         const float bot = (1.f - ax) * a10 + ax * a11;
