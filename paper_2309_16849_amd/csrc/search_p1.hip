@@ -124,8 +124,11 @@ SNLS_DEV void bitonic_stage(unsigned long long& x0, unsigned long long& x1, int 
   }
 }
 
-// Sort the group's 32 entries in descending order.
+// Sort the group's 32 entries in descending order.  The lane index is made
+// opaque so that each stage forms its direction flags from it instead of a
+// caller's loop keeping every stage's lane masks live.
 SNLS_DEV void bitonic_sort32(unsigned long long& x0, unsigned long long& x1, int l) {
+  asm volatile("" : "+v"(l));
   bitonic_stage<2, 1>(x0, x1, l);
   bitonic_stage<4, 2>(x0, x1, l);
   bitonic_stage<4, 1>(x0, x1, l);
@@ -148,6 +151,7 @@ SNLS_DEV void bitonic_sort32(unsigned long long& x0, unsigned long long& x1, int
 // a bitonic sequence, then a bitonic merge.
 SNLS_DEV void merge_top32(unsigned long long& a0, unsigned long long& a1, unsigned long long s0,
                           unsigned long long s1, int l) {
+  asm volatile("" : "+v"(l));  // as in bitonic_sort32
   // s[31 - e] for e = 2l is s1 of lane 15 - l, for e = 2l + 1 it is s0
   const unsigned long long r0 = grp_xor64<15>(s1), r1 = grp_xor64<15>(s0);
   a0 = a0 > r0 ? a0 : r0;
@@ -159,7 +163,35 @@ SNLS_DEV void merge_top32(unsigned long long& a0, unsigned long long& a1, unsign
   bitonic_stage<64, 1>(a0, a1, l);
 }
 
+// Bit d_w set where pred(d_w) holds, for the WSM columns of a window row;
+// built by shifts, so no per-column constants are held in registers.
+template <class Pred>
+SNLS_DEV unsigned col_mask(Pred pred) {
+  unsigned m = 0;
+#pragma unroll
+  for (int dw = p1::WSM - 1; dw >= 0; --dw) m = (m << 1) | (pred(dw) ? 1u : 0u);
+  return m;
+}
+
 // ---- scores of one frame ----
+
+// Score of a cell that does not exist (d_w >= ws, a thread with d_h >= ws, a
+// query outside the grid): the NaN whose order key is 0, so that comparisons
+// and order keys drop it without per-column masks.
+SNLS_DEV float no_cell() { return __uint_as_float(0xffffffffu); }
+
+// Number of real cells in the calling thread's window row: ws, or 0 for
+// threads with d_h >= ws and queries outside the grid.  The thread index is
+// opaque, so the per-column compares against it stay inside a caller's frame
+// loop instead of being hoisted as live lane masks.
+SNLS_DEV int p1_row_cells(const Geo& g, int ty, int tx) {
+  using namespace p1;
+  int tid = threadIdx.x, ws = g.ws;
+  asm volatile("" : "+v"(tid), "+s"(ws));
+  const int j = tid / NR, dh = tid % NR;
+  const int mh = ty * TQ + j / TQ, mw = tx * TQ + j % TQ;
+  return (mh < g.nH && mw < g.nW && dh < ws) ? ws : 0;
+}
 
 struct P1Smem {
   // key region chunks (double buffer), pixel-major with the chunk's CC
@@ -173,8 +205,9 @@ struct P1Smem {
 
 // Scores of the window row of thread (j = tid / 16, d_h = tid % 16) for frame
 // step dt of query tile (ty, tx) of image (b, hd, t): sc[d_w] for d_w < ws,
-// -inf for invalid cells and NaN similarities; threads with d_h >= ws (and
-// queries outside the grid) get none.  Workgroup barriers inside: every
+// -inf for invalid cells and NaN similarities, no_cell() where there is no
+// cell (d_w >= ws; every d_w of threads with d_h >= ws and of queries outside
+// the grid).  Workgroup barriers inside: every
 // thread calls it; its staging buffers are free again at the caller's next
 // barrier.
 SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const float* __restrict__ k,
@@ -186,11 +219,17 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
   // and kept live (spilled) across the selection.
   int tid = threadIdx.x;
   asm volatile("" : "+v"(tid));
+  // The window side and radius likewise: the per-column values derived from
+  // them (offsets d - r, column compares) are formed where they are used
+  // instead of being held in registers across the caller's loop.  The key
+  // stride is 1 on this route, so a cell's offset is F + (d - r).
+  int ws = g.ws, r = g.r;
+  asm volatile("" : "+s"(ws), "+s"(r));
   const int j = tid / NR, dh = tid % NR;
   const int t2 = t + dt;
   const int mh = ty * TQ + j / TQ, mw = tx * TQ + j % TQ;  // query-grid position
   const bool inside = mh < g.nH && mw < g.nW;
-  const bool rowtask = inside && dh <= g.ws;  // thread accumulates a key row
+  const bool rowtask = inside && dh <= ws;  // thread accumulates a key row
   const int h = mh * g.s0, w = mw * g.s0;
 
   float fh = 0.f, fw = 0.f;
@@ -203,11 +242,11 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
   // this thread's key row and the first column of the query's rows; offsets
   // that are not finite or absurdly large are placed at 0 for the region
   // (their cells fail the exact validity test)
-  const int drow = min(dh, g.ws - 1);
-  const float disp_h = cand_disp(fh, g.s1, drow, g.r);
-  const float disp_w0 = cand_disp(fw, g.s1, 0, g.r);
+  const int drow = min(dh, ws - 1);
+  const float disp_h = cand_disp(fh, 1.f, drow, r);
+  const float disp_w0 = cand_disp(fw, 1.f, 0, r);
   const bool sane = fabsf(fh) < kFarDisp && fabsf(fw) < kFarDisp;
-  const int below = dh == g.ws ? 1 : 0;  // the row under the last window row
+  const int below = dh == ws ? 1 : 0;  // the row under the last window row
   const int y0 = (sane ? h + (int)floorf(disp_h) : h) + below;
   const int x0 = sane ? w + (int)floorf(disp_w0) : w;
   if (tid < 4) sm.ubox[tid] = (tid & 1) ? INT_MIN : INT_MAX;
@@ -358,7 +397,7 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
     if (more) store_chunk(buf ^ 1);
   }
   const int ynext = next_lane(y0);
-  const bool okh = inside && dh < g.ws && centre_ok(h, disp_h, g.H) && sane;
+  const bool okh = inside && dh < ws && centre_ok(h, disp_h, g.H) && sane;
 #pragma unroll
   for (int dw = 0; dw < WSM; ++dw) sc[dw] = -INFINITY;
   // Common case: offsets below 64 px whose fractions lie at least 1e-3 from
@@ -382,7 +421,7 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
     float top[WSM];
 #pragma unroll
     for (int dw = 0; dw < WSM; ++dw) {
-      const float disp_w = cand_disp(fw, g.s1, dw, g.r);
+      const float disp_w = cand_disp(fw, 1.f, dw, r);
       const float aw = disp_w - (fl0 + (float)dw);
       top[dw] = fmaf(aw, cr[dw + 1] - cr[dw], cr[dw]);
       if (centre_ok(w, disp_w, g.W)) {
@@ -391,7 +430,7 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
       }
     }
     if (!okh) dlo = WSM;
-    dhi = min(dhi, g.ws - 1);
+    dhi = min(dhi, ws - 1);
 #pragma unroll
     for (int dw = 0; dw < WSM; ++dw) {
       const float bot = next_lane(top[dw]);
@@ -407,8 +446,8 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
       // rounding moved the next window row by two key rows: score directly
       // (one call site; the score lands in its register by selects)
 #pragma unroll 1
-      for (int dw = 0; dw < g.ws; ++dw) {
-        const float disp_w = cand_disp(fw, g.s1, dw, g.r);
+      for (int dw = 0; dw < ws; ++dw) {
+        const float disp_w = cand_disp(fw, 1.f, dw, r);
         const float d = centre_ok(w, disp_w, g.W)
                             ? fmaxf(score_candidate(q, k, g, b, hd, t, h, w, t2, disp_h, disp_w), -INFINITY)
                             : -INFINITY;
@@ -421,8 +460,8 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
       const int fl0 = (int)floorf(disp_w0);
 #pragma unroll
       for (int dw = 0; dw < WSM; ++dw) {
-        if (dw < g.ws) {
-          const float disp_w = cand_disp(fw, g.s1, dw, g.r);
+        if (dw < ws) {
+          const float disp_w = cand_disp(fw, 1.f, dw, r);
           const bool ok = centre_ok(w, disp_w, g.W);
           const float flw = floorf(disp_w);
           const float aw = disp_w - flw;
@@ -440,6 +479,9 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
       }
     }
   }
+  const int nreal = p1_row_cells(g, ty, tx);
+#pragma unroll
+  for (int dw = 0; dw < WSM; ++dw) sc[dw] = dw < nreal ? sc[dw] : no_cell();
 }
 
 // ---- scores to the workspace (k > 32) ----
@@ -532,11 +574,11 @@ __global__ void __launch_bounds__(p1::NT) search_p1_topk_kernel(const float* __r
     if (t2 >= 0 && t2 < g.T) {
       p1_frame_scores(sm, q, k, flows, g, b, hd, t, dt, ty, tx, sc);
     } else {
+      const int nreal = p1_row_cells(g, ty, tx);  // frame outside the clip: invalid cells
 #pragma unroll
-      for (int dw = 0; dw < WSM; ++dw) sc[dw] = -INFINITY;  // frame outside the clip
+      for (int dw = 0; dw < WSM; ++dw) sc[dw] = dw < nreal ? -INFINITY : no_cell();
     }
     if (!inside) continue;
-    const bool cells = dh < g.ws;
     // threshold: the list's k-th entry
     const unsigned long long tsel = (k1 & 1) ? L1 : L0;
     const unsigned thi = (unsigned)__shfl((int)(unsigned)(tsel >> 32), gb + (k1 >> 1));
@@ -552,19 +594,14 @@ __global__ void __launch_bounds__(p1::NT) search_p1_topk_kernel(const float* __r
     // the exact merge); no cell passes when thr is above +inf's key
     const float thrf = empty ? -INFINITY : key_score(thr);
     int npass = 0;
-    if (cells) {
 #pragma unroll
-      for (int dw = 0; dw < WSM; ++dw) npass += (dw < g.ws && sc[dw] >= thrf) ? 1 : 0;
-    }
+    for (int dw = 0; dw < WSM; ++dw) npass += sc[dw] >= thrf ? 1 : 0;  // no_cell() fails every compare
     const int n = grp_sum(npass);
     if (n == 0) continue;
     unsigned u[WSM];  // order keys of the row's cells (0: no cell)
-    unsigned sel = 0;
 #pragma unroll
-    for (int dw = 0; dw < WSM; ++dw) {
-      u[dw] = (cells && dw < g.ws) ? order_key(sc[dw]) : 0u;
-      if (u[dw] != 0u && u[dw] >= thr) sel |= 1u << dw;
-    }
+    for (int dw = 0; dw < WSM; ++dw) u[dw] = order_key(sc[dw]);
+    unsigned sel = col_mask([&](int dw) { return u[dw] != 0u && u[dw] >= thr; });
     auto ukey = [&](int dw) -> unsigned { return u[dw]; };
     int nsel = grp_sum(__builtin_popcount(sel));
     if (nsel > LS) {
@@ -577,7 +614,7 @@ __global__ void __launch_bounds__(p1::NT) search_p1_topk_kernel(const float* __r
       float fmx = -INFINITY, fmn = INFINITY;
 #pragma unroll
       for (int dw = 0; dw < WSM; ++dw)
-        if (cells && dw < g.ws && sc[dw] > -INFINITY) {
+        if (sc[dw] > -INFINITY) {
           fmx = fmaxf(fmx, sc[dw]);
           fmn = fminf(fmn, sc[dw]);
         }
@@ -590,7 +627,7 @@ __global__ void __launch_bounds__(p1::NT) search_p1_topk_kernel(const float* __r
         if (!(thrf > fmn)) flo = nextafterf(fmn, -INFINITY);
         int clo = 0;
 #pragma unroll
-        for (int dw = 0; dw < WSM; ++dw) clo += (cells && dw < g.ws && sc[dw] > flo) ? 1 : 0;
+        for (int dw = 0; dw < WSM; ++dw) clo += sc[dw] > flo ? 1 : 0;
         clo = grp_sum(clo);
         if (clo > LS) {
           for (int it = 0; it < 24; ++it) {
@@ -598,7 +635,7 @@ __global__ void __launch_bounds__(p1::NT) search_p1_topk_kernel(const float* __r
             if (!(mid > flo && mid < fhi)) break;  // adjacent values (or overflow): no split
             int c = 0;
 #pragma unroll
-            for (int dw = 0; dw < WSM; ++dw) c += (cells && dw < g.ws && sc[dw] > mid) ? 1 : 0;
+            for (int dw = 0; dw < WSM; ++dw) c += sc[dw] > mid ? 1 : 0;
             c = grp_sum(c);
             if (c > LS) {
               flo = mid;
@@ -614,9 +651,7 @@ __global__ void __launch_bounds__(p1::NT) search_p1_topk_kernel(const float* __r
       }
       sel = 0;
       if (found) {
-#pragma unroll
-        for (int dw = 0; dw < WSM; ++dw)
-          if (cells && dw < g.ws && sc[dw] > fth) sel |= 1u << dw;
+        sel = col_mask([&](int dw) { return sc[dw] > fth; });
       } else {
         // order keys: cnt(> lo) > 32 and cnt(> hi) < k
         unsigned lo = 0u, hi = 0u;
@@ -641,19 +676,12 @@ __global__ void __launch_bounds__(p1::NT) search_p1_topk_kernel(const float* __r
           }
         }
         if (kfound) {
-#pragma unroll
-          for (int dw = 0; dw < WSM; ++dw)
-            if (ukey(dw) > lo) sel |= 1u << dw;
+          sel = col_mask([&](int dw) { return ukey(dw) > lo; });
         } else {
           // every key above lo equals hi: the cells above hi plus the tied
           // ones of smallest id (lane order, then column order) make k
-          unsigned eq = 0;
-#pragma unroll
-          for (int dw = 0; dw < WSM; ++dw) {
-            const unsigned u = ukey(dw);
-            if (u > hi) sel |= 1u << dw;
-            if (u == hi) eq |= 1u << dw;
-          }
+          sel = col_mask([&](int dw) { return ukey(dw) > hi; });
+          unsigned eq = col_mask([&](int dw) { return ukey(dw) == hi; });
           const int need = g.k - grp_sum(__builtin_popcount(sel));
           int take = need - grp_excl_scan(__builtin_popcount(eq));
           take = min(max(take, 0), __builtin_popcount(eq));
