@@ -24,20 +24,25 @@
 namespace snls {
 
 namespace p1 {
-constexpr int TQ = 8;                  // 8 x 8 queries per workgroup (query-grid units)
-constexpr int NQ = TQ * TQ;
+// TQH x TQW queries per workgroup (query-grid units).  4 x 8 queries make a
+// 512-thread workgroup whose LDS (about 72 KB) and registers (at most 128
+// VGPRs) let two workgroups share a CU, so one's barriers and selection
+// overlap the other's staging and products.
+constexpr int TQH = 4, TQW = 8;
+constexpr int NQ = TQH * TQW;
 constexpr int WSM = 15;                // largest window side
 constexpr int NR = 16;                 // thread slots per query (key rows): one 16-lane DPP row
-constexpr int NT = NQ * NR;            // 1024
+constexpr int NT = NQ * NR;            // 512
 constexpr int NC = WSM + 2;            // correlation columns per key row
 constexpr int CC = 4;                  // channels per staging chunk (double-buffered)
-constexpr int RH = 48, RW = 48;        // key region of the tile
+constexpr int RH = 40, RW = 48;        // key region of the tile
 constexpr int RP = RW + 1;             // row pitch (odd)
 constexpr int NRI = (RH + NT / 64 - 1) / (NT / 64);  // region rows per thread (lane = column)
 constexpr int CHUNK = CC * RH * RP;
 constexpr int QR = WSM + 2;            // per-query block (when the tile's region is too wide): rows ..
 constexpr int QB = QR * NC;            // .. x NC columns, one channel at a time
 constexpr int LS = 32;                 // list slots per query in the fused selection (2 per lane)
+constexpr int WPE = 4;                 // waves per SIMD the registers are budgeted for (128 VGPRs)
 static_assert(NQ * QB <= 2 * CHUNK, "per-query blocks fit in the two staging buffers");
 static_assert(RW <= 64, "a region row is staged by one wave");
 static_assert(NQ * WSM * WSM <= 2 * CHUNK, "the tile's scores of one frame fit in the staging buffers");
@@ -189,7 +194,7 @@ SNLS_DEV int p1_row_cells(const Geo& g, int ty, int tx) {
   int tid = threadIdx.x, ws = g.ws;
   asm volatile("" : "+v"(tid), "+s"(ws));
   const int j = tid / NR, dh = tid % NR;
-  const int mh = ty * TQ + j / TQ, mw = tx * TQ + j % TQ;
+  const int mh = ty * TQH + j / TQW, mw = tx * TQW + j % TQW;
   return (mh < g.nH && mw < g.nW && dh < ws) ? ws : 0;
 }
 
@@ -227,7 +232,7 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
   asm volatile("" : "+s"(ws), "+s"(r));
   const int j = tid / NR, dh = tid % NR;
   const int t2 = t + dt;
-  const int mh = ty * TQ + j / TQ, mw = tx * TQ + j % TQ;  // query-grid position
+  const int mh = ty * TQH + j / TQW, mw = tx * TQW + j % TQW;  // query-grid position
   const bool inside = mh < g.nH && mw < g.nW;
   const bool rowtask = inside && dh <= ws;  // thread accumulates a key row
   const int h = mh * g.s0, w = mw * g.s0;
@@ -287,7 +292,7 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
     return (y >= 0 && y < g.H && x >= 0 && x < g.W) ? kb[(long long)c * g.HW + (long long)y * g.W + x] : 0.f;
   };
   const int cpc = staged ? CC : 1;  // channels per chunk
-  // Region staging through registers: lane = column, the 16 waves take the
+  // Region staging through registers: lane = column, the NT / 64 waves take the
   // rows (NRI rows each); a chunk's loads are issued before the products of
   // the previous chunk and written to LDS after them.
   const int xx = tid & 63;
@@ -312,7 +317,7 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
   unsigned qoff = OOB;
   if (tid < CC * NQ) {
     const int c = tid / NQ, jj = tid % NQ;
-    const int qh = (ty * TQ + jj / TQ) * g.s0, qw = (tx * TQ + jj % TQ) * g.s0;
+    const int qh = (ty * TQH + jj / TQW) * g.s0, qw = (tx * TQW + jj % TQW) * g.s0;
     if (qh < g.H && qw < g.W) qoff = (unsigned)(((long long)c * g.HW + (long long)qh * g.W + qw) * 4);
   }
   float stg[CC][NRI];
@@ -348,7 +353,7 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
       (&sm.reg[0][0])[e] = kval(c0, sm.y0q[jj] + yy, sm.x0q[jj] + x);
     }
     if (tid < NQ) {
-      const int qh = (ty * TQ + tid / TQ) * g.s0, qw = (tx * TQ + tid % TQ) * g.s0;
+      const int qh = (ty * TQH + tid / TQW) * g.s0, qw = (tx * TQW + tid % TQW) * g.s0;
       sm.qs[0][tid][0] = (qh < g.H && qw < g.W) ? qb[(long long)c0 * g.HW + (long long)qh * g.W + qw] : 0.f;
     }
   };
@@ -486,7 +491,7 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
 
 // ---- scores to the workspace (k > 32) ----
 
-__global__ void __launch_bounds__(p1::NT) search_p1_scores_kernel(const float* __restrict__ q,
+__global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_scores_kernel(const float* __restrict__ q,
                                                                const float* __restrict__ k,
                                                                const float* __restrict__ flows, Geo g, int tiles_x,
                                                                float* __restrict__ scores, int pitch) {
@@ -517,7 +522,7 @@ __global__ void __launch_bounds__(p1::NT) search_p1_scores_kernel(const float* _
   // copy out: one wave per query row of the tile at a time
   const int lane = tid & 63;
   for (int jj = tid >> 6; jj < NQ; jj += NT / 64) {
-    const int qh = ty * TQ + jj / TQ, qw = tx * TQ + jj % TQ;
+    const int qh = ty * TQH + jj / TQW, qw = tx * TQW + jj % TQW;
     if (qh >= g.nH || qw >= g.nW) continue;
     const long long qrow = ((((long long)b * g.HD + hd) * g.T + t) * g.nH + qh) * g.nW + qw;
     float* srow = scores + qrow * pitch + (dt + g.wt) * nc2;
@@ -527,7 +532,7 @@ __global__ void __launch_bounds__(p1::NT) search_p1_scores_kernel(const float* _
 
 // ---- fused search and top-k (k <= 32) ----
 //
-// One workgroup = 8 x 8 queries of one (b, head, t), looping over the frames
+// One workgroup = TQH x TQW queries of one (b, head, t), looping over the frames
 // of the window, the query frame first and then the nearest frames (good
 // thresholds early).  The 16 threads of a query (one 16-lane DPP row) hold
 // its running list of the 32 best candidates so far, 2 per lane, best first,
@@ -542,7 +547,7 @@ __global__ void __launch_bounds__(p1::NT) search_p1_scores_kernel(const float* _
 // cells above the tie plus the tied ones of smallest id make the frame's
 // top k.  Frames outside the clip contribute invalid candidates (-inf) in
 // id order, which matter only while fewer than k better entries are known.
-__global__ void __launch_bounds__(p1::NT) search_p1_topk_kernel(const float* __restrict__ q,
+__global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_topk_kernel(const float* __restrict__ q,
                                                              const float* __restrict__ k,
                                                              const float* __restrict__ flows, Geo g, int tiles_x,
                                                              float* __restrict__ dists, float* __restrict__ inds) {
@@ -559,7 +564,7 @@ __global__ void __launch_bounds__(p1::NT) search_p1_topk_kernel(const float* __r
   const int xcd = (int)blockIdx.x % 8, xq = ntile / 8, xrem = ntile % 8;
   const int tile = xcd * xq + min(xcd, xrem) + (int)blockIdx.x / 8;
   const int ty = tile / tiles_x, tx = tile % tiles_x;
-  const int mh = ty * TQ + j / TQ, mw = tx * TQ + j % TQ;
+  const int mh = ty * TQH + j / TQW, mw = tx * TQW + j % TQW;
   const bool inside = mh < g.nH && mw < g.nW;  // the same for the query's 16 lanes
   const int gb = (tid & 63) & ~15;             // the group's first lane in the wave
   const int ncell = g.ws * g.ws;
@@ -768,7 +773,7 @@ bool p1_fused(const Geo& g) { return p1_supported(g) && g.k <= p1::LS; }
 
 snls_status launch_search_p1_scores(const float* q, const float* k, const float* flows, const Geo& g, float* scores,
                                     int pitch, hipStream_t s) {
-  const int tiles_x = (g.nW + p1::TQ - 1) / p1::TQ, tiles_y = (g.nH + p1::TQ - 1) / p1::TQ;
+  const int tiles_x = (g.nW + p1::TQW - 1) / p1::TQW, tiles_y = (g.nH + p1::TQH - 1) / p1::TQH;
   const long long ntile = (long long)tiles_x * tiles_y;
   if (ntile == 0 || g.rows == 0) return SNLS_OK;
   if (ntile > 0x7fffffffLL || (long long)g.B * g.HD * g.T > 65535 || 2 * g.wt + 1 > 65535) return SNLS_ERR_UNSUPPORTED;
@@ -779,7 +784,7 @@ snls_status launch_search_p1_scores(const float* q, const float* k, const float*
 
 snls_status launch_search_p1_topk(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                   float* inds, hipStream_t s) {
-  const int tiles_x = (g.nW + p1::TQ - 1) / p1::TQ, tiles_y = (g.nH + p1::TQ - 1) / p1::TQ;
+  const int tiles_x = (g.nW + p1::TQW - 1) / p1::TQW, tiles_y = (g.nH + p1::TQH - 1) / p1::TQH;
   const long long ntile = (long long)tiles_x * tiles_y;
   if (ntile == 0 || g.rows == 0) return SNLS_OK;
   if (ntile > 0x7fffffffLL || (long long)g.B * g.HD * g.T > 65535) return SNLS_ERR_UNSUPPORTED;
