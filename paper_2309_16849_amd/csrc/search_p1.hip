@@ -174,7 +174,7 @@ template <class Pred>
 SNLS_DEV unsigned col_mask(Pred pred) {
   unsigned m = 0;
 #pragma unroll
-  for (int dw = p1::WSM - 1; dw >= 0; --dw) m = (m << 1) | (pred(dw) ? 1u : 0u);
+  for (int dw = p1::WSM - 1; dw >= 0; --dw) m = m + m + (pred(dw) ? 1u : 0u);  // one add with carry-in
   return m;
 }
 
@@ -418,24 +418,20 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
     // next row's come from the next lane (every lane of the query takes part)
     const float fl0 = floorf(disp_w0);
     const float ah = disp_h - floorf(disp_h);
-    // valid cells: centre column w + disp_w in [0, W-1]; disp_w is monotone
-    // in d_w, so they form one range of d_w
-    // valid cells: centre column w + disp_w in [0, W-1]; disp_w is monotone
-    // in d_w, so they form one range of d_w
-    int dlo = WSM, dhi = -1;
+    // Valid cells: centre column w + disp_w in [0, W-1], i.e. d_w - r in
+    // [-w - F, W-1-w - F].  Here the rounded offsets stay between the same
+    // integers as the exact ones, and the bounds below are computed with an
+    // error far below the fractions' 1e-3 distance from an integer, so their
+    // ceiling and floor give the exact range of d_w.
+    const int dlo = okh ? max(0, (int)ceilf((float)(r - w) - fw)) : WSM;
+    const int dhi = min(ws - 1, (int)floorf((float)(g.W - 1 - w + r) - fw));
     float top[WSM];
 #pragma unroll
     for (int dw = 0; dw < WSM; ++dw) {
       const float disp_w = cand_disp(fw, 1.f, dw, r);
       const float aw = disp_w - (fl0 + (float)dw);
       top[dw] = fmaf(aw, cr[dw + 1] - cr[dw], cr[dw]);
-      if (centre_ok(w, disp_w, g.W)) {
-        dlo = min(dlo, dw);
-        dhi = dw;
-      }
     }
-    if (!okh) dlo = WSM;
-    dhi = min(dhi, ws - 1);
 #pragma unroll
     for (int dw = 0; dw < WSM; ++dw) {
       const float bot = next_lane(top[dw]);
@@ -598,17 +594,14 @@ __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_topk_kernel(const f
     // order only merges -0 and +0, which lets a few more cells through to
     // the exact merge); no cell passes when thr is above +inf's key
     const float thrf = empty ? -INFINITY : key_score(thr);
-    int npass = 0;
-#pragma unroll
-    for (int dw = 0; dw < WSM; ++dw) npass += sc[dw] >= thrf ? 1 : 0;  // no_cell() fails every compare
-    const int n = grp_sum(npass);
-    if (n == 0) continue;
-    unsigned u[WSM];  // order keys of the row's cells (0: no cell)
-#pragma unroll
-    for (int dw = 0; dw < WSM; ++dw) u[dw] = order_key(sc[dw]);
-    unsigned sel = col_mask([&](int dw) { return u[dw] != 0u && u[dw] >= thr; });
-    auto ukey = [&](int dw) -> unsigned { return u[dw]; };
+    // The cells passing the float test are taken: a superset of those whose
+    // key reaches thr (the extra ones, -0 cells against a threshold of +0,
+    // are real candidates ranking after the list's k-th entry, so they
+    // cannot enter the k best); no_cell() fails every compare.
+    unsigned sel = col_mask([&](int dw) { return sc[dw] >= thrf; });
     int nsel = grp_sum(__builtin_popcount(sel));
+    if (nsel == 0) continue;
+    auto ukey = [&](int dw) -> unsigned { return order_key(sc[dw]); };  // 0: no cell
     if (nsel > LS) {
       // More than 32 cells rank before the list's k-th entry: keep the
       // frame's best only, above a threshold with between k and 32 cells
@@ -616,13 +609,13 @@ __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_topk_kernel(const f
       // Bisection over the scores' values first, over their order keys
       // when the values do not separate (ties, -inf cells, huge ranges).
       bool found = false;
-      float fmx = -INFINITY, fmn = INFINITY;
+      float fmx = -INFINITY, fmn = INFINITY;  // over the cells above -inf (no_cell() fails both tests)
 #pragma unroll
-      for (int dw = 0; dw < WSM; ++dw)
-        if (sc[dw] > -INFINITY) {
-          fmx = fmaxf(fmx, sc[dw]);
-          fmn = fminf(fmn, sc[dw]);
-        }
+      for (int dw = 0; dw < WSM; ++dw) {
+        const float v = sc[dw];
+        fmx = v > fmx ? v : fmx;
+        fmn = v > -INFINITY && v < fmn ? v : fmn;
+      }
       fmx = __uint_as_float(order_key_inv(grp_max(order_key(fmx))));
       fmn = -__uint_as_float(order_key_inv(grp_max(order_key(-fmn))));
       float flo = thrf > fmn ? thrf : fmn, fhi = fmx;  // keep cnt(> fhi) = 0 < k
