@@ -658,20 +658,26 @@ __global__ void __launch_bounds__(256) to_head_channels_last_kernel(const float*
 // Single-pixel patches (P = 1): a query covers only its own pixel (count 1),
 // so the output at a query pixel is the weighted sum of the k bilinear reads
 // of its neighbours and every other pixel is 0 (a query stride above 1
-// leaves holes).  A workgroup takes 64 consecutive query rows: their scores
-// and positions are copied to LDS with consecutive threads on consecutive
-// addresses, and one thread per row turns the scores into softmax weights.
+// leaves holes).  A workgroup takes an 8 x 8 tile of queries of one (b,
+// head, t): one wave per query row reads its scores and positions (lane =
+// neighbour, coalesced), forms the softmax weights with wave reductions and
+// stores (weight, frame, offsets) per neighbour in LDS as one 16-byte
+// record.  The tiles of one (b, head) run in the order (tile
+// row, tile column, t), so that the workgroups in flight on an XCD cover a
+// band of the frame in every query frame: their neighbours' taps then fall
+// in a few MB of V that the XCD's L2 holds, instead of a whole frame per
+// query frame.
 // Then each thread takes (query, group of 4 channels) pairs -- consecutive
 // lanes the channel groups of one query, then the next query -- and reads
 // per neighbour four 16-byte pieces of the head-major channels-last V (the
 // lanes of a query read one contiguous pixel record per tap).  Each pair
 // also clears the other pixels of its S_Q x S_Q cell.
 namespace aggp1 {
-constexpr int NQ = 64;    // query rows per workgroup
-constexpr int KMAX = 60;  // neighbours per row (LDS below 64 KB)
-// dynamic LDS: NQ rows of scores / weights (odd pitch), then NQ rows of positions
-SNLS_DEV int pitch(int k) { return k | 1; }
-inline size_t lds_bytes(int k) { return (size_t)NQ * ((k | 1) + 3 * k) * sizeof(float); }
+constexpr int TH = 8, TW = 8;  // query tile (query-grid units)
+constexpr int NQ = TH * TW;    // query rows per workgroup
+constexpr int KMAX = 60;  // neighbours per row (a wave's lanes; LDS below 64 KB)
+// dynamic LDS: NQ rows of k (weight, frame, disp_h, disp_w) records
+inline size_t lds_bytes(int k) { return (size_t)NQ * k * 4 * sizeof(float); }
 }  // namespace aggp1
 
 __global__ void __launch_bounds__(256) aggregate_p1_kernel(const float* __restrict__ vhl,
@@ -679,56 +685,68 @@ __global__ void __launch_bounds__(256) aggregate_p1_kernel(const float* __restri
                                                            const float* __restrict__ inds, Geo g, float scale,
                                                            float* __restrict__ out) {
   using namespace aggp1;
-  extern __shared__ float lds_p1[];
-  const int k = g.k, KP = pitch(k);
-  float* wl_s = lds_p1;              // scores, then weights (0: neighbour skipped)
-  float* ind_s = lds_p1 + NQ * KP;   // (frame, disp_h, disp_w) per neighbour
+  extern __shared__ float4 nb_s[];  // [NQ][k]: weight (0: skipped), frame, disp_h, disp_w
+  const int k = g.k;
   const int tid = threadIdx.x;
   // Consecutive workgroups land on different XCDs (8 per device): give each
-  // XCD a contiguous run of query rows, whose neighbours' taps overlap in
-  // its L2.
+  // XCD a contiguous run of tiles, whose neighbours' taps overlap in its L2.
   const long long nwg = (long long)gridDim.x;
   const long long xcd = blockIdx.x % 8, xq = nwg / 8, xrem = nwg % 8;
   const long long wg = xcd * xq + (xcd < xrem ? xcd : xrem) + blockIdx.x / 8;
-  const long long row0 = wg * NQ;
-  const int nq = (int)min((long long)NQ, g.rows - row0);
-  for (int e = tid; e < nq * k; e += 256) wl_s[(e / k) * KP + e % k] = dists[row0 * k + e];
-  for (int e = tid; e < nq * 3 * k; e += 256) ind_s[e] = inds[row0 * 3 * k + e];
-  __syncthreads();
-  if (tid < nq) {
-    const float sscale = (g.dist == SNLS_DIST_PROD ? 1.f : -1.f) * scale;
-    float* d = &wl_s[tid * KP];
-    const float* ind = &ind_s[tid * 3 * k];
-    float m = -INFINITY;
-    for (int l = 0; l < k; ++l)
-      if (isfinite(d[l])) m = fmaxf(m, sscale * d[l]);
-    float z = 0.f;
-    for (int l = 0; l < k; ++l)
-      if (isfinite(d[l])) z += expf(sscale * d[l] - m);
-    const float inv = z > 0.f ? 1.f / z : 0.f;
-    for (int l = 0; l < k; ++l) {
-      const float tf = ind[3 * l], dh = ind[3 * l + 1], dw = ind[3 * l + 2];
-      const bool ok = isfinite(d[l]) && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < kFarDisp &&
-                      fabsf(dw) < kFarDisp;
-      d[l] = ok ? expf(sscale * d[l] - m) * inv : 0.f;
+  const int tqx = (g.nW + TW - 1) / TW, tqy = (g.nH + TH - 1) / TH;
+  long long rr = wg;
+  const int t = (int)(rr % g.T);
+  rr /= g.T;
+  const int tx = (int)(rr % tqx);
+  rr /= tqx;
+  const int ty = (int)(rr % tqy);
+  rr /= tqy;
+  const int hd = (int)(rr % g.HD);
+  const int b = (int)(rr / g.HD);
+  const long long rowimg = (((long long)b * g.HD + hd) * g.T + t) * g.nH;
+  // query jq of the tile: grid position, whether it exists, its row
+  auto qpos = [&](int jq, int& mh, int& mw) {
+    mh = ty * TH + jq / TW;
+    mw = tx * TW + jq % TW;
+    return mh < g.nH && mw < g.nW;
+  };
+  // softmax weights: one wave per query row, lane = neighbour
+  const int lane = tid & 63;
+  const float sscale = (g.dist == SNLS_DIST_PROD ? 1.f : -1.f) * scale;
+  for (int jq = tid >> 6; jq < NQ; jq += 4) {
+    int mh, mw;
+    if (!qpos(jq, mh, mw)) continue;  // the same for the whole wave
+    const long long row = (rowimg + mh) * g.nW + mw;
+    const bool on = lane < k;
+    const float d = on ? dists[row * k + lane] : 0.f;
+    float tf = 0.f, dh = 0.f, dw = 0.f;
+    if (on) {
+      tf = inds[(row * k + lane) * 3];
+      dh = inds[(row * k + lane) * 3 + 1];
+      dw = inds[(row * k + lane) * 3 + 2];
     }
+    const bool fin = on && isfinite(d);
+    const float x = sscale * d;
+    float m = fin ? x : -INFINITY;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    const float e = fin ? expf(x - m) : 0.f;
+    float z = e;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o);
+    const float inv = z > 0.f ? 1.f / z : 0.f;
+    const bool ok = fin && tf >= 0.f && tf < (float)g.T && tf == floorf(tf) && fabsf(dh) < kFarDisp &&
+                    fabsf(dw) < kFarDisp;
+    if (on) nb_s[jq * k + lane] = make_float4(ok ? e * inv : 0.f, tf, dh, dw);
   }
   __syncthreads();
   const int ngrp = g.Ch / 4;
-  for (int pr = tid; pr < nq * ngrp; pr += 256) {
+  for (int pr = tid; pr < NQ * ngrp; pr += 256) {
     const int jq = pr / ngrp, cg = pr - jq * ngrp;
-    const long long row = row0 + jq;
-    const int mw = (int)(row % g.nW);
-    long long r = row / g.nW;
-    const int mh = (int)(r % g.nH);
-    r /= g.nH;
-    const int t = (int)(r % g.T);
-    r /= g.T;
-    const int hd = (int)(r % g.HD);
-    const int b = (int)(r / g.HD);
+    int mh, mw;
+    if (!qpos(jq, mh, mw)) continue;
     const int h = mh * g.s0, w = mw * g.s0;
-    const float* wrow = &wl_s[jq * KP];
-    const float* ind = &ind_s[jq * 3 * k];
+    const float4* nb = &nb_s[jq * k];
     // head plane of V (frame added per neighbour), this thread's 4 channels
     const float* vh = vhl + ((long long)b * g.T * g.HD + hd) * g.HW * g.Ch + 4 * cg;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -736,11 +754,11 @@ __global__ void __launch_bounds__(256) aggregate_p1_kernel(const float* __restri
     // the reads of several neighbours are in flight together
 #pragma unroll 2
     for (int l = 0; l < k; ++l) {
-      const float wl = wrow[l];
+      const float4 rec = nb[l];
+      const float wl = rec.x;
       const bool use = wl != 0.f;
-      const float tf0 = ind[3 * l], dh0 = ind[3 * l + 1], dw0 = ind[3 * l + 2];
-      const float tf = use ? tf0 : 0.f;
-      const float dh = use ? dh0 : 0.f, dw = use ? dw0 : 0.f;
+      const float tf = use ? rec.y : 0.f;
+      const float dh = use ? rec.z : 0.f, dw = use ? rec.w : 0.f;
       int ny, nx;
       float ay, ax;
       split_disp(dh, &ny, &ay);
@@ -892,7 +910,8 @@ snls_status launch_aggregate(const float* v, const float* dists, const float* in
   const int nslot = 2 * g.wt + 1;
   if (g.ps == 1 && g.Ch % 4 == 0 && g.k <= aggp1::KMAX) {
     // single-pixel patches: per-query gather, holes cleared
-    const long long nblk = (g.rows + aggp1::NQ - 1) / aggp1::NQ;
+    const long long nblk = (long long)g.B * g.HD * g.T * ((g.nH + aggp1::TH - 1) / aggp1::TH) *
+                           ((g.nW + aggp1::TW - 1) / aggp1::TW);
     if (nblk > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
     dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
     hipLaunchKernelGGL(to_head_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
