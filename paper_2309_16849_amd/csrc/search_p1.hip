@@ -231,6 +231,7 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
   int ws = g.ws, r = g.r;
   asm volatile("" : "+s"(ws), "+s"(r));
   const int j = tid / NR, dh = tid % NR;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int t2 = t + dt;
   const int mh = ty * TQH + j / TQW, mw = tx * TQW + j % TQW;  // query-grid position
   const bool inside = mh < g.nH && mw < g.nW;
@@ -261,15 +262,19 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
   }
   __syncthreads();
   {
-    // union bounds: wave reductions, then one LDS atomic per wave
-    int a0 = rowtask ? y0 : INT_MAX, a1 = rowtask ? y0 : INT_MIN;
-    int a2 = rowtask ? x0 : INT_MAX, a3 = rowtask ? x0 : INT_MIN;
+    // union bounds: a query's key rows grow with d_h (its first row at d_h =
+    // 0, its last at d_h = ws) and all its rows start at one column, so a
+    // wave reads the bounds from its queries' lanes; one LDS atomic per wave
+    int a0 = INT_MAX, a1 = INT_MIN, a2 = INT_MAX, a3 = INT_MIN;
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      a0 = min(a0, __shfl_xor(a0, off));
-      a1 = max(a1, __shfl_xor(a1, off));
-      a2 = min(a2, __shfl_xor(a2, off));
-      a3 = max(a3, __shfl_xor(a3, off));
+    for (int qq = 0; qq < 64 / NR; ++qq) {
+      const int jq = wv * (64 / NR) + qq;  // the query of lanes NR qq .. NR qq + NR - 1
+      if (ty * TQH + jq / TQW < g.nH && tx * TQW + jq % TQW < g.nW) {
+        a0 = min(a0, __builtin_amdgcn_readlane(y0, NR * qq));
+        a1 = max(a1, __builtin_amdgcn_readlane(y0, NR * qq + ws));
+        a2 = min(a2, __builtin_amdgcn_readlane(x0, NR * qq));
+        a3 = max(a3, __builtin_amdgcn_readlane(x0, NR * qq));
+      }
     }
     if ((tid & 63) == 0 && a0 <= a1) {
       atomicMin(&sm.ubox[0], a0);
@@ -303,12 +308,12 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
   const __amdgpu_buffer_rsrc_t k_rs =
       __builtin_amdgcn_make_buffer_rsrc((void*)kb, (short)0, (int)(g.Ch * g.HW * 4), 0x00020000);
   unsigned roff[NRI];  // byte offset of this thread's region pixels in channel 0 (OOB: none)
+  const int x = rx0 + xx;
+  const bool colok = staged && xx < rw && x >= 0 && x < g.W;
 #pragma unroll
   for (int i = 0; i < NRI; ++i) {
-    const int yy = (tid >> 6) + (NT / 64) * i;
-    const int y = ry0 + yy, x = rx0 + xx;
-    roff[i] = (staged && xx < rw && yy < rh && y >= 0 && y < g.H && x >= 0 && x < g.W) ? (unsigned)((y * g.W + x) * 4)
-                                                                                        : OOB;
+    const int yy = wv + (NT / 64) * i, y = ry0 + yy;  // uniform: the row test is scalar
+    roff[i] = (yy < rh && y >= 0 && y < g.H && colok) ? (unsigned)((y * g.W + x) * 4) : OOB;
   }
   // this thread's q staging item (tid < CC * NQ): channel tid / NQ of query
   // tid % NQ, as a byte offset in channel 0 (OOB: outside the frame)
@@ -341,7 +346,7 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
       float4* r4 = reinterpret_cast<float4*>(sm.reg[buf]);
 #pragma unroll
       for (int i = 0; i < NRI; ++i)
-        r4[((tid >> 6) + (NT / 64) * i) * RP + xx] = make_float4(stg[0][i], stg[1][i], stg[2][i], stg[3][i]);
+        r4[(wv + (NT / 64) * i) * RP + xx] = make_float4(stg[0][i], stg[1][i], stg[2][i], stg[3][i]);
     }
     if (tid < CC * NQ) sm.qs[buf][tid % NQ][tid / NQ] = qstg;
   };
