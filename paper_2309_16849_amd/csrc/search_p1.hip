@@ -296,7 +296,6 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
   auto kval = [&](int c, int y, int x) -> float {
     return (y >= 0 && y < g.H && x >= 0 && x < g.W) ? kb[(long long)c * g.HW + (long long)y * g.W + x] : 0.f;
   };
-  const int cpc = staged ? CC : 1;  // channels per chunk
   // Region staging through registers: lane = column, the NT / 64 waves take the
   // rows (NRI rows each); a chunk's loads are issued before the products of
   // the previous chunk and written to LDS after them.
@@ -368,23 +367,17 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
   float cr[NC];  // correlations of key row y0, columns x0 ..
 #pragma unroll
   for (int x = 0; x < NC; ++x) cr[x] = 0.f;
+  // Two separate loops (the branch is uniform), so that the accumulators
+  // are not merged from two paths on every chunk.
   if (staged) {
     load_chunk(0);
     store_chunk(0);
-  }
-  int buf = 0;
-  for (int c0 = 0; c0 < g.Ch; c0 += cpc, buf ^= staged ? 1 : 0) {
-    const bool more = staged && c0 + cpc < g.Ch;
-    if (staged) {
-      __syncthreads();  // chunk c0 is staged in buf; buf^1 is free
-      if (more) load_chunk(c0 + cpc);  // in flight during this chunk's products
-    } else {
-      __syncthreads();  // the previous channel is no longer read
-      stage_blocks(c0);
-      __syncthreads();
-    }
-    if (rowtask) {
-      if (staged) {
+    int buf = 0;
+    for (int c0 = 0; c0 < g.Ch; c0 += CC, buf ^= 1) {
+      const bool more = c0 + CC < g.Ch;
+      __syncthreads();                 // chunk c0 is staged in buf; buf^1 is free
+      if (more) load_chunk(c0 + CC);  // in flight during this chunk's products
+      if (rowtask) {
         // channels past the head were staged as zeros
         static_assert(CC == 4, "one 16-byte slot per pixel");
         const float4 q4 = *reinterpret_cast<const float4*>(sm.qs[buf][j]);
@@ -397,14 +390,21 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
           cr[x] = fmaf(q4.z, kv.z, cr[x]);
           cr[x] = fmaf(q4.w, kv.w, cr[x]);
         }
-      } else {
+      }
+      if (more) store_chunk(buf ^ 1);
+    }
+  } else {
+    for (int c0 = 0; c0 < g.Ch; ++c0) {
+      __syncthreads();  // the previous channel is no longer read
+      stage_blocks(c0);
+      __syncthreads();
+      if (rowtask) {
         const float qv = sm.qs[0][j][0];
         const float* r0 = &sm.reg[0][0] + toff;
 #pragma unroll
         for (int x = 0; x < NC; ++x) cr[x] = fmaf(qv, r0[x], cr[x]);
       }
     }
-    if (more) store_chunk(buf ^ 1);
   }
   const int ynext = next_lane(y0);
   const bool okh = inside && dh < ws && centre_ok(h, disp_h, g.H) && sane;
