@@ -56,28 +56,51 @@ SNLS_DEV int next_lane(int v) { return __builtin_amdgcn_update_dpp(0, v, 0x101, 
 
 // ---- 16-lane group operations (the 16 threads of a query are one DPP row) ----
 
-// Value of lane ^ M of the group (M < 16).
+// DPP row operation CTRL on a 32-bit value (every lane of the row is active).
+template <int CTRL>
+SNLS_DEV unsigned dpp_row(unsigned v) {
+  return (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xf, 0xf, false);
+}
+// Value of lane i ^ M of the group (M in {1, 2, 4, 8, 15}; l = i) through
+// DPP, not the LDS crossbar: quad permutes for 1 and 2, a row rotation by 8,
+// for 4 a rotation by 4 (lane i - 4, bit 2 of i set) or by 12 (lane i + 4),
+// the row mirror for 15.  A rotation by N gives lane i the value of lane
+// (i - N) mod 16.
 template <int M>
-SNLS_DEV unsigned grp_xor(unsigned x) {
-  return (unsigned)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (M << 10));
+SNLS_DEV unsigned grp_xor(unsigned x, int l) {
+  static_assert(M == 1 || M == 2 || M == 4 || M == 8 || M == 15, "partner distance");
+  if constexpr (M == 1) return dpp_row<0xB1>(x);  // quad_perm [1,0,3,2]
+  else if constexpr (M == 2) return dpp_row<0x4E>(x);  // quad_perm [2,3,0,1]
+  else if constexpr (M == 8) return dpp_row<0x128>(x);  // row_ror:8
+  else if constexpr (M == 15) return dpp_row<0x140>(x);  // row_mirror
+  else {
+    // both rotations run with every lane of the row active (a DPP read from
+    // a lane switched off by a branch returns 0), then one is selected
+    unsigned a = dpp_row<0x124>(x), b = dpp_row<0x12C>(x);  // row_ror:4 / row_ror:12
+    asm volatile("" : "+v"(a), "+v"(b));
+    return (l & 4) ? a : b;
+  }
 }
 template <int M>
-SNLS_DEV unsigned long long grp_xor64(unsigned long long x) {
-  return ((unsigned long long)grp_xor<M>((unsigned)(x >> 32)) << 32) | grp_xor<M>((unsigned)x);
+SNLS_DEV unsigned long long grp_xor64(unsigned long long x, int l) {
+  return ((unsigned long long)grp_xor<M>((unsigned)(x >> 32), l) << 32) | grp_xor<M>((unsigned)x, l);
 }
-// Sum and maximum over the group (every lane gets the result).
+// Sum and maximum over the group (every lane gets the result): rotations by
+// 8, 4, 2 and 1 lanes -- after the step by 8 a lane's value depends only on
+// its lane mod 8, so the rotation by 4 reads its xor-4 partner's value, and
+// so on.
 SNLS_DEV int grp_sum(int x) {
-  x += (int)grp_xor<8>((unsigned)x);
-  x += (int)grp_xor<4>((unsigned)x);
-  x += (int)grp_xor<2>((unsigned)x);
-  x += (int)grp_xor<1>((unsigned)x);
+  x += (int)dpp_row<0x128>((unsigned)x);
+  x += (int)dpp_row<0x124>((unsigned)x);
+  x += (int)dpp_row<0x122>((unsigned)x);
+  x += (int)dpp_row<0x121>((unsigned)x);
   return x;
 }
 SNLS_DEV unsigned grp_max(unsigned x) {
-  x = max(x, grp_xor<8>(x));
-  x = max(x, grp_xor<4>(x));
-  x = max(x, grp_xor<2>(x));
-  x = max(x, grp_xor<1>(x));
+  x = max(x, dpp_row<0x128>(x));
+  x = max(x, dpp_row<0x124>(x));
+  x = max(x, dpp_row<0x122>(x));
+  x = max(x, dpp_row<0x121>(x));
   return x;
 }
 // Value of lane i - N of the row (0 for i < N).
@@ -122,7 +145,7 @@ SNLS_DEV void bitonic_stage(unsigned long long& x0, unsigned long long& x1, int 
     x1 = desc ? lo : hi;
   } else {
     constexpr int LM = STRIDE / 2;  // partner lane distance
-    const unsigned long long p0 = grp_xor64<LM>(x0), p1 = grp_xor64<LM>(x1);
+    const unsigned long long p0 = grp_xor64<LM>(x0, l), p1 = grp_xor64<LM>(x1, l);
     const bool keep_max = ((l & LM) == 0) == desc;
     x0 = keep_max ? (x0 > p0 ? x0 : p0) : (x0 < p0 ? x0 : p0);
     x1 = keep_max ? (x1 > p1 ? x1 : p1) : (x1 < p1 ? x1 : p1);
@@ -158,7 +181,7 @@ SNLS_DEV void merge_top32(unsigned long long& a0, unsigned long long& a1, unsign
                           unsigned long long s1, int l) {
   asm volatile("" : "+v"(l));  // as in bitonic_sort32
   // s[31 - e] for e = 2l is s1 of lane 15 - l, for e = 2l + 1 it is s0
-  const unsigned long long r0 = grp_xor64<15>(s1), r1 = grp_xor64<15>(s0);
+  const unsigned long long r0 = grp_xor64<15>(s1, l), r1 = grp_xor64<15>(s0, l);
   a0 = a0 > r0 ? a0 : r0;
   a1 = a1 > r1 ? a1 : r1;
   bitonic_stage<64, 16>(a0, a1, l);
