@@ -733,7 +733,9 @@ __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_topk_kernel(const f
       }
     }
     wave_lds_sync();
-    if (ntot <= kInsertMax) {
+    // One choice for the whole wave: its groups would otherwise run both
+    // paths one after the other.  The sort path takes any count up to 32.
+    if (__builtin_amdgcn_ballot_w64(ntot > kInsertMax) == 0) {
       // few cells: insert them one at a time (the entries above a cell are
       // a prefix of the sorted list; the ones after it move down one slot)
       for (int i = 0; i < ntot; ++i) {
