@@ -212,10 +212,12 @@ SNLS_DEV float no_cell() { return __uint_as_float(0xffffffffu); }
 // threads with d_h >= ws and queries outside the grid.  The thread index is
 // opaque, so the per-column compares against it stay inside a caller's frame
 // loop instead of being hoisted as live lane masks.
+template <int WSF>
 SNLS_DEV int p1_row_cells(const Geo& g, int ty, int tx) {
   using namespace p1;
-  int tid = threadIdx.x, ws = g.ws;
-  asm volatile("" : "+v"(tid), "+s"(ws));
+  int tid = threadIdx.x, ws = WSF > 0 ? WSF : g.ws;
+  asm volatile("" : "+v"(tid));
+  if constexpr (WSF == 0) asm volatile("" : "+s"(ws));
   const int j = tid / NR, dh = tid % NR;
   const int mh = ty * TQH + j / TQW, mw = tx * TQW + j % TQW;
   return (mh < g.nH && mw < g.nW && dh < ws) ? ws : 0;
@@ -238,6 +240,7 @@ struct P1Smem {
 // the grid).  Workgroup barriers inside: every
 // thread calls it; its staging buffers are free again at the caller's next
 // barrier.
+template <int WSF>
 SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const float* __restrict__ k,
                               const float* __restrict__ flows, const Geo& g, int b, int hd, int t, int dt, int ty,
                               int tx, float (&sc)[p1::WSM]) {
@@ -249,10 +252,11 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
   asm volatile("" : "+v"(tid));
   // The window side and radius likewise: the per-column values derived from
   // them (offsets d - r, column compares) are formed where they are used
-  // instead of being held in registers across the caller's loop.  The key
-  // stride is 1 on this route, so a cell's offset is F + (d - r).
-  int ws = g.ws, r = g.r;
-  asm volatile("" : "+s"(ws), "+s"(r));
+  // instead of being held in registers across the caller's loop; a window
+  // side fixed at compile time (WSF > 0) makes them immediates instead.  The
+  // key stride is 1 on this route, so a cell's offset is F + (d - r).
+  int ws = WSF > 0 ? WSF : g.ws, r = WSF > 0 ? WSF / 2 : g.r;
+  if constexpr (WSF == 0) asm volatile("" : "+s"(ws), "+s"(r));
   const int j = tid / NR, dh = tid % NR;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index (uniform)
   const int t2 = t + dt;
@@ -508,7 +512,7 @@ SNLS_DEV void p1_frame_scores(P1Smem& sm, const float* __restrict__ q, const flo
       }
     }
   }
-  const int nreal = p1_row_cells(g, ty, tx);
+  const int nreal = p1_row_cells<WSF>(g, ty, tx);
 #pragma unroll
   for (int dw = 0; dw < WSM; ++dw) sc[dw] = dw < nreal ? sc[dw] : no_cell();
 }
@@ -529,7 +533,7 @@ __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_scores_kernel(const
   if (t2 < 0 || t2 >= g.T) return;  // whole workgroup: frame outside the clip
   const int ty = (int)blockIdx.x / tiles_x, tx = (int)blockIdx.x % tiles_x;
   float sc[WSM];
-  p1_frame_scores(sm, q, k, flows, g, b, hd, t, dt, ty, tx, sc);
+  p1_frame_scores<0>(sm, q, k, flows, g, b, hd, t, dt, ty, tx, sc);
   // The scores of the tile's queries for this frame go through LDS (the
   // staging buffers are free once every thread is past the channel loop):
   // query j's ws^2 scores at sbuf[j * ws^2 ..], then copied to the workspace
@@ -571,6 +575,7 @@ __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_scores_kernel(const
 // cells above the tie plus the tied ones of smallest id make the frame's
 // top k.  Frames outside the clip contribute invalid candidates (-inf) in
 // id order, which matter only while fewer than k better entries are known.
+template <int WSF>
 __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_topk_kernel(const float* __restrict__ q,
                                                              const float* __restrict__ k,
                                                              const float* __restrict__ flows, Geo g, int tiles_x,
@@ -591,7 +596,8 @@ __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_topk_kernel(const f
   const int mh = ty * TQH + j / TQW, mw = tx * TQW + j % TQW;
   const bool inside = mh < g.nH && mw < g.nW;  // the same for the query's 16 lanes
   const int gb = (tid & 63) & ~15;             // the group's first lane in the wave
-  const int ncell = g.ws * g.ws;
+  const int wsk = WSF > 0 ? WSF : g.ws;  // window side (a constant when WSF > 0)
+  const int ncell = wsk * wsk;
   const int k1 = g.k - 1;
 
   unsigned long long L0 = 0ull, L1 = 0ull;  // list slots 2 dh and 2 dh + 1
@@ -601,9 +607,9 @@ __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_topk_kernel(const f
     const int cbase = (dt + g.wt) * ncell;
     float sc[WSM];
     if (t2 >= 0 && t2 < g.T) {
-      p1_frame_scores(sm, q, k, flows, g, b, hd, t, dt, ty, tx, sc);
+      p1_frame_scores<WSF>(sm, q, k, flows, g, b, hd, t, dt, ty, tx, sc);
     } else {
-      const int nreal = p1_row_cells(g, ty, tx);  // frame outside the clip: invalid cells
+      const int nreal = p1_row_cells<WSF>(g, ty, tx);  // frame outside the clip: invalid cells
 #pragma unroll
       for (int dw = 0; dw < WSM; ++dw) sc[dw] = dw < nreal ? -INFINITY : no_cell();
     }
@@ -724,7 +730,7 @@ __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_topk_kernel(const f
     // compaction into the query's slots (at most 32), id order
     int off = grp_excl_scan(__builtin_popcount(sel));
     const int ntot = min(nsel, LS);
-    const unsigned idb = (unsigned)(cbase + dh * g.ws);
+    const unsigned idb = (unsigned)(cbase + dh * wsk);
 #pragma unroll
     for (int dw = 0; dw < WSM; ++dw) {
       if ((sel >> dw) & 1u) {
@@ -770,7 +776,7 @@ __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_topk_kernel(const f
     // every candidate was ranked, so the k best are real candidates; the
     // clamp only keeps a placeholder id in bounds
     const int cid = min(max((int)~(unsigned)x, 0), g.ncand - 1);
-    const int dw = cid % g.ws, dhh = (cid / g.ws) % g.ws, dtt = cid / ncell - g.wt;
+    const int dw = cid % wsk, dhh = (cid / wsk) % wsk, dtt = cid / ncell - g.wt;
     float fh = 0.f, fw = 0.f;
     if (dtt != 0) {
       const long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dtt, g.wt)) * 2;
@@ -812,7 +818,12 @@ snls_status launch_search_p1_topk(const float* q, const float* k, const float* f
   if (ntile == 0 || g.rows == 0) return SNLS_OK;
   if (ntile > 0x7fffffffLL || (long long)g.B * g.HD * g.T > 65535) return SNLS_ERR_UNSUPPORTED;
   dim3 grid((unsigned)ntile, (unsigned)(g.B * g.HD * g.T));
-  hipLaunchKernelGGL(search_p1_topk_kernel, grid, dim3(p1::NT), 0, s, q, k, flows, g, tiles_x, dists, inds);
+  // a 15 x 15 window gets its own instance (window side and radius as
+  // immediates)
+  if (g.ws == p1::WSM)
+    hipLaunchKernelGGL(search_p1_topk_kernel<p1::WSM>, grid, dim3(p1::NT), 0, s, q, k, flows, g, tiles_x, dists, inds);
+  else
+    hipLaunchKernelGGL(search_p1_topk_kernel<0>, grid, dim3(p1::NT), 0, s, q, k, flows, g, tiles_x, dists, inds);
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
 }
 
