@@ -582,7 +582,9 @@ __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_topk_kernel(const f
                                                              float* __restrict__ dists, float* __restrict__ inds) {
   using namespace p1;
   __shared__ P1Smem sm;
-  __shared__ unsigned long long surv[NQ][LS];  // a frame's selected cells per query
+  // a frame's selected cells per query; the odd row pitch (LS + 1 entries)
+  // puts the four queries of a wave on different banks for the same slot
+  __shared__ unsigned long long surv[NQ][LS + 1];
 
   const int tid = threadIdx.x, j = tid / NR, dh = tid % NR;
   const int img = (int)blockIdx.y;  // (b, hd, t)
