@@ -161,6 +161,10 @@ def test_search_workspace(lib):
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(p1)) == rows1 * 676 * 4  # 675 padded to 676
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, stride0=2, ws=15, k=32))) == 0
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, stride0=2, ws=17, k=30))) == 0
+    # at query stride 1 too: the fused single-pixel kernel up to k = 32 (no
+    # workspace), the tiled scores above
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, ws=9, k=27))) == 0
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, ws=9, k=33))) == rows * 244 * 4
     # squared L2 (key stride 1): the scores, the key-norm terms, the query-norm
     # terms, five key pair planes and the query pixel-norm plane per frame and head
     plane = (rows * 28 * 4 + 255) // 256 * 256
