@@ -820,10 +820,12 @@ snls_status launch_search_p1_topk(const float* q, const float* k, const float* f
   if (ntile == 0 || g.rows == 0) return SNLS_OK;
   if (ntile > 0x7fffffffLL || (long long)g.B * g.HD * g.T > 65535) return SNLS_ERR_UNSUPPORTED;
   dim3 grid((unsigned)ntile, (unsigned)(g.B * g.HD * g.T));
-  // a 15 x 15 window gets its own instance (window side and radius as
-  // immediates)
+  // 15 x 15 and 9 x 9 windows get their own instances (window side and
+  // radius as immediates)
   if (g.ws == p1::WSM)
     hipLaunchKernelGGL(search_p1_topk_kernel<p1::WSM>, grid, dim3(p1::NT), 0, s, q, k, flows, g, tiles_x, dists, inds);
+  else if (g.ws == 9)
+    hipLaunchKernelGGL(search_p1_topk_kernel<9>, grid, dim3(p1::NT), 0, s, q, k, flows, g, tiles_x, dists, inds);
   else
     hipLaunchKernelGGL(search_p1_topk_kernel<0>, grid, dim3(p1::NT), 0, s, q, k, flows, g, tiles_x, dists, inds);
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
