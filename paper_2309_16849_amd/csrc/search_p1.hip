@@ -795,8 +795,12 @@ __global__ void __launch_bounds__(p1::NT, p1::WPE) search_p1_topk_kernel(const f
 
 // P = 1, key stride 1, inner product, ws <= 15 (any query stride).
 bool p1_supported(const Geo& g) {
+  // grid limits of both kernels: tiles in x, images (b, head, t) in y,
+  // frame steps in z; larger problems take another route
+  const long long ntile = (long long)((g.nW + p1::TQW - 1) / p1::TQW) * ((g.nH + p1::TQH - 1) / p1::TQH);
   return g.ps == 1 && g.s1 == 1.0f && g.dist == SNLS_DIST_PROD && g.ws <= p1::WSM && g.k >= 1 &&
-         (long long)(g.Ch + p1::CC) * g.HW * 4 < (1LL << 31);
+         (long long)(g.Ch + p1::CC) * g.HW * 4 < (1LL << 31) && ntile <= 0x7fffffffLL &&
+         (long long)g.B * g.HD * g.T <= 65535 && 2 * g.wt + 1 <= 65535;
 }
 
 // The fused kernel keeps at most 32 entries per query.
