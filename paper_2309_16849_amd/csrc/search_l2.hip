@@ -29,6 +29,13 @@
 // non-finite key value reaches exactly the positions whose taps read it.
 // A sixth plane holds |q(y,x)|^2 of the query video, so Qn is a sum of
 // P^2 plane values per query.
+//
+// At a key stride S_K != 1 the cells of a window have fractions of their
+// own, so G is formed per cell (l2_norms_cells_kernel): with n = floor(disp)
+// and the cell's weights, the ten terms above become ten box sums of the
+// planes over the query's in-frame patch pixels, each at the offset of its
+// term ((0|1, 0|1) for N, (0|1, 0) for R, (0, 0|1) for D, (0, 0) for X and
+// A), gathered in one pass over the (P+1) x (P+1) positions.
 #include "snls_internal.h"
 
 namespace snls {
@@ -292,6 +299,99 @@ __global__ void __launch_bounds__(l2n::NT, 3) l2_norms_kernel(const float* __res
   }
 }
 
+// G of every cell for a key stride S_K != 1: one thread per (query, cell)
+// of one frame step (grid y = dt + wt), consecutive threads the cells of a
+// query; Qn by the first cell's thread of the query frame.
+__global__ void __launch_bounds__(256) l2_norms_cells_kernel(const float* __restrict__ planes,
+                                                             const float* __restrict__ flows, Geo g,
+                                                             float* __restrict__ G, int pitch,
+                                                             float* __restrict__ Qn) {
+  const int ncf = g.ws * g.ws;  // cells per frame step
+  const long long e = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= g.rows * ncf) return;
+  const long long row = e / ncf;
+  const int cell = (int)(e - row * ncf);
+  const int dt = (int)blockIdx.y - g.wt;
+  const int mw = (int)(row % g.nW);
+  long long rr = row / g.nW;
+  const int mh = (int)(rr % g.nH);
+  rr /= g.nH;
+  const int t = (int)(rr % g.T);
+  rr /= g.T;
+  const int hd = (int)(rr % g.HD);
+  const int b = (int)(rr / g.HD);
+  const int t2 = t + dt;
+  const int h = mh * g.s0, w = mw * g.s0;
+  // patch rows and columns whose query pixel is inside the frame
+  const int ip0 = max(0, -h - g.lo), ip1 = min(g.ps - 1, g.H - 1 - h - g.lo);
+  const int jp0 = max(0, -w - g.lo), jp1 = min(g.ps - 1, g.W - 1 - w - g.lo);
+  if (dt == 0 && cell == 0) {
+    const float* qpl = planes + ((((long long)b * g.T + t) * g.HD + hd) * NPLANE + NKP) * g.HW;
+    float sq = 0.f;
+    for (int ip = ip0; ip <= ip1; ++ip)
+      for (int jp = jp0; jp <= jp1; ++jp) sq += qpl[(long long)(h + g.lo + ip) * g.W + w + g.lo + jp];
+    Qn[row] = sq;
+  }
+  if (t2 < 0 || t2 >= g.T) return;  // candidates of frames outside the clip rank as invalid
+  float fh = 0.f, fw = 0.f;
+  if (dt != 0) {
+    const long long base = (((long long)b * g.T + t) * g.nslot + flow_slot(dt, g.wt)) * 2;
+    const long long pix = (long long)h * g.W + w;
+    fh = flows[base * g.HW + pix];
+    fw = flows[(base + 1) * g.HW + pix];
+  }
+  float gsum = 0.f;
+  // non-finite or absurd offsets: their candidates are invalid (the inner
+  // product pass scores them so); any G value does
+  if (fabsf(fh) < kFarDisp && fabsf(fw) < kFarDisp) {
+    const int dh = cell / g.ws, dw = cell - (cell / g.ws) * g.ws;
+    const float disp_h = cand_disp(fh, g.s1, dh, g.r), disp_w = cand_disp(fw, g.s1, dw, g.r);
+    const float fly = floorf(disp_h), flx = floorf(disp_w);
+    const float ay = disp_h - fly, ax = disp_w - flx;
+    const int y0 = h + g.lo + (int)fly, x0 = w + g.lo + (int)flx;  // tap (0, 0) of patch pixel (0, 0)
+    const float* kb = planes + (((long long)b * g.T + t2) * g.HD + hd) * NPLANE * g.HW;
+    // box sums over the in-frame patch pixels, at the offsets of the terms
+    float n00 = 0.f, n01 = 0.f, n10 = 0.f, n11 = 0.f, r0 = 0.f, r1 = 0.f, d0 = 0.f, d1 = 0.f, xs = 0.f, as = 0.f;
+    for (int a = ip0; a <= ip1 + 1; ++a) {
+      const int y = y0 + a;
+      const bool yin = y >= 0 && y < g.H;
+      // row a is patch row a for the terms at row offset 0, patch row a - 1
+      // for those at row offset 1 (and likewise for columns below)
+      const bool ra = a <= ip1, rb = a > ip0;
+      for (int c = jp0; c <= jp1 + 1; ++c) {
+        const int x = x0 + c;
+        if (!yin || x < 0 || x >= g.W) continue;  // every plane reads 0 outside the frame
+        const bool ca = c <= jp1, cb = c > jp0;
+        const float* pp = kb + (long long)y * g.W + x;
+        const float vn = pp[0];
+        n00 += ra && ca ? vn : 0.f;
+        n01 += ra && cb ? vn : 0.f;
+        n10 += rb && ca ? vn : 0.f;
+        n11 += rb && cb ? vn : 0.f;
+        if (ca) {
+          const float vr = pp[g.HW];
+          r0 += ra ? vr : 0.f;
+          r1 += rb ? vr : 0.f;
+        }
+        if (ra) {
+          const float vd = pp[2 * (long long)g.HW];
+          d0 += ca ? vd : 0.f;
+          d1 += cb ? vd : 0.f;
+          if (ca) {
+            xs += pp[3 * (long long)g.HW];
+            as += pp[4 * (long long)g.HW];
+          }
+        }
+      }
+    }
+    const float w00 = (1.f - ay) * (1.f - ax), w01 = (1.f - ay) * ax, w10 = ay * (1.f - ax), w11 = ay * ax;
+    gsum = w00 * w00 * n00 + w01 * w01 * n01 + w10 * w10 * n10 + w11 * w11 * n11 + 2.f * w00 * w01 * r0 +
+           2.f * w10 * w11 * r1 + 2.f * w00 * w10 * d0 + 2.f * w01 * w11 * d1 + 2.f * w00 * w11 * xs +
+           2.f * w01 * w10 * as;
+  }
+  G[row * pitch + (dt + g.wt) * ncf + cell] = gsum;
+}
+
 size_t l2_planes_bytes(const Geo& g) {
   return ((size_t)NPLANE * g.B * g.T * g.HD * (size_t)g.HW * sizeof(float) + 255) & ~(size_t)255;
 }
@@ -304,6 +404,15 @@ snls_status launch_l2_norms(const float* q, const float* k, const float* flows, 
   if (ntile > 0x7fffffffLL || (long long)g.B * g.HD * g.T > 65535 || 2 * g.wt + 1 > 65535) return SNLS_ERR_UNSUPPORTED;
   const dim3 pgrid((unsigned)((g.HW + 255) / 256), (unsigned)(g.B * g.T * g.HD));
   hipLaunchKernelGGL(l2_pair_planes_kernel, pgrid, dim3(256), 0, s, q, k, g, planes);
+  if (g.s1 != 1.0f) {
+    // per-cell fractions: G cell by cell
+    const long long nth = g.rows * (long long)(g.ws * g.ws);
+    const long long nblk = (nth + 255) / 256;
+    if (nblk > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
+    dim3 cgrid((unsigned)nblk, (unsigned)(2 * g.wt + 1));
+    hipLaunchKernelGGL(l2_norms_cells_kernel, cgrid, dim3(256), 0, s, planes, flows, g, G, pitch, Qn);
+    return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
+  }
   dim3 grid((unsigned)ntile, (unsigned)(g.B * g.HD * g.T), (unsigned)(2 * g.wt + 1));
   hipLaunchKernelGGL(l2_norms_kernel, grid, dim3(l2n::NT), 0, s, q, planes, flows, g, tiles_x, G, pitch, Qn);
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;

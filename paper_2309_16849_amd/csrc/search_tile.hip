@@ -923,7 +923,7 @@ __global__ void __launch_bounds__(wtk::WAVES * 64) wave_topk_kernel(const float*
 // The tiled path handles any S_Q, P <= 7, Ws <= 9 with the inner product
 // (S_K <= 1) or the squared L2 distance (S_K = 1).
 bool tile_supported(const Geo& g) {
-  const bool dist_ok = g.dist == SNLS_DIST_PROD ? g.s1 > 0.f && g.s1 <= 1.0f : g.s1 == 1.0f;
+  const bool dist_ok = g.s1 > 0.f && g.s1 <= 1.0f;  // both distances (L2: norm terms per cell unless S_K = 1)
   return dist_ok && g.ps <= 7 && g.ws <= tile::WSMAX && g.W >= 4 && g.k >= 1 &&
          (long long)g.Ch * g.HW * 4 < (1LL << 31);
 }

@@ -142,17 +142,15 @@ def test_aggregate_and_backward_validation(lib):
 
 
 def test_search_workspace(lib):
-    """The tiled top-k path (ps <= 7, ws <= 9, any stride0; inner product with
-    stride1 <= 1, squared L2 with stride1 = 1) scores every candidate into the
-    workspace; other paths need none."""
+    """The tiled top-k path (ps <= 7, ws <= 9, any stride0, stride1 <= 1)
+    scores every candidate into the workspace; other paths need none."""
     prm = _params()
     rows, ncand = 1 * 2 * 3 * 16 * 17, 3 * 3 * 3
     need = lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(prm))
     assert need == rows * ((ncand + 3) // 4 * 4) * 4  # rows padded to a multiple of 4 candidates
     # query stride 2: a query grid of 8 x 9
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(stride0=2))) == 1 * 2 * 3 * 8 * 9 * 28 * 4
-    for kw in (dict(k=0), dict(dist_type=1, stride1=0.5), dict(stride1=1.5), dict(ps=9),
-               dict(ws=11, k=4)):
+    for kw in (dict(k=0), dict(stride1=1.5), dict(ps=9), dict(ws=11, k=4)):
         assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(**kw))) == 0, kw
     # single-pixel patches at query stride 2: the scores of every candidate
     # for k above 32; up to 32 the selection runs inside the scoring kernel
@@ -171,6 +169,9 @@ def test_search_workspace(lib):
     a256 = lambda n: (n + 255) // 256 * 256
     pairs = a256(6 * 1 * 3 * 2 * 16 * 17 * 4)
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(dist_type=1))) == \
+        2 * plane + a256(rows * 4) + pairs
+    # the same at a fractional key stride (norm terms per cell, same planes)
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(dist_type=1, stride1=0.5))) == \
         2 * plane + a256(rows * 4) + pairs
     assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, None, BIG, None) == B.SNLS_ERR_WORKSPACE
     assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, FAKE, need - 1,

@@ -381,11 +381,20 @@ L2_TILE_CASES = [
     # products, ranked by the squared L2 distance
     (small_params(T=3, C=8, H=26, W=56, ws=9, wt=1, ps=7, k=10, dist_type=1), "split"),
     (small_params(T=3, C=8, H=64, W=40, ws=9, wt=1, ps=7, k=10, dist_type=1), "vspread"),
+    # fractional key strides: the norm terms cell by cell (each cell its own
+    # bilinear fractions), border queries, every patch size class
+    (small_params(T=3, C=8, H=23, W=31, ws=9, wt=1, ps=7, k=10, dist_type=1, stride1=0.5), "frac"),
+    (small_params(T=3, C=12, HD=2, H=21, W=26, ws=7, wt=1, ps=5, k=12, dist_type=1, stride1=0.75), "edge"),
+    (small_params(T=2, C=5, H=17, W=19, ws=5, wt=1, ps=3, k=7, dist_type=1, stride1=0.3), "smooth"),
+    (small_params(T=2, C=4, H=13, W=16, ws=9, wt=1, ps=1, k=6, dist_type=1, stride1=0.25), "int"),
+    (small_params(T=3, C=8, H=25, W=30, ws=9, wt=1, ps=7, k=10, dist_type=1, stride1=0.5), "far"),
+    (small_params(T=3, C=16, H=33, W=35, ws=9, wt=1, ps=7, k=10, dist_type=1, stride0=2, stride1=0.5), "wide"),
 ]
 
 
 @pytest.mark.parametrize("case", range(len(L2_TILE_CASES)),
-                         ids=["l%d-ws%d-ps%d-%s" % (i, p["ws"], p["ps"], kd) for i, (p, kd) in enumerate(L2_TILE_CASES)])
+                         ids=["l%d-ws%d-ps%d-sk%g-%s" % (i, p["ws"], p["ps"], p["stride1"], kd)
+                              for i, (p, kd) in enumerate(L2_TILE_CASES)])
 def test_tiled_search_l2(dev, case):
     p, kind = L2_TILE_CASES[case]
     r = np.random.default_rng(8500 + case)
