@@ -61,21 +61,24 @@ constexpr int KP = 45;                  // K row pitch (odd: spreads the 16 rows
 constexpr int QP = 21;                  // q row pitch (odd)
 constexpr int NIT = 2;                  // staging items (4 columns of one row) per thread and chunk
 constexpr int MAXBLK = 5;               // shift-column blocks: union width <= 30
-constexpr int WSMAX = 9;
-constexpr int WP = WSMAX + 2;           // window-table pitch (shifts floor(disp_0) .. floor(disp_last) + 1)
-constexpr int WIN = WP * WP;
+constexpr int WSMAX = 9;                // window side of the common instances
+constexpr int WSBIG = 15;               // ... and of the P = 7 instance for larger windows
+// window-table pitch for windows up to WSM (shifts floor(disp_0) ..
+// floor(disp_last) + 1) and the table of one query
+constexpr int wpitch(int WSM) { return WSM + 2; }
+constexpr int wtable(int WSM) { return wpitch(WSM) * wpitch(WSM); }
 
 // Staging buffers (double-buffered chunks of CC channels).
 constexpr int KST_F = (CC * KR * KP + 63) / 64 * 64;     // 6528 floats
 constexpr int QST_F = (CC * HROWS * QP + 63) / 64 * 64;  // 1344
 
 
-template <int PS>
+template <int PS, int WSM>
 struct Smem {
   static constexpr int QN = (HROWS - PS + 1) * TQW;  // queries per tile
   float kst[2][KST_F];  // K union region chunks (double buffer)
   float qst[2][QST_F];  // q halo chunks
-  float bw[QN * WIN];   // per-query window of box sums
+  float bw[QN * wtable(WSM)];  // per-query window of box sums
   int qlo_h[QN], qlo_w[QN];  // smallest integer shift of the query's window (table origin)
   float qf_h[QN], qf_w[QN];  // the offset itself
   int uni[4];                // min N_h, max N_h, min N_w, max N_w
@@ -174,7 +177,8 @@ SNLS_DEV void box_cols(float (&a)[L][S]) {
   }
 }
 
-template <int PS>
+// WSM: the largest window side of the instance (the window tables' size).
+template <int PS, int WSM>
 __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(const float* __restrict__ q,
                                                                              const float* __restrict__ k,
                                                                              const float* __restrict__ flows, Geo g,
@@ -187,8 +191,10 @@ __global__ void __launch_bounds__(tile::NTHREADS) search_tile_scores_kernel(cons
   constexpr int NQIT = CC * HROWS * QC4;  // q items per chunk (a multiple of 64)
   static_assert(NQIT % 64 == 0 && NQIT <= NTHREADS, "q items fill whole waves of item slot 1");
   static_assert(CC * KR * ((KP + 3) / 4) <= 2 * NTHREADS - NQIT, "every K item has a slot");
-  constexpr int QN = Smem<PS>::QN;
-  __shared__ Smem<PS> sm;
+  constexpr int QN = Smem<PS, WSM>::QN;
+  constexpr int WP = wpitch(WSM), WIN = wtable(WSM);
+  static_assert(sizeof(Smem<PS, WSM>) <= 160 * 1024, "the LDS of one CU");
+  __shared__ Smem<PS, WSM> sm;
 
   const int tid = threadIdx.x;
   const int lane16 = tid & 15;
@@ -924,7 +930,11 @@ __global__ void __launch_bounds__(wtk::WAVES * 64) wave_topk_kernel(const float*
 // (S_K <= 1) or the squared L2 distance (S_K = 1).
 bool tile_supported(const Geo& g) {
   const bool dist_ok = g.s1 > 0.f && g.s1 <= 1.0f;  // both distances (L2: norm terms per cell unless S_K = 1)
-  return dist_ok && g.ps <= 7 && g.ws <= tile::WSMAX && g.W >= 4 && g.k >= 1 &&
+  // windows above 9 only at P = 7 (its 80-query tile keeps 15 x 15 windows'
+  // tables within the LDS; smaller patches make taller tiles) and for the
+  // inner product (the L2 norm-term grids are sized for windows up to 9)
+  const bool ws_ok = g.ws <= tile::WSMAX || (g.ws <= tile::WSBIG && g.ps == 7 && g.dist == SNLS_DIST_PROD);
+  return dist_ok && g.ps <= 7 && ws_ok && g.W >= 4 && g.k >= 1 &&
          (long long)g.Ch * g.HW * 4 < (1LL << 31);
 }
 
@@ -999,11 +1009,15 @@ snls_status launch_search_tile(const float* q, const float* k, const float* flow
   if (nwg == 0) return SNLS_OK;
   if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
   dim3 grid((unsigned)nwg), block(tile::NTHREADS);
-  switch (g.ps) {
+  switch (g.ws > tile::WSMAX ? 0 : g.ps) {
+    case 0:  // P = 7 with a window above 9 (tile_supported)
+      hipLaunchKernelGGL((search_tile_scores_kernel<7, tile::WSBIG>), grid, block, 0, s, q, k, flows, g, tiles_x,
+                         tiles_y, scores, tile_ws_pitch(g));
+      break;
 #define SNLS_TILE_CASE(P)                                                                                       \
   case P:                                                                                                       \
-    hipLaunchKernelGGL((search_tile_scores_kernel<P>), grid, block, 0, s, q, k, flows, g, tiles_x, tiles_y,    \
-                       scores, tile_ws_pitch(g));                                                               \
+    hipLaunchKernelGGL((search_tile_scores_kernel<P, tile::WSMAX>), grid, block, 0, s, q, k, flows, g, tiles_x, \
+                       tiles_y, scores, tile_ws_pitch(g));                                                      \
     break;
     SNLS_TILE_CASE(1)
     SNLS_TILE_CASE(2)

@@ -170,6 +170,9 @@ def test_search_workspace(lib):
     pairs = a256(6 * 1 * 3 * 2 * 16 * 17 * 4)
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(dist_type=1))) == \
         2 * plane + a256(rows * 4) + pairs
+    # windows above 9: tiled at P = 7 for the inner product, else none
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=7))) == rows * 364 * 4
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=7, dist_type=1))) == 0
     # the same at a fractional key stride (norm terms per cell, same planes)
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(dist_type=1, stride1=0.5))) == \
         2 * plane + a256(rows * 4) + pairs

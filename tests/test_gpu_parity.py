@@ -273,6 +273,12 @@ TILE_CASES = _tile_cases() + [
     (small_params(T=3, C=8, H=64, W=40, ws=9, wt=1, ps=7, k=10), "vspread"),
     (small_params(T=2, C=8, H=61, W=33, ws=5, wt=1, ps=3, k=8, stride1=0.5), "vspread"),
     (small_params(T=3, C=8, H=30, W=56, ws=9, wt=1, ps=5, k=10), "split"),
+    # windows above 9 at P = 7 (the 15 x 15 window-table instance): every
+    # window side class, key strides 1 and 1/2, strided queries, k past 16
+    (small_params(T=3, C=16, H=29, W=33, ws=15, wt=1, ps=7, k=10), "smooth"),
+    (small_params(T=2, C=8, H=24, W=27, ws=11, wt=1, ps=7, k=20, stride1=0.5), "frac"),
+    (small_params(T=2, C=12, H=31, W=26, ws=13, wt=0, ps=7, k=12, stride0=2), "edge"),
+    (small_params(T=3, C=8, H=20, W=40, ws=15, wt=1, ps=7, k=10), "wide"),
 ]
 TILE_IDS = ["t%d-ws%d-wt%d-ps%d-sk%g-k%d-%s" % (i, p["ws"], p["wt"], p["ps"], p["stride1"], p["k"], kd)
             for i, (p, kd) in enumerate(TILE_CASES)]
