@@ -31,7 +31,8 @@
 // P^2 plane values per query.
 //
 // At a key stride S_K != 1 the cells of a window have fractions of their
-// own, so G is formed per cell (l2_norms_cells_kernel): with n = floor(disp)
+// own, so G is formed per cell (l2_norms_cells_kernel; also for windows
+// larger than the grids of l2_norms_kernel): with n = floor(disp)
 // and the cell's weights, the ten terms above become ten box sums of the
 // planes over the query's in-frame patch pixels, each at the offset of its
 // term ((0|1, 0|1) for N, (0|1, 0) for R, (0, 0|1) for D, (0, 0) for X and
@@ -404,8 +405,8 @@ snls_status launch_l2_norms(const float* q, const float* k, const float* flows, 
   if (ntile > 0x7fffffffLL || (long long)g.B * g.HD * g.T > 65535 || 2 * g.wt + 1 > 65535) return SNLS_ERR_UNSUPPORTED;
   const dim3 pgrid((unsigned)((g.HW + 255) / 256), (unsigned)(g.B * g.T * g.HD));
   hipLaunchKernelGGL(l2_pair_planes_kernel, pgrid, dim3(256), 0, s, q, k, g, planes);
-  if (g.s1 != 1.0f) {
-    // per-cell fractions: G cell by cell
+  if (g.s1 != 1.0f || g.ws > l2n::WSMAX) {
+    // per-cell fractions, or windows past the grids below: G cell by cell
     const long long nth = g.rows * (long long)(g.ws * g.ws);
     const long long nblk = (nth + 255) / 256;
     if (nblk > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;

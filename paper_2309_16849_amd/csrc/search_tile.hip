@@ -662,7 +662,8 @@ __global__ void __launch_bounds__(tk::ROWS) tile_topk_kernel(const float* __rest
   const int lo = (max(0, t - g.wt) - t + g.wt) * ncell, hi = (min(g.T - 1, t + g.wt) - t + g.wt + 1) * ncell;
   float ts = -INFINITY;  // threshold entry: candidates ranking after it are skipped
   int ti = 0x7fffffff;
-  if (g.k <= ncell) {
+  // (the spiral covers the central 9 x 9 cells: a bound needs k of them)
+  if (g.k <= ncell && g.k <= 81) {
     ts = INFINITY;
     ti = -1;
     for (int i = 0, n = 0; n < g.k && i < 81; ++i) {
@@ -930,10 +931,10 @@ __global__ void __launch_bounds__(wtk::WAVES * 64) wave_topk_kernel(const float*
 // (S_K <= 1) or the squared L2 distance (S_K = 1).
 bool tile_supported(const Geo& g) {
   const bool dist_ok = g.s1 > 0.f && g.s1 <= 1.0f;  // both distances (L2: norm terms per cell unless S_K = 1)
-  // windows above 9 only at P = 7 (its 80-query tile keeps 15 x 15 windows'
-  // tables within the LDS; smaller patches make taller tiles) and for the
-  // inner product (the L2 norm-term grids are sized for windows up to 9)
-  const bool ws_ok = g.ws <= tile::WSMAX || (g.ws <= tile::WSBIG && g.ps == 7 && g.dist == SNLS_DIST_PROD);
+  // windows above 9 only at P = 7: its 80-query tile keeps 15 x 15 windows'
+  // tables within the LDS (smaller patches make taller tiles); their L2 norm
+  // terms are formed cell by cell
+  const bool ws_ok = g.ws <= tile::WSMAX || (g.ws <= tile::WSBIG && g.ps == 7);
   return dist_ok && g.ps <= 7 && ws_ok && g.W >= 4 && g.k >= 1 &&
          (long long)g.Ch * g.HW * 4 < (1LL << 31);
 }

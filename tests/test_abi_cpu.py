@@ -170,9 +170,13 @@ def test_search_workspace(lib):
     pairs = a256(6 * 1 * 3 * 2 * 16 * 17 * 4)
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(dist_type=1))) == \
         2 * plane + a256(rows * 4) + pairs
-    # windows above 9: tiled at P = 7 for the inner product, else none
+    # windows above 9: tiled at P = 7 (scores; for L2 also the norm terms and
+    # planes), none at other patch sizes
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=7))) == rows * 364 * 4
-    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=7, dist_type=1))) == 0
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=5))) == 0
+    plane11 = (rows * 364 * 4 + 255) // 256 * 256
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=7, dist_type=1))) == \
+        2 * plane11 + (rows * 4 + 255) // 256 * 256 + (6 * 1 * 3 * 2 * 16 * 17 * 4 + 255) // 256 * 256
     # the same at a fractional key stride (norm terms per cell, same planes)
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(dist_type=1, stride1=0.5))) == \
         2 * plane + a256(rows * 4) + pairs

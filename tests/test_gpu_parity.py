@@ -279,6 +279,8 @@ TILE_CASES = _tile_cases() + [
     (small_params(T=2, C=8, H=24, W=27, ws=11, wt=1, ps=7, k=20, stride1=0.5), "frac"),
     (small_params(T=2, C=12, H=31, W=26, ws=13, wt=0, ps=7, k=12, stride0=2), "edge"),
     (small_params(T=3, C=8, H=20, W=40, ws=15, wt=1, ps=7, k=10), "wide"),
+    # k above the 81 cells of the top-k's seeding spiral
+    (small_params(T=2, C=8, H=21, W=23, ws=15, wt=1, ps=7, k=100), "smooth"),
 ]
 TILE_IDS = ["t%d-ws%d-wt%d-ps%d-sk%g-k%d-%s" % (i, p["ws"], p["wt"], p["ps"], p["stride1"], p["k"], kd)
             for i, (p, kd) in enumerate(TILE_CASES)]
@@ -395,6 +397,10 @@ L2_TILE_CASES = [
     (small_params(T=2, C=4, H=13, W=16, ws=9, wt=1, ps=1, k=6, dist_type=1, stride1=0.25), "int"),
     (small_params(T=3, C=8, H=25, W=30, ws=9, wt=1, ps=7, k=10, dist_type=1, stride1=0.5), "far"),
     (small_params(T=3, C=16, H=33, W=35, ws=9, wt=1, ps=7, k=10, dist_type=1, stride0=2, stride1=0.5), "wide"),
+    # windows above 9 at P = 7 (15 x 15 window tables, norm terms per cell)
+    (small_params(T=3, C=8, H=27, W=30, ws=15, wt=1, ps=7, k=10, dist_type=1), "smooth"),
+    (small_params(T=2, C=8, H=22, W=25, ws=11, wt=1, ps=7, k=12, dist_type=1, stride1=0.5), "frac"),
+    (small_params(T=2, C=8, H=19, W=22, ws=13, wt=1, ps=7, k=128, dist_type=1), "smooth"),
 ]
 
 
