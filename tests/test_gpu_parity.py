@@ -328,6 +328,57 @@ def test_tiled_search_topk(dev, case):
     compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
 
 
+# The tiled route at P = 7, S_Q = 1 with 64 channels per head runs its
+# correlations on the matrix cores (10 x 10 query tiles): unions of up to
+# 17 shift columns (two 16-column key blocks), 18-25 (three blocks), wider
+# ones scored directly; tall unions in several rounds of shift rows; two
+# heads; key strides below 1; L2; windows of 5 to 9.
+MFMA_CASES = [
+    (small_params(T=3, C=64, H=30, W=33, ws=9, wt=1, ps=7, k=10), "smooth"),
+    (small_params(T=3, C=64, H=27, W=31, ws=9, wt=1, ps=7, k=10), "wide"),
+    (small_params(T=2, C=128, HD=2, H=23, W=26, ws=7, wt=1, ps=7, k=12, stride1=0.5), "frac"),
+    (small_params(T=3, C=64, H=21, W=37, ws=9, wt=1, ps=7, k=20, dist_type=1), "edge"),
+    (small_params(T=2, C=64, H=64, W=24, ws=9, wt=1, ps=7, k=10), "vspread"),
+    (small_params(T=2, C=64, H=20, W=22, ws=9, wt=1, ps=7, k=10), "far"),
+    (small_params(T=3, C=64, H=26, W=29, ws=5, wt=1, ps=7, k=8, stride1=0.3), "int"),
+    (small_params(B=2, T=3, C=64, H=19, W=41, ws=9, wt=2, ps=7, k=16, dist_type=1, stride1=0.75), "split"),
+]
+
+
+@pytest.mark.parametrize("case", range(len(MFMA_CASES)),
+                         ids=["m%d-ws%d-hd%d-sk%g-d%d-%s" % (i, p["ws"], p["HD"], p["stride1"], p["dist_type"], kd)
+                              for i, (p, kd) in enumerate(MFMA_CASES)])
+def test_mfma_tiled_search(dev, case):
+    p, kind = MFMA_CASES[case]
+    r = np.random.default_rng(9500 + case)
+    shp = (p["B"], p["T"], p["C"], p["H"], p["W"])
+    q = r.standard_normal(shp, dtype=np.float32)
+    k = (q + 0.5 * r.standard_normal(shp, dtype=np.float32)).astype(np.float32) if case % 2 else \
+        r.standard_normal(shp, dtype=np.float32)
+    flows = _tile_flows(p, kind, r)
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    torch.cuda.synchronize()
+    res = oracle.search(q, k, flows, p)
+    compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
+
+
+def test_mfma_tiled_nan_features(dev):
+    """NaN feature values away from the borders on the matrix-core route:
+    every candidate whose patch reads one is invalid, as in the oracle."""
+    p = small_params(T=3, C=64, H=34, W=36, ws=9, wt=1, ps=7, k=10)
+    r = np.random.default_rng(9600)
+    q, k, v, flows = _inputs(p, 9601)
+    m = 4 + 6
+    for arr in (q, k):
+        for _ in range(4):
+            arr[0, r.integers(0, 3), r.integers(0, 64), r.integers(m, 34 - m), r.integers(m, 36 - m)] = np.nan
+    gd, gi = B.snls_search(_d(q, dev), _d(k, dev), _d(flows, dev), p)
+    torch.cuda.synchronize()
+    assert not np.isnan(_h(gd)).any()
+    res = oracle.search(q, k, flows, p)
+    compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
+
+
 # Task packing of the tiled scores kernel: every tile of every frame gets
 # offsets whose integer parts span a chosen number of rows and columns, so
 # the union of its windows is 10..22 shift rows by 10..26 shift columns.
