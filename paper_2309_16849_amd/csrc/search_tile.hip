@@ -1010,14 +1010,7 @@ snls_status launch_search_tile(const float* q, const float* k, const float* flow
   if (nwg == 0) return SNLS_OK;
   if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
   dim3 grid((unsigned)nwg), block(tile::NTHREADS);
-  // P = 7 at S_Q = 1 with 64 channels per head: the correlations on the matrix cores
-  const int sw = mfma_scores_supported(g) ? -1 : (g.ws > tile::WSMAX ? 0 : g.ps);
-  switch (sw) {
-    case -1: {
-      const snls_status st = launch_mfma_scores(q, k, flows, g, scores, tile_ws_pitch(g), s);
-      if (st != SNLS_OK) return st;
-      break;
-    }
+  switch (g.ws > tile::WSMAX ? 0 : g.ps) {
     case 0:  // P = 7 with a window above 9 (tile_supported)
       hipLaunchKernelGGL((search_tile_scores_kernel<7, tile::WSBIG>), grid, block, 0, s, q, k, flows, g, tiles_x,
                          tiles_y, scores, tile_ws_pitch(g));

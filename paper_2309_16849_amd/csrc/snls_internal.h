@@ -84,11 +84,6 @@ snls_status launch_search_topk_direct(const float* q, const float* k, const floa
                                       float* dists, float* inds, hipStream_t s);
 snls_status launch_search_tile(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                                float* inds, float* scores, hipStream_t s);
-// Scores of the tiled route on the matrix cores (P = 7, S_Q = 1, 64
-// channels per head, Ws <= 9), written to the same workspace rows.
-bool mfma_scores_supported(const Geo& g);
-snls_status launch_mfma_scores(const float* q, const float* k, const float* flows, const Geo& g, float* scores,
-                               int pitch, hipStream_t s);
 snls_status launch_search_p1(const float* q, const float* k, const float* flows, const Geo& g, float* dists,
                              float* inds, float* scores, hipStream_t s);
 snls_status launch_search_p1_scores(const float* q, const float* k, const float* flows, const Geo& g, float* scores,

@@ -328,12 +328,11 @@ def test_tiled_search_topk(dev, case):
     compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
 
 
-# The tiled route at P = 7, S_Q = 1 with 64 channels per head runs its
-# correlations on the matrix cores (10 x 10 query tiles): unions of up to
-# 17 shift columns (two 16-column key blocks), 18-25 (three blocks), wider
-# ones scored directly; tall unions in several rounds of shift rows; two
-# heads; key strides below 1; L2; windows of 5 to 9.
-MFMA_CASES = [
+# The tiled route at P = 7, S_Q = 1 with 64 channels per head (the 480x854
+# workload's channel count: 16 chunks of 4 channels): smooth, wide (several
+# shift-column blocks), far (scored directly) and tall (several rounds of
+# shift rows) unions; two heads; key strides below 1; L2; windows of 5 to 9.
+C64_CASES = [
     (small_params(T=3, C=64, H=30, W=33, ws=9, wt=1, ps=7, k=10), "smooth"),
     (small_params(T=3, C=64, H=27, W=31, ws=9, wt=1, ps=7, k=10), "wide"),
     (small_params(T=2, C=128, HD=2, H=23, W=26, ws=7, wt=1, ps=7, k=12, stride1=0.5), "frac"),
@@ -345,11 +344,11 @@ MFMA_CASES = [
 ]
 
 
-@pytest.mark.parametrize("case", range(len(MFMA_CASES)),
-                         ids=["m%d-ws%d-hd%d-sk%g-d%d-%s" % (i, p["ws"], p["HD"], p["stride1"], p["dist_type"], kd)
-                              for i, (p, kd) in enumerate(MFMA_CASES)])
-def test_mfma_tiled_search(dev, case):
-    p, kind = MFMA_CASES[case]
+@pytest.mark.parametrize("case", range(len(C64_CASES)),
+                         ids=["c%d-ws%d-hd%d-sk%g-d%d-%s" % (i, p["ws"], p["HD"], p["stride1"], p["dist_type"], kd)
+                              for i, (p, kd) in enumerate(C64_CASES)])
+def test_tiled_search_c64(dev, case):
+    p, kind = C64_CASES[case]
     r = np.random.default_rng(9500 + case)
     shp = (p["B"], p["T"], p["C"], p["H"], p["W"])
     q = r.standard_normal(shp, dtype=np.float32)
@@ -362,8 +361,8 @@ def test_mfma_tiled_search(dev, case):
     compare_topk(_h(gd).reshape(-1, p["k"]), _h(gi).reshape(-1, p["k"], 3), res, p["k"])
 
 
-def test_mfma_tiled_nan_features(dev):
-    """NaN feature values away from the borders on the matrix-core route:
+def test_tiled_nan_features_c64(dev):
+    """NaN feature values away from the borders with 64 channels (P = 7):
     every candidate whose patch reads one is invalid, as in the oracle."""
     p = small_params(T=3, C=64, H=34, W=36, ws=9, wt=1, ps=7, k=10)
     r = np.random.default_rng(9600)
