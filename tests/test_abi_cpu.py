@@ -147,34 +147,34 @@ def test_search_workspace(lib):
     prm = _params()
     rows, ncand = 1 * 2 * 3 * 16 * 17, 3 * 3 * 3
     need = lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(prm))
-    assert need == rows * ((ncand + 3) // 4 * 4) * 4  # rows padded to a multiple of 4 candidates
+    assert need == rows * ((ncand + 31) // 32 * 32) * 4  # rows padded to a multiple of 32 candidates
     # query stride 2: a query grid of 8 x 9
-    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(stride0=2))) == 1 * 2 * 3 * 8 * 9 * 28 * 4
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(stride0=2))) == 1 * 2 * 3 * 8 * 9 * 32 * 4
     for kw in (dict(k=0), dict(stride1=1.5), dict(ps=9), dict(ws=11, k=4)):
         assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(**kw))) == 0, kw
     # single-pixel patches at query stride 2: the scores of every candidate
     # for k above 32; up to 32 the selection runs inside the scoring kernel
     p1 = _params(ps=1, stride0=2, ws=15, k=33)
     rows1 = 1 * 2 * 3 * 8 * 9
-    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(p1)) == rows1 * 676 * 4  # 675 padded to 676
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(p1)) == rows1 * 704 * 4  # 675 padded to 704
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, stride0=2, ws=15, k=32))) == 0
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, stride0=2, ws=17, k=30))) == 0
     # at query stride 1 too: the fused single-pixel kernel up to k = 32 (no
     # workspace), the tiled scores above
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, ws=9, k=27))) == 0
-    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, ws=9, k=33))) == rows * 244 * 4
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ps=1, ws=9, k=33))) == rows * 256 * 4
     # squared L2 (key stride 1): the scores, the key-norm terms, the query-norm
     # terms, five key pair planes and the query pixel-norm plane per frame and head
-    plane = (rows * 28 * 4 + 255) // 256 * 256
+    plane = (rows * 32 * 4 + 255) // 256 * 256
     a256 = lambda n: (n + 255) // 256 * 256
     pairs = a256(6 * 1 * 3 * 2 * 16 * 17 * 4)
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(dist_type=1))) == \
         2 * plane + a256(rows * 4) + pairs
     # windows above 9: tiled at P = 7 (scores; for L2 also the norm terms and
     # planes), none at other patch sizes
-    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=7))) == rows * 364 * 4
+    assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=7))) == rows * 384 * 4
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=5))) == 0
-    plane11 = (rows * 364 * 4 + 255) // 256 * 256
+    plane11 = (rows * 384 * 4 + 255) // 256 * 256
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=7, dist_type=1))) == \
         2 * plane11 + (rows * 4 + 255) // 256 * 256 + (6 * 1 * 3 * 2 * 16 * 17 * 4 + 255) // 256 * 256
     # the same at a fractional key stride (norm terms per cell, same planes)
