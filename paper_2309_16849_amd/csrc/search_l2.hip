@@ -36,7 +36,7 @@
 // and the cell's weights, the ten terms above become ten box sums of the
 // planes over the query's in-frame patch pixels, each at the offset of its
 // term ((0|1, 0|1) for N, (0|1, 0) for R, (0, 0|1) for D, (0, 0) for X and
-// A), gathered in one pass over the (P+1) x (P+1) positions.
+// A), each four reads of the plane's summed-area table (fp64, exact).
 #include "snls_internal.h"
 
 namespace snls {
@@ -300,10 +300,61 @@ __global__ void __launch_bounds__(l2n::NT, 3) l2_norms_kernel(const float* __res
   }
 }
 
-// G of every cell for a key stride S_K != 1: one thread per (query, cell)
-// of one frame step (grid y = dt + wt), consecutive threads the cells of a
-// query; Qn by the first cell's thread of the query frame.
+// Summed-area tables of the five key pair planes, in fp64 (exact box sums
+// at any offset): S[y][x] = sum of the plane over rows < y, columns < x,
+// (H + 1) x (W + 1) per (b, t, head, plane).  First the prefix along each
+// row (one thread per row), then down each column (one thread per column).
+__global__ void __launch_bounds__(256) l2_sat_rows_kernel(const float* __restrict__ planes, Geo g,
+                                                          double* __restrict__ sat) {
+  const int y = blockIdx.x * 256 + threadIdx.x;
+  if (y >= g.H) return;
+  const long long sp = blockIdx.y;  // slab * NKP + plane
+  const long long slab = sp / NKP, m = sp - slab * NKP;
+  const float* src = planes + (slab * NPLANE + m) * g.HW + (long long)y * g.W;
+  double* dst = sat + (sp * (g.H + 1) + y + 1) * (long long)(g.W + 1);
+  double acc = 0.0;
+  dst[0] = 0.0;
+  for (int x = 0; x < g.W; ++x) {
+    acc += (double)src[x];
+    dst[x + 1] = acc;
+  }
+}
+
+__global__ void __launch_bounds__(256) l2_sat_cols_kernel(Geo g, double* __restrict__ sat) {
+  const int x = blockIdx.x * 256 + threadIdx.x;
+  if (x > g.W) return;
+  const long long sp = blockIdx.y;
+  double* col = sat + sp * (g.H + 1) * (long long)(g.W + 1) + x;
+  const long long W1 = g.W + 1;
+  double acc = 0.0;
+  col[0] = 0.0;
+  for (int y = 1; y <= g.H; ++y) {
+    acc += col[y * W1];
+    col[y * W1] = acc;
+  }
+}
+
+// Sum of one plane over rows r0..r1, columns c0..c1 (inclusive), pixels
+// outside the frame counting 0: four reads of its summed-area table.
+SNLS_DEV double sat_rect(const double* __restrict__ S, const Geo& g, int r0, int r1, int c0, int c1) {
+  r0 = max(r0, 0);
+  r1 = min(r1, g.H - 1);
+  c0 = max(c0, 0);
+  c1 = min(c1, g.W - 1);
+  if (r0 > r1 || c0 > c1) return 0.0;
+  const long long W1 = g.W + 1;
+  return (S[(r1 + 1) * W1 + c1 + 1] - S[r0 * W1 + c1 + 1]) - (S[(r1 + 1) * W1 + c0] - S[r0 * W1 + c0]);
+}
+
+// G of every cell, cell by cell (a key stride S_K != 1 gives the cells of a
+// window fractions of their own; windows above 9 exceed the per-query grids
+// of l2_norms_kernel): one thread per (query, cell) of one frame step (grid
+// y = dt + wt), consecutive threads the cells of a query; Qn by the first
+// cell's thread of the query frame.  Each of the ten terms is a box sum of
+// one pair plane over the query's in-frame patch pixels at the term's tap
+// offset: a rectangle of the plane's summed-area table.
 __global__ void __launch_bounds__(256) l2_norms_cells_kernel(const float* __restrict__ planes,
+                                                             const double* __restrict__ sat,
                                                              const float* __restrict__ flows, Geo g,
                                                              float* __restrict__ G, int pitch,
                                                              float* __restrict__ Qn) {
@@ -350,51 +401,35 @@ __global__ void __launch_bounds__(256) l2_norms_cells_kernel(const float* __rest
     const float fly = floorf(disp_h), flx = floorf(disp_w);
     const float ay = disp_h - fly, ax = disp_w - flx;
     const int y0 = h + g.lo + (int)fly, x0 = w + g.lo + (int)flx;  // tap (0, 0) of patch pixel (0, 0)
-    const float* kb = planes + (((long long)b * g.T + t2) * g.HD + hd) * NPLANE * g.HW;
-    // box sums over the in-frame patch pixels, at the offsets of the terms
-    float n00 = 0.f, n01 = 0.f, n10 = 0.f, n11 = 0.f, r0 = 0.f, r1 = 0.f, d0 = 0.f, d1 = 0.f, xs = 0.f, as = 0.f;
-    for (int a = ip0; a <= ip1 + 1; ++a) {
-      const int y = y0 + a;
-      const bool yin = y >= 0 && y < g.H;
-      // row a is patch row a for the terms at row offset 0, patch row a - 1
-      // for those at row offset 1 (and likewise for columns below)
-      const bool ra = a <= ip1, rb = a > ip0;
-      for (int c = jp0; c <= jp1 + 1; ++c) {
-        const int x = x0 + c;
-        if (!yin || x < 0 || x >= g.W) continue;  // every plane reads 0 outside the frame
-        const bool ca = c <= jp1, cb = c > jp0;
-        const float* pp = kb + (long long)y * g.W + x;
-        const float vn = pp[0];
-        n00 += ra && ca ? vn : 0.f;
-        n01 += ra && cb ? vn : 0.f;
-        n10 += rb && ca ? vn : 0.f;
-        n11 += rb && cb ? vn : 0.f;
-        if (ca) {
-          const float vr = pp[g.HW];
-          r0 += ra ? vr : 0.f;
-          r1 += rb ? vr : 0.f;
-        }
-        if (ra) {
-          const float vd = pp[2 * (long long)g.HW];
-          d0 += ca ? vd : 0.f;
-          d1 += cb ? vd : 0.f;
-          if (ca) {
-            xs += pp[3 * (long long)g.HW];
-            as += pp[4 * (long long)g.HW];
-          }
-        }
-      }
-    }
-    const float w00 = (1.f - ay) * (1.f - ax), w01 = (1.f - ay) * ax, w10 = ay * (1.f - ax), w11 = ay * ax;
-    gsum = w00 * w00 * n00 + w01 * w01 * n01 + w10 * w10 * n10 + w11 * w11 * n11 + 2.f * w00 * w01 * r0 +
-           2.f * w10 * w11 * r1 + 2.f * w00 * w10 * d0 + 2.f * w01 * w11 * d1 + 2.f * w00 * w11 * xs +
-           2.f * w01 * w10 * as;
+    const long long pst = (long long)(g.H + 1) * (g.W + 1);
+    const double* S = sat + (((long long)b * g.T + t2) * g.HD + hd) * NKP * pst;
+    const double* SN = S, *SR = S + pst, *SD = S + 2 * pst, *SX = S + 3 * pst, *SA = S + 4 * pst;
+    // patch rows a in [ip0, ip1] read rows y0 + a at row offset 0 and
+    // y0 + a + 1 at offset 1 (likewise columns)
+    const int ra0 = y0 + ip0, ra1 = y0 + ip1, ca0 = x0 + jp0, ca1 = x0 + jp1;
+    const double n00 = sat_rect(SN, g, ra0, ra1, ca0, ca1), n01 = sat_rect(SN, g, ra0, ra1, ca0 + 1, ca1 + 1);
+    const double n10 = sat_rect(SN, g, ra0 + 1, ra1 + 1, ca0, ca1);
+    const double n11 = sat_rect(SN, g, ra0 + 1, ra1 + 1, ca0 + 1, ca1 + 1);
+    const double r0 = sat_rect(SR, g, ra0, ra1, ca0, ca1), r1 = sat_rect(SR, g, ra0 + 1, ra1 + 1, ca0, ca1);
+    const double d0 = sat_rect(SD, g, ra0, ra1, ca0, ca1), d1 = sat_rect(SD, g, ra0, ra1, ca0 + 1, ca1 + 1);
+    const double xs = sat_rect(SX, g, ra0, ra1, ca0, ca1), as = sat_rect(SA, g, ra0, ra1, ca0, ca1);
+    const double w00 = (1.0 - ay) * (1.0 - ax), w01 = (1.0 - ay) * ax, w10 = ay * (1.0 - ax), w11 = ay * ax;
+    gsum = (float)(w00 * w00 * n00 + w01 * w01 * n01 + w10 * w10 * n10 + w11 * w11 * n11 + 2.0 * w00 * w01 * r0 +
+                   2.0 * w10 * w11 * r1 + 2.0 * w00 * w10 * d0 + 2.0 * w01 * w11 * d1 + 2.0 * w00 * w11 * xs +
+                   2.0 * w01 * w10 * as);
   }
   G[row * pitch + (dt + g.wt) * ncf + cell] = gsum;
 }
 
-size_t l2_planes_bytes(const Geo& g) {
+static bool l2_cells(const Geo& g) { return g.s1 != 1.0f || g.ws > l2n::WSMAX; }
+static size_t l2_plane_only_bytes(const Geo& g) {
   return ((size_t)NPLANE * g.B * g.T * g.HD * (size_t)g.HW * sizeof(float) + 255) & ~(size_t)255;
+}
+// pair planes, then (cell by cell only) their summed-area tables in fp64
+size_t l2_planes_bytes(const Geo& g) {
+  size_t b = l2_plane_only_bytes(g);
+  if (l2_cells(g)) b += ((size_t)NKP * g.B * g.T * g.HD * (size_t)(g.H + 1) * (g.W + 1) * sizeof(double) + 255) & ~(size_t)255;
+  return b;
 }
 
 snls_status launch_l2_norms(const float* q, const float* k, const float* flows, const Geo& g, float* G, int pitch,
@@ -405,13 +440,20 @@ snls_status launch_l2_norms(const float* q, const float* k, const float* flows, 
   if (ntile > 0x7fffffffLL || (long long)g.B * g.HD * g.T > 65535 || 2 * g.wt + 1 > 65535) return SNLS_ERR_UNSUPPORTED;
   const dim3 pgrid((unsigned)((g.HW + 255) / 256), (unsigned)(g.B * g.T * g.HD));
   hipLaunchKernelGGL(l2_pair_planes_kernel, pgrid, dim3(256), 0, s, q, k, g, planes);
-  if (g.s1 != 1.0f || g.ws > l2n::WSMAX) {
+  if (l2_cells(g)) {
     // per-cell fractions, or windows past the grids below: G cell by cell
+    // from the planes' summed-area tables
     const long long nth = g.rows * (long long)(g.ws * g.ws);
     const long long nblk = (nth + 255) / 256;
-    if (nblk > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
+    const long long nsp = (long long)g.B * g.T * g.HD * NKP;
+    if (nblk > 0x7fffffffLL || nsp > 65535) return SNLS_ERR_UNSUPPORTED;
+    double* sat = reinterpret_cast<double*>(reinterpret_cast<char*>(planes) + l2_plane_only_bytes(g));
+    hipLaunchKernelGGL(l2_sat_rows_kernel, dim3((unsigned)((g.H + 255) / 256), (unsigned)nsp), dim3(256), 0, s, planes,
+                       g, sat);
+    hipLaunchKernelGGL(l2_sat_cols_kernel, dim3((unsigned)((g.W + 1 + 255) / 256), (unsigned)nsp), dim3(256), 0, s, g,
+                       sat);
     dim3 cgrid((unsigned)nblk, (unsigned)(2 * g.wt + 1));
-    hipLaunchKernelGGL(l2_norms_cells_kernel, cgrid, dim3(256), 0, s, planes, flows, g, G, pitch, Qn);
+    hipLaunchKernelGGL(l2_norms_cells_kernel, cgrid, dim3(256), 0, s, planes, sat, flows, g, G, pitch, Qn);
     return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
   }
   dim3 grid((unsigned)ntile, (unsigned)(g.B * g.HD * g.T), (unsigned)(2 * g.wt + 1));

@@ -175,11 +175,13 @@ def test_search_workspace(lib):
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=7))) == rows * 384 * 4
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=5))) == 0
     plane11 = (rows * 384 * 4 + 255) // 256 * 256
+    # (norm terms cell by cell: the planes' fp64 summed-area tables follow)
+    sat = a256(5 * 1 * 3 * 2 * 17 * 18 * 8)
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(ws=11, ps=7, dist_type=1))) == \
-        2 * plane11 + (rows * 4 + 255) // 256 * 256 + (6 * 1 * 3 * 2 * 16 * 17 * 4 + 255) // 256 * 256
-    # the same at a fractional key stride (norm terms per cell, same planes)
+        2 * plane11 + (rows * 4 + 255) // 256 * 256 + (6 * 1 * 3 * 2 * 16 * 17 * 4 + 255) // 256 * 256 + sat
+    # the same at a fractional key stride (norm terms per cell)
     assert lib.snls_workspace_size(B.SNLS_OP_SEARCH, ctypes.byref(_params(dist_type=1, stride1=0.5))) == \
-        2 * plane + a256(rows * 4) + pairs
+        2 * plane + a256(rows * 4) + pairs + sat
     assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, None, BIG, None) == B.SNLS_ERR_WORKSPACE
     assert lib.snls_search(FAKE, FAKE, FAKE, ctypes.byref(prm), FAKE, FAKE, FAKE, need - 1,
                            None) == B.SNLS_ERR_WORKSPACE
