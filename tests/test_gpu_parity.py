@@ -451,6 +451,10 @@ L2_TILE_CASES = [
     (small_params(T=3, C=8, H=27, W=30, ws=15, wt=1, ps=7, k=10, dist_type=1), "smooth"),
     (small_params(T=2, C=8, H=22, W=25, ws=11, wt=1, ps=7, k=12, dist_type=1, stride1=0.5), "frac"),
     (small_params(T=2, C=8, H=19, W=22, ws=13, wt=1, ps=7, k=128, dist_type=1), "smooth"),
+    # norm terms from the summed-area tables at the frame's edges: a frame
+    # smaller than the patch, and a thin one at S_K = 1/4
+    (small_params(T=2, C=8, H=5, W=6, ws=5, wt=1, ps=7, k=6, dist_type=1, stride1=0.5), "frac"),
+    (small_params(T=3, C=4, H=9, W=40, ws=9, wt=1, ps=5, k=10, dist_type=1, stride1=0.25), "wide"),
 ]
 
 
