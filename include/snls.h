@@ -123,15 +123,18 @@ typedef struct {
  *             dists (B, HD, T, nH, nW, (2wt+1)*ws*ws), inds (..., 3)
  *   workspace device scratch of at least snls_workspace_size(SNLS_OP_SEARCH, p)
  *             bytes, 256-byte aligned; may be NULL when that size is 0.  The
- *             top-k paths for stride0 = 1, ps <= 7, ws <= 9 (inner product
- *             with stride1 <= 1, squared L2 with stride1 = 1) and for ps = 1,
- *             stride1 = 1, ws <= 15 (inner product, any stride0) score every
- *             candidate into it (4 bytes per query row and candidate) before
- *             selecting; squared L2 adds the key-norm term of every
- *             candidate, the query norm of every row, five key pair
- *             products per key pixel, frame and head and the squared norm
- *             of every query pixel per frame and head.  Its contents are not
- *             needed between calls
+ *             tiled top-k path (ps <= 7 with ws <= 9, or ps = 7 with ws <=
+ *             15; stride1 <= 1; any stride0) and the single-pixel path with
+ *             k > 32 (ps = 1, stride1 = 1, ws <= 15, inner product) score
+ *             every candidate into it (4 bytes per query row and candidate,
+ *             rows padded to 32 candidates) before selecting; squared L2
+ *             adds the key-norm term of every candidate, the query norm of
+ *             every row, five key pair products per key pixel, frame and
+ *             head, the squared norm of every query pixel per frame and head
+ *             and, where the norm terms are formed cell by cell (stride1 < 1
+ *             or ws > 9), fp64 summed-area tables of the five products.  The
+ *             fused single-pixel path (k <= 32) needs none.  Its contents
+ *             are not needed between calls
  * Errors: SNLS_ERR_INVALID_ARG for shapes/parameters out of range or NULL
  * buffers; SNLS_ERR_UNSUPPORTED for k > SNLS_MAX_K; SNLS_ERR_WORKSPACE for a
  * missing, short or misaligned workspace; SNLS_ERR_HIP on a launch failure. */
