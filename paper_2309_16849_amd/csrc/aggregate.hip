@@ -93,6 +93,54 @@ __global__ void __launch_bounds__(256) to_channels_last_kernel(const float* __re
   }
 }
 
+// The same transpose with 16-byte accesses on both sides, for C and the
+// head's channels multiples of 4 (HEAD: head-major order, each head's
+// channels of a pixel contiguous): a thread loads 4 consecutive pixels of
+// one channel (raw buffer loads at any 4-byte offset; pixels past the frame
+// read 0) and stores 4 consecutive channels of one pixel.
+template <bool HEAD>
+__global__ void __launch_bounds__(256) to_channels_last4_kernel(const float* __restrict__ v, Geo g,
+                                                                float* __restrict__ vcl) {
+  __shared__ float tileb[64][65];  // [channel][pixel]
+  const long long bt = blockIdx.z;
+  const int c0 = blockIdx.y * 64;
+  const long long p0 = (long long)blockIdx.x * 64;
+  const float* src = v + bt * g.C * g.HW;
+  float* dst = vcl + bt * g.C * g.HW;
+  const int q4 = threadIdx.x & 15, r16 = threadIdx.x >> 4;
+  // one channel plane per buffer: offsets past the frame read 0
+  for (int i = r16; i < 64; i += 16) {
+    const int c = c0 + i;
+    float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+    const long long p = p0 + 4 * q4;
+    if (c < g.C && p + 3 < g.HW) {
+      const __amdgpu_buffer_rsrc_t rs =
+          __builtin_amdgcn_make_buffer_rsrc((void*)(src + (long long)c * g.HW), (short)0, (int)(g.HW * 4), 0x00020000);
+      typedef float f32x4 __attribute__((ext_vector_type(4)));
+      const f32x4 y = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (unsigned)(p * 4), 0, 0));
+      x = make_float4(y.x, y.y, y.z, y.w);
+    } else if (c < g.C) {  // the frame's last pixels: one at a time
+      const float* sp = src + (long long)c * g.HW;
+      x.x = p < g.HW ? sp[p] : 0.f;
+      x.y = p + 1 < g.HW ? sp[p + 1] : 0.f;
+      x.z = p + 2 < g.HW ? sp[p + 2] : 0.f;
+    }
+    tileb[i][4 * q4] = x.x;
+    tileb[i][4 * q4 + 1] = x.y;
+    tileb[i][4 * q4 + 2] = x.z;
+    tileb[i][4 * q4 + 3] = x.w;
+  }
+  __syncthreads();
+  for (int j = r16; j < 64; j += 16) {
+    const long long p = p0 + j;
+    const int c = c0 + 4 * q4;
+    if (c < g.C && p < g.HW) {
+      const float4 x = make_float4(tileb[4 * q4][j], tileb[4 * q4 + 1][j], tileb[4 * q4 + 2][j], tileb[4 * q4 + 3][j]);
+      const long long o = HEAD ? ((long long)(c / g.Ch) * g.HW + p) * g.Ch + c % g.Ch : p * g.C + c;
+      *reinterpret_cast<float4*>(dst + o) = x;
+    }
+  }
+}
 
 // Merged gather.  One workgroup = 8 x 8 output pixels of one (b, t, head);
 // one wave per pixel at a time, lane = channel (CPL channels per lane).
@@ -867,7 +915,10 @@ __global__ void __launch_bounds__(256) aggregate_gather_kernel(const float* __re
 
 snls_status launch_to_channels_last(const float* x, const Geo& g, float* xcl, hipStream_t s) {
   dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
-  hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, x, g, xcl);
+  if (g.C % 4 == 0 && (long long)g.HW * 4 < (1LL << 31))
+    hipLaunchKernelGGL(to_channels_last4_kernel<false>, tgrid, dim3(256), 0, s, x, g, xcl);
+  else
+    hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, x, g, xcl);
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
 }
 
@@ -914,7 +965,10 @@ snls_status launch_aggregate(const float* v, const float* dists, const float* in
                            ((g.nW + aggp1::TW - 1) / aggp1::TW);
     if (nblk > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
     dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
-    hipLaunchKernelGGL(to_head_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
+    if (g.C % 4 == 0 && (long long)g.HW * 4 < (1LL << 31))
+      hipLaunchKernelGGL(to_channels_last4_kernel<true>, tgrid, dim3(256), 0, s, v, g, vcl);
+    else
+      hipLaunchKernelGGL(to_head_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
     hipLaunchKernelGGL(aggregate_p1_kernel, dim3((unsigned)nblk), dim3(256), aggp1::lds_bytes(g.k), s, vcl, dists,
                        inds, g, scale, out);
     return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
@@ -927,7 +981,10 @@ snls_status launch_aggregate(const float* v, const float* dists, const float* in
   if (nslot <= aggt::NSLOT && g.Ch <= 64 && (long long)g.T * g.HW * g.C < (1LL << 31) &&
       g.ps <= 11 && nq_tile <= aggt::MAXQ && nq_tile * g.k <= aggt::MAXREC) {
     dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
-    hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
+    if (g.C % 4 == 0 && (long long)g.HW * 4 < (1LL << 31))
+      hipLaunchKernelGGL(to_channels_last4_kernel<false>, tgrid, dim3(256), 0, s, v, g, vcl);
+    else
+      hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
     const int tiles_x = (g.W + aggt::TX - 1) / aggt::TX, tiles_y = (g.H + aggt::TY - 1) / aggt::TY;
     const long long nwg = (long long)tiles_x * tiles_y * g.B * g.T * g.HD;
     if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
@@ -950,7 +1007,10 @@ snls_status launch_aggregate(const float* v, const float* dists, const float* in
   }
   if (nslot <= agg::NSLOT && g.Ch <= 256 && (long long)g.T * g.HW * g.C < (1LL << 31) && g.ps <= 11) {
     dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
-    hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
+    if (g.C % 4 == 0 && (long long)g.HW * 4 < (1LL << 31))
+      hipLaunchKernelGGL(to_channels_last4_kernel<false>, tgrid, dim3(256), 0, s, v, g, vcl);
+    else
+      hipLaunchKernelGGL(to_channels_last_kernel, tgrid, dim3(256), 0, s, v, g, vcl);
     const int tiles_x = (g.W + agg::TX - 1) / agg::TX, tiles_y = (g.H + agg::TY - 1) / agg::TY;
     const long long nwg = (long long)tiles_x * tiles_y * g.B * g.T * g.HD;
     if (nwg > 0x7fffffffLL) return SNLS_ERR_UNSUPPORTED;
