@@ -176,6 +176,43 @@ __global__ void __launch_bounds__(256) from_channels_last_kernel(const float* __
   }
 }
 
+// The same with 16-byte accesses (C a multiple of 4): a thread reads 4
+// consecutive channels of one pixel and writes 4 consecutive pixels of one
+// channel (the frame's last pixels one at a time).
+__global__ void __launch_bounds__(256) from_channels_last4_kernel(const float* __restrict__ xcl, Geo g,
+                                                                  float* __restrict__ x) {
+  __shared__ float tileb[64][65];  // [pixel][channel]
+  const long long bt = blockIdx.z;
+  const int c0 = blockIdx.y * 64;
+  const long long p0 = (long long)blockIdx.x * 64;
+  const float* src = xcl + bt * g.C * g.HW;
+  float* dst = x + bt * g.C * g.HW;
+  const int q4 = threadIdx.x & 15, r16 = threadIdx.x >> 4;
+  for (int j = r16; j < 64; j += 16) {
+    const long long p = p0 + j;
+    const int c = c0 + 4 * q4;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (c < g.C && p < g.HW) v = *reinterpret_cast<const float4*>(src + p * g.C + c);
+    tileb[j][4 * q4] = v.x;
+    tileb[j][4 * q4 + 1] = v.y;
+    tileb[j][4 * q4 + 2] = v.z;
+    tileb[j][4 * q4 + 3] = v.w;
+  }
+  __syncthreads();
+  for (int i = r16; i < 64; i += 16) {
+    const int c = c0 + i;
+    const long long p = p0 + 4 * q4;
+    if (c >= g.C || p >= g.HW) continue;
+    float* dp = dst + (long long)c * g.HW + p;
+    if (p + 3 < g.HW && (((long long)c * g.HW + p) & 3) == 0) {
+      *reinterpret_cast<float4*>(dp) = make_float4(tileb[4 * q4][i], tileb[4 * q4 + 1][i], tileb[4 * q4 + 2][i],
+                                                   tileb[4 * q4 + 3][i]);
+    } else {
+      for (int e = 0; e < 4 && p + e < g.HW; ++e) dp[e] = tileb[4 * q4 + e][i];
+    }
+  }
+}
+
 __global__ void __launch_bounds__(256) backward_agg_kernel(const float* __restrict__ vcl,
                                                            const float* __restrict__ dists,
                                                            const float* __restrict__ inds,
@@ -1089,9 +1126,16 @@ snls_status launch_backward(const float* q, const float* k, const float* v, cons
   }
   if (nvid > 0) {
     dim3 tgrid((unsigned)((g.HW + 63) / 64), (unsigned)((g.C + 63) / 64), (unsigned)(g.B * g.T));
-    hipLaunchKernelGGL(from_channels_last_kernel, tgrid, dim3(256), 0, s, dqcl, g, grad_q);
-    hipLaunchKernelGGL(from_channels_last_kernel, tgrid, dim3(256), 0, s, dkcl, g, grad_k);
-    hipLaunchKernelGGL(from_channels_last_kernel, tgrid, dim3(256), 0, s, dvcl, g, grad_v);
+    const bool a16 = (((uintptr_t)grad_q | (uintptr_t)grad_k | (uintptr_t)grad_v) & 15) == 0;
+    if (g.C % 4 == 0 && a16) {
+      hipLaunchKernelGGL(from_channels_last4_kernel, tgrid, dim3(256), 0, s, dqcl, g, grad_q);
+      hipLaunchKernelGGL(from_channels_last4_kernel, tgrid, dim3(256), 0, s, dkcl, g, grad_k);
+      hipLaunchKernelGGL(from_channels_last4_kernel, tgrid, dim3(256), 0, s, dvcl, g, grad_v);
+    } else {
+      hipLaunchKernelGGL(from_channels_last_kernel, tgrid, dim3(256), 0, s, dqcl, g, grad_q);
+      hipLaunchKernelGGL(from_channels_last_kernel, tgrid, dim3(256), 0, s, dkcl, g, grad_k);
+      hipLaunchKernelGGL(from_channels_last_kernel, tgrid, dim3(256), 0, s, dvcl, g, grad_v);
+    }
   }
   return hipGetLastError() == hipSuccess ? SNLS_OK : SNLS_ERR_HIP;
 }
